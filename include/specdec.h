@@ -1,0 +1,256 @@
+/*
+ * specdec.h -- C ABI of the MI355X (gfx950) speculative-decoding hot path.
+ *
+ * One draft-and-verify iteration (the inner loop of the MemSpec runtime,
+ * Sec. 3.4, Alg. 3: "run draft d_i; verify with target model"):
+ *
+ *   for s in 0..gamma-1: specdec_draft_step(draft, draft_kv, ..., slot = s)
+ *   specdec_verify(target, target_kv, ...)      -- one target pass over gamma+1 tokens
+ *   specdec_accept(...)                         -- speculative accept / resample
+ *   specdec_kv_commit(target_kv, TARGET, ...);  specdec_kv_commit(draft_kv, DRAFT, ...)
+ *
+ * Throughput of the loop is E[A] / L_iter (Sec. 2.1, Eq. (1)); A is the number
+ * of drafted tokens the target accepts.  The verification rule (accept with
+ * probability min(1, p/q), else resample from norm(max(0, p - q)), bonus
+ * token from p_{gamma+1} when all are accepted) is the one of the
+ * speculative-decoding works the paper builds on; the paper itself runs the
+ * greedy special case (Sec. 4.1, "Runtime configuration").
+ *
+ * Conventions for every function below:
+ *  - Pointers are DEVICE pointers unless marked "host".  The caller owns every
+ *    buffer (weights, KV, workspace, outputs); the library never allocates
+ *    device memory, so calls can be captured into a HIP graph.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Calls are asynchronous on it unless documented as synchronizing.
+ *  - Argument and shape errors are returned synchronously and nothing is
+ *    launched.  Errors only a kernel can see (token id out of range, KV
+ *    capacity overflow, NaN/Inf probabilities) set a sticky device status
+ *    word (specdec_kv.state, or the `status` argument of specdec_accept);
+ *    the kernel then skips the offending writes.  Read it with
+ *    specdec_kv_read_state or specdec_device_status.
+ *  - Handles are not thread-safe; calls on one KV cache must be
+ *    stream-ordered.
+ *  - Storage types: SPECDEC_F32 (weights and KV float32) or SPECDEC_BF16
+ *    (weights and KV bfloat16).  Activations, logits and probabilities are
+ *    always float32.
+ */
+#ifndef SPECDEC_H
+#define SPECDEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define SPECDEC_API __attribute__((visibility("default")))
+#else
+#define SPECDEC_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPECDEC_OK = 0,
+  SPECDEC_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad enum */
+  SPECDEC_ERR_SHAPE = -2,       /* dimensions the kernels do not support */
+  SPECDEC_ERR_KV_CAPACITY = -3, /* the call could write past the KV capacity */
+  SPECDEC_ERR_NONFINITE = -4,   /* NaN/Inf probability or logit (device status) */
+  SPECDEC_ERR_HIP = -5,         /* a HIP runtime call failed */
+  SPECDEC_ERR_UNSUPPORTED = -6, /* valid request outside what is implemented */
+  SPECDEC_ERR_BAD_TOKEN = -7    /* token id outside [0, vocab) (device status) */
+} specdec_status;
+
+enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1 };
+enum { SPECDEC_ROLE_TARGET = 0, SPECDEC_ROLE_DRAFT = 1 };
+enum { SPECDEC_INPUT_PROBS = 0, SPECDEC_INPUT_LOGITS = 1 };
+/* Philox counter purposes (see specdec_draw_u32). */
+enum { SPECDEC_PURPOSE_DRAFT = 0, SPECDEC_PURPOSE_ACCEPT = 1, SPECDEC_PURPOSE_RESAMPLE = 2 };
+
+/* Llama-style decoder shape.  The paper's targets are LLaMA-2 7B and
+ * Qwen2.5 7B with 400M/0.5B drafts (Sec. 4.1, "Models"); a draft here is a
+ * prefix of the target's layers sharing its embedding, final norm and LM head. */
+typedef struct {
+  int32_t n_layers;   /* layers held by the weight arrays */
+  int32_t d_model;    /* d: multiple of 64 */
+  int32_t n_heads;    /* query heads h; h*hd a multiple of 64 */
+  int32_t n_kv_heads; /* kv heads; n_heads % n_kv_heads == 0 (GQA: kv head = q head / (h / h_kv)) */
+  int32_t head_dim;   /* hd: 32, 64 or 128 */
+  int32_t ffn_dim;    /* SwiGLU hidden size F: multiple of 32 */
+  int32_t vocab;      /* V: multiple of 16 */
+  float rms_eps;      /* RMSNorm epsilon */
+  float rope_base;    /* RoPE base (rotate-half pairs (j, j + hd/2), theta_j = base^(-2j/hd)) */
+  int32_t dtype;      /* SPECDEC_F32 or SPECDEC_BF16 */
+} specdec_model_desc;
+
+/* Device pointers to weights, all row-major [out, in] of the storage type.
+ * Per-layer arrays are HOST arrays of n_layers device pointers. */
+typedef struct {
+  const void* embed;      /* [V, d] */
+  const void* lm_head;    /* [V, d] (not tied to embed) */
+  const void* final_norm; /* [d] */
+  const void* const* attn_norm; /* L x [d] */
+  const void* const* wq;        /* L x [h*hd, d] */
+  const void* const* wk;        /* L x [h_kv*hd, d] */
+  const void* const* wv;        /* L x [h_kv*hd, d] */
+  const void* const* wo;        /* L x [d, h*hd] */
+  const void* const* ffn_norm;  /* L x [d] */
+  const void* const* w_gate;    /* L x [F, d] */
+  const void* const* w_up;      /* L x [F, d] */
+  const void* const* w_down;    /* L x [d, F] */
+} specdec_weights;
+
+typedef struct specdec_model specdec_model; /* opaque host handle */
+
+/* Per-model-instance KV cache and sequence state.  A POD the caller allocates
+ * (host memory); specdec_kv_init fills it.  Fields are read-only for the caller. */
+typedef struct {
+  void* data;          /* device: K and V of every layer (layout private to the library) */
+  int32_t* state;      /* device: int32 [4*batch + 4]: len[B], pending[2B], n_pending[B], status */
+  int32_t batch;       /* sequences */
+  int32_t capacity;    /* positions per sequence (multiple of 64) */
+  int32_t n_layers;    /* layers this cache serves */
+  int32_t n_kv_heads, head_dim, dtype;
+  int64_t len_upper;   /* host-side upper bound of max_b len[b] (kept by the library) */
+} specdec_kv;
+
+/* ---------------------------------------------------------------- set-up */
+
+/* Bytes of workspace a model handle needs for calls with up to `max_rows`
+ * rows (rows = batch*(gamma+1) for verify, 2*batch for the draft's first
+ * slot, batch*chunk for prefill) and contexts of up to `max_ctx` positions. */
+SPECDEC_API size_t specdec_workspace_bytes(const specdec_model_desc* desc, int32_t max_rows, int32_t max_ctx);
+
+/* Create a handle over caller-owned weights.  n_layers_used <= desc->n_layers
+ * selects a layer prefix (a draft).  `workspace` (device, >= specdec_workspace_bytes,
+ * 256-byte aligned) belongs to the handle until specdec_model_destroy; two
+ * handles may share one workspace only if their calls never overlap.
+ * Launches nothing.
+ * Errors: INVALID_ARG (nulls), SHAPE (unsupported dims), HIP. */
+SPECDEC_API specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* weights,
+                                    int32_t n_layers_used, int32_t max_rows, int32_t max_ctx,
+                                    void* workspace, size_t workspace_bytes, specdec_model** out);
+SPECDEC_API void specdec_model_destroy(specdec_model* model);
+
+/* Bytes of KV storage for `batch` sequences of `capacity` positions over the
+ * first `n_layers_used` layers of the model shape. */
+SPECDEC_API size_t specdec_kv_bytes(const specdec_model_desc* desc, int32_t n_layers_used, int32_t batch, int32_t capacity);
+/* Number of int32 entries of the KV state array (4*batch + 4). */
+SPECDEC_API int32_t specdec_kv_state_count(int32_t batch);
+
+/* Fill `kv` (host POD) over caller-owned device buffers and zero the state
+ * (all lengths 0, no pending tokens, status OK).  Asynchronous on stream. */
+SPECDEC_API specdec_status specdec_kv_init(specdec_kv* kv, const specdec_model* model, int32_t batch, int32_t capacity,
+                               void* data, size_t data_bytes, int32_t* state, void* stream);
+
+/* Install K and V rows for sequence b, layer `layer`, positions [pos0, pos0+n):
+ * k, v are device arrays [n, n_kv_heads, head_dim] of the storage type (K
+ * after RoPE, as a forward pass would have stored it).  Used to set up a
+ * resident context without prefill.  Asynchronous. */
+SPECDEC_API specdec_status specdec_kv_write_context(specdec_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t n,
+                                        const void* k, const void* v, void* stream);
+/* Copy K and V rows back out (same layout as specdec_kv_write_context). */
+SPECDEC_API specdec_status specdec_kv_read_context(const specdec_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t n,
+                                       void* k, void* v, void* stream);
+
+/* Set lengths and pending tokens from HOST arrays: len[B], pending[2B]
+ * (right-aligned: pending[2b+1] is the newest token), n_pending[B] in {1,2}.
+ * Clears the status word.  Synchronizes the stream. */
+SPECDEC_API specdec_status specdec_kv_set_state(specdec_kv* kv, const int32_t* len, const int32_t* pending,
+                                    const int32_t* n_pending, void* stream);
+/* Read lengths, pending tokens and the status word into HOST arrays (any may
+ * be NULL).  Synchronizes the stream and refreshes kv->len_upper. */
+SPECDEC_API specdec_status specdec_kv_read_state(specdec_kv* kv, int32_t* len, int32_t* pending, int32_t* n_pending,
+                                     int32_t* status, void* stream);
+
+/* Commit a prompt: run the model over tokens[b, 0..n-2] (device int32 [batch, n])
+ * in chunks, appending their K/V from position len[b], then len[b] += n-1 and
+ * the pending token becomes tokens[b, n-1].  Not on the timed path (the paper
+ * excludes prompt encoding from throughput, Sec. 4.1). */
+SPECDEC_API specdec_status specdec_prefill(const specdec_model* model, specdec_kv* kv, int32_t n, const int32_t* tokens,
+                               void* stream);
+
+/* ---------------------------------------------------------------- hot path */
+
+/* Draft single-token decode step at draft slot `slot` (0 <= slot < gamma):
+ *  slot 0 processes the cache's 1 or 2 pending tokens (2 after an iteration
+ *  that accepted every draft), slot s > 0 processes d_out[b*ld_d + s-1].
+ *  It appends their K/V speculatively (len is unchanged until commit), runs
+ *  the LM head, and proposes d_out[b*ld_d + slot]:
+ *    temperature == 0: argmax of the logits (lowest index on ties);
+ *    temperature >  0: q = softmax(logits / T) written to q_out[b, slot, :]
+ *      (q_out is [batch, gamma, V] float32) and the token drawn from q with
+ *      the fixed-point inverse-CDF sampler (see specdec_sample) using the
+ *      32-bit word rand[b] if rand != NULL, else Philox(seed, b, step,
+ *      SPECDEC_PURPOSE_DRAFT, slot).
+ *  logits_out (optional, [batch, V]) receives the proposing row's logits.
+ * Errors: INVALID_ARG, SHAPE (batch/gamma beyond the handle's max_rows),
+ * KV_CAPACITY (len_upper + 2 + gamma > capacity). */
+SPECDEC_API specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, int32_t gamma, int32_t slot,
+                                  float temperature, uint64_t seed, uint64_t step, const uint32_t* rand,
+                                  float* q_out, int32_t* d_out, int32_t ld_d, float* logits_out, void* stream);
+
+/* Target verify pass: one forward over the gamma+1 tokens
+ * [pending token, d[b*ld_d + 0 .. gamma-1]] at positions len[b] .. len[b]+gamma,
+ * causal inside the block, against the resident cache (the drafted tokens'
+ * K/V are appended speculatively).  logits_out: [batch, gamma+1, V] float32,
+ * row i = next-token logits after token i. */
+SPECDEC_API specdec_status specdec_verify(const specdec_model* target, specdec_kv* kv, int32_t gamma, const int32_t* d,
+                              int32_t ld_d, float* logits_out, void* stream);
+
+/* Accept / resample for every sequence b (one draft-and-verify decision):
+ *  p:  [batch, gamma+1, V] float32 -- target probabilities (input_kind PROBS)
+ *      or logits (input_kind LOGITS: p = softmax(logits / temperature));
+ *  q:  [batch, gamma, V] float32 draft probabilities (unused when greedy);
+ *  d:  drafted tokens d[b*ld_d + i];
+ *  rand: [batch, gamma+1] 32-bit words ([0, gamma) accept tests, [gamma] the
+ *      resample / bonus draw) or NULL => Philox(seed, b, step, purpose, index).
+ * Sampling (temperature > 0): accept d_i iff fl32(u_i * q_i(d_i)) < p_i(d_i)
+ * with u_i = (word >> 8) * 2^-24; at the first rejection emit a draw from
+ * max(0, fl32(p_i - q_i)) (from p_i if that is all zero); if all accepted emit
+ * a draw from p_{gamma+1}.  Greedy (temperature == 0): A = length of the
+ * prefix where d_i equals argmax p_i; emit argmax p_{A+1}.
+ * Outputs n_accepted[b] = A in [0, gamma], next_token[b].  NaN/Inf inputs set
+ * *status = SPECDEC_ERR_NONFINITE (device int32, sticky) and write A = -1. */
+SPECDEC_API specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
+                              const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
+                              uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
+                              int32_t* status, void* stream);
+
+/* KV commit / rollback after specdec_accept (device-side, graph friendly):
+ *  TARGET: len += A+1; pending = [next]                       (n_pending = 1)
+ *  DRAFT:  len += n_pending + min(A, gamma-1);
+ *          pending = [d_gamma, next] if A == gamma else [next]
+ * Entries at or beyond the new length are speculative and get overwritten.
+ * A < 0 (an accept error) leaves the cache untouched. */
+SPECDEC_API specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, const int32_t* n_accepted,
+                                 const int32_t* d, int32_t ld_d, const int32_t* next_token, void* stream);
+
+/* ---------------------------------------------------------------- building blocks */
+
+/* Fixed-point inverse-CDF draw for each row b of probs [batch, ld] (first
+ * `vocab` entries used): R_j = floor(r_j * 2^40) (uint64), S = sum R_j,
+ * t = floor(x * S / 2^32), out[b] = smallest j with R_0 + ... + R_j > t,
+ * where x = rand[b] if rand != NULL else Philox(seed, b, step, purpose, index).
+ * All-zero rows give out[b] = -1.  Integer sums make it independent of the
+ * reduction order, so it is bit-exact with any correct implementation. */
+SPECDEC_API specdec_status specdec_sample(int32_t batch, int32_t vocab, const float* probs, int64_t ld, const uint32_t* rand,
+                              uint64_t seed, uint64_t step, int32_t purpose, int32_t index, int32_t* out,
+                              void* stream);
+
+/* Philox4x32-10 (Salmon et al., SC'11) word 0 for each b in [0, batch):
+ * key = (seed & 0xffffffff, seed >> 32),
+ * counter = (b, step & 0xffffffff, step >> 32, (purpose << 16) | index). */
+SPECDEC_API specdec_status specdec_draw_u32(int32_t batch, uint64_t seed, uint64_t step, int32_t purpose, int32_t index,
+                                uint32_t* out, void* stream);
+
+/* Synchronize the stream and return the sticky status word of `kv` (also
+ * written to *host_out if non-NULL). */
+SPECDEC_API specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host_out);
+
+SPECDEC_API const char* specdec_status_string(specdec_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECDEC_H */

@@ -1,0 +1,563 @@
+// C ABI of the speculative-decoding hot path: argument validation, workspace
+// carving, and the launch sequence of one forward pass (verify or draft step).
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "device_common.h"
+#include "internal.h"
+#include "specdec.h"
+
+using namespace specdec;
+
+
+struct specdec_model {
+  specdec_model_desc desc;
+  int n_layers;  // layers this handle runs
+  int max_rows, max_ctx;
+  const void* embed;
+  const void* lm_head;
+  const void* final_norm;
+  std::vector<const void*> attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up, w_down;
+  // workspace carve
+  RowDesc* rows;
+  float* rope_cs;
+  float* h;
+  float* ss;
+  int ss_ld, ss_parts_max;
+  float* qkv;
+  float* qr;
+  float* o_part;
+  float* ml_part;
+  float* o;
+  float* u;
+  float* logits;
+  int chunk, n_split_max;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
+
+// Workspace layout (in order); shared by specdec_workspace_bytes and create.
+struct WsLayout {
+  size_t rows, rope, h, ss, qkv, qr, o_part, ml_part, o, u, logits, total;
+  int ss_parts, chunk, n_split;
+};
+
+WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
+  WsLayout w{};
+  const size_t R = (size_t)max_rows;
+  const int hd = d->head_dim, H = d->n_heads, G = d->n_kv_heads;
+  w.ss_parts = std::max(1, gemm_row_blocks(d->dtype, EPI_RESID, d->d_model, max_rows));
+  w.chunk = attention_chunk(hd);
+  w.n_split = (max_ctx + w.chunk - 1) / w.chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t at = off; off = align_up(off + bytes); return at; };
+  w.rows = take(R * sizeof(RowDesc));
+  w.rope = take(R * hd * 4);
+  w.h = take(R * d->d_model * 4);
+  w.ss = take((size_t)w.ss_parts * R * 4);
+  w.qkv = take(R * (H + 2 * G) * hd * 4);
+  w.qr = take(R * H * hd * 4);
+  w.o_part = take(R * H * (size_t)w.n_split * hd * 4);
+  w.ml_part = take(R * H * (size_t)w.n_split * 2 * 4);
+  w.o = take(R * H * hd * 4);
+  w.u = take(R * d->ffn_dim * 4);
+  w.logits = take(R * d->vocab * 4);
+  w.total = off;
+  return w;
+}
+
+specdec_status check_desc(const specdec_model_desc* d) {
+  if (!d) return SPECDEC_ERR_INVALID_ARG;
+  if (d->dtype != SPECDEC_F32 && d->dtype != SPECDEC_BF16) return SPECDEC_ERR_INVALID_ARG;
+  if (d->n_layers <= 0 || d->d_model <= 0 || d->n_heads <= 0 || d->n_kv_heads <= 0 || d->head_dim <= 0 ||
+      d->ffn_dim <= 0 || d->vocab <= 0 || !(d->rms_eps >= 0.f) || !(d->rope_base > 0.f))
+    return SPECDEC_ERR_INVALID_ARG;
+  if (d->d_model % 64 || d->ffn_dim % 32 || d->vocab % 16 || d->n_heads % d->n_kv_heads) return SPECDEC_ERR_SHAPE;
+  if (d->head_dim != 32 && d->head_dim != 64 && d->head_dim != 128) return SPECDEC_ERR_SHAPE;
+  if ((d->n_heads * d->head_dim) % 64 || (d->n_kv_heads * d->head_dim) % 32) return SPECDEC_ERR_SHAPE;
+  return SPECDEC_OK;
+}
+
+specdec_status hip_status(hipError_t e) { return e == hipSuccess ? SPECDEC_OK : SPECDEC_ERR_HIP; }
+
+#define SD_TRY(expr)                                   \
+  do {                                                 \
+    hipError_t _e = (expr);                            \
+    if (_e != hipSuccess) return SPECDEC_ERR_HIP;      \
+  } while (0)
+
+int32_t* kv_len(const specdec_kv* kv) { return kv->state; }
+int32_t* kv_pending(const specdec_kv* kv) { return kv->state + kv->batch; }
+int32_t* kv_npending(const specdec_kv* kv) { return kv->state + 3 * kv->batch; }
+int32_t* kv_status(const specdec_kv* kv) { return kv->state + 4 * kv->batch; }
+
+KvLayout kv_layout(const specdec_kv* kv) {
+  return KvLayout{kv->data, kv->batch, kv->capacity, kv->n_kv_heads, kv->head_dim, kv->dtype};
+}
+
+specdec_status check_kv(const specdec_model* m, const specdec_kv* kv) {
+  if (!m || !kv || !kv->data || !kv->state) return SPECDEC_ERR_INVALID_ARG;
+  if (kv->n_layers < m->n_layers || kv->n_kv_heads != m->desc.n_kv_heads || kv->head_dim != m->desc.head_dim ||
+      kv->dtype != m->desc.dtype)
+    return SPECDEC_ERR_SHAPE;
+  return SPECDEC_OK;
+}
+
+// Runs GEMM `g` over the rows [0, M) in launches of at most kMaxGemmRows rows.
+hipError_t gemm_rows(int dtype, GemmArgs g, int M, hipStream_t s) {
+  for (int m0 = 0; m0 < M; m0 += kMaxGemmRows) {
+    GemmArgs c = g;
+    c.M = std::min(kMaxGemmRows, M - m0);
+    c.x = g.x + (size_t)m0 * g.ldx;
+    c.out = g.out + (size_t)m0 * g.ldo;
+    if (g.ss_in) c.ss_in = g.ss_in + m0;
+    if (g.ss_out) c.ss_out = g.ss_out + m0;
+    hipError_t e = launch_gemm(dtype, c, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// One forward pass over M = B*rps rows described by `ra` (mode, token source),
+// writing logits [M, V] to `logits`.  ctx_bound: host upper bound of pos+1.
+specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int ctx_bound, float* logits,
+                       hipStream_t s) {
+  const specdec_model_desc& d = m->desc;
+  const int M = ra.M, dt = d.dtype;
+  const int H = d.n_heads, G = d.n_kv_heads, hd = d.head_dim;
+  if (M > m->max_rows) return SPECDEC_ERR_SHAPE;
+  ctx_bound = std::min(ctx_bound, kv->capacity);
+  const int n_split = (ctx_bound + m->chunk - 1) / m->chunk;
+  if (n_split > m->n_split_max) return SPECDEC_ERR_SHAPE;
+
+  ra.len = kv_len(kv);
+  ra.pending = kv_pending(kv);
+  ra.n_pending = kv_npending(kv);
+  ra.status = kv_status(kv);
+  ra.capacity = kv->capacity;
+  ra.vocab = d.vocab;
+  ra.d_model = d.d_model;
+  ra.head_dim = hd;
+  ra.rope_base = d.rope_base;
+  ra.embed = m->embed;
+  ra.rows = m->rows;
+  ra.rope_cs = m->rope_cs;
+  ra.h = m->h;
+  ra.ss = m->ss;
+  SD_TRY(launch_rows_embed(dt, ra, s));
+
+  GemmArgs base{};
+  base.eps = d.rms_eps;
+  base.ss_ld = m->ss_ld;
+  int n_ss = 1;
+  const int n_resid_blocks = gemm_row_blocks(dt, EPI_RESID, d.d_model, M);
+
+  AttnArgs at{};
+  at.rows = m->rows;
+  at.M = M;
+  at.rps = ra.rps;
+  at.n_heads = H;
+  at.n_kv_heads = G;
+  at.head_dim = hd;
+  at.qkv = m->qkv;
+  at.rope_cs = m->rope_cs;
+  at.qr = m->qr;
+  at.kv = kv_layout(kv);
+  at.max_ctx = ctx_bound;
+  at.chunk = m->chunk;
+  at.n_split = n_split;
+  at.o_part = m->o_part;
+  at.ml_part = m->ml_part;
+  at.o = m->o;
+  at.status = kv_status(kv);
+
+  for (int l = 0; l < m->n_layers; ++l) {
+    GemmArgs q = base;  // RMSNorm + Q|K|V projections
+    q.x = m->h; q.ldx = d.d_model; q.gain = m->attn_norm[l]; q.ss_in = m->ss; q.n_ss = n_ss;
+    q.K = d.d_model;
+    q.w[0] = m->wq[l]; q.w[1] = m->wk[l]; q.w[2] = m->wv[l];
+    q.n_seg[0] = H * hd; q.n_seg[1] = G * hd; q.n_seg[2] = G * hd;
+    q.n_rows = (H + 2 * G) * hd; q.kind = EPI_STORE; q.out = m->qkv; q.ldo = (H + 2 * G) * hd;
+    SD_TRY(gemm_rows(dt, q, M, s));
+
+    at.layer = l;
+    SD_TRY(launch_rope_append(at, s));
+    SD_TRY(launch_attention(at, s));
+
+    GemmArgs o = base;  // O projection + residual
+    o.x = m->o; o.ldx = H * hd; o.K = H * hd;
+    o.w[0] = m->wo[l]; o.n_seg[0] = d.d_model; o.n_rows = d.d_model; o.kind = EPI_RESID;
+    o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss;
+    SD_TRY(gemm_rows(dt, o, M, s));
+    n_ss = n_resid_blocks;
+
+    GemmArgs gu = base;  // RMSNorm + gate|up + SwiGLU
+    gu.x = m->h; gu.ldx = d.d_model; gu.gain = m->ffn_norm[l]; gu.ss_in = m->ss; gu.n_ss = n_ss;
+    gu.K = d.d_model;
+    gu.w[0] = m->w_gate[l]; gu.w[1] = m->w_up[l]; gu.n_seg[0] = d.ffn_dim; gu.n_seg[1] = d.ffn_dim;
+    gu.n_rows = d.ffn_dim; gu.kind = EPI_SWIGLU; gu.out = m->u; gu.ldo = d.ffn_dim;
+    SD_TRY(gemm_rows(dt, gu, M, s));
+
+    GemmArgs dn = base;  // down projection + residual
+    dn.x = m->u; dn.ldx = d.ffn_dim; dn.K = d.ffn_dim;
+    dn.w[0] = m->w_down[l]; dn.n_seg[0] = d.d_model; dn.n_rows = d.d_model; dn.kind = EPI_RESID;
+    dn.out = m->h; dn.ldo = d.d_model; dn.ss_out = m->ss;
+    SD_TRY(gemm_rows(dt, dn, M, s));
+  }
+
+  GemmArgs hd_ = base;  // final RMSNorm + LM head
+  hd_.x = m->h; hd_.ldx = d.d_model; hd_.gain = m->final_norm; hd_.ss_in = m->ss; hd_.n_ss = n_ss;
+  hd_.K = d.d_model; hd_.w[0] = m->lm_head; hd_.n_seg[0] = d.vocab; hd_.n_rows = d.vocab;
+  hd_.kind = EPI_STORE; hd_.out = logits; hd_.ldo = d.vocab;
+  SD_TRY(gemm_rows(dt, hd_, M, s));
+  return SPECDEC_OK;
+}
+
+__global__ void prefill_finish_kernel(int B, int n, const int32_t* tokens, int32_t* len, int32_t* pending,
+                                      int32_t* n_pending) {
+  for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    len[b] += n - 1;
+    pending[2 * b] = 0;
+    pending[2 * b + 1] = tokens[(size_t)b * n + n - 1];
+    n_pending[b] = 1;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t specdec_workspace_bytes(const specdec_model_desc* desc, int32_t max_rows, int32_t max_ctx) {
+  if (check_desc(desc) != SPECDEC_OK || max_rows <= 0 || max_ctx <= 0) return 0;
+  return ws_layout(desc, max_rows, max_ctx).total;
+}
+
+specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
+                                    int32_t max_rows, int32_t max_ctx, void* workspace, size_t workspace_bytes,
+                                    specdec_model** out) {
+  if (!out) return SPECDEC_ERR_INVALID_ARG;
+  *out = nullptr;
+  specdec_status st = check_desc(desc);
+  if (st != SPECDEC_OK) return st;
+  if (!w || !workspace || max_rows <= 0 || max_ctx <= 0) return SPECDEC_ERR_INVALID_ARG;
+  if (n_layers_used <= 0 || n_layers_used > desc->n_layers) return SPECDEC_ERR_INVALID_ARG;
+  if ((uintptr_t)workspace % kAlign) return SPECDEC_ERR_INVALID_ARG;
+  const WsLayout L = ws_layout(desc, max_rows, max_ctx);
+  if (workspace_bytes < L.total) return SPECDEC_ERR_INVALID_ARG;
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo ||
+      !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return SPECDEC_ERR_INVALID_ARG;
+  for (int l = 0; l < n_layers_used; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->ffn_norm[l] || !w->w_gate[l] ||
+        !w->w_up[l] || !w->w_down[l])
+      return SPECDEC_ERR_INVALID_ARG;
+
+  specdec_model* m = new specdec_model();
+  m->desc = *desc;
+  m->n_layers = n_layers_used;
+  m->max_rows = max_rows;
+  m->max_ctx = max_ctx;
+  m->embed = w->embed;
+  m->lm_head = w->lm_head;
+  m->final_norm = w->final_norm;
+  m->attn_norm.assign(w->attn_norm, w->attn_norm + n_layers_used);
+  m->wq.assign(w->wq, w->wq + n_layers_used);
+  m->wk.assign(w->wk, w->wk + n_layers_used);
+  m->wv.assign(w->wv, w->wv + n_layers_used);
+  m->wo.assign(w->wo, w->wo + n_layers_used);
+  m->ffn_norm.assign(w->ffn_norm, w->ffn_norm + n_layers_used);
+  m->w_gate.assign(w->w_gate, w->w_gate + n_layers_used);
+  m->w_up.assign(w->w_up, w->w_up + n_layers_used);
+  m->w_down.assign(w->w_down, w->w_down + n_layers_used);
+  char* base = (char*)workspace;
+  m->rows = (RowDesc*)(base + L.rows);
+  m->rope_cs = (float*)(base + L.rope);
+  m->h = (float*)(base + L.h);
+  m->ss = (float*)(base + L.ss);
+  m->ss_ld = max_rows;
+  m->ss_parts_max = L.ss_parts;
+  m->qkv = (float*)(base + L.qkv);
+  m->qr = (float*)(base + L.qr);
+  m->o_part = (float*)(base + L.o_part);
+  m->ml_part = (float*)(base + L.ml_part);
+  m->o = (float*)(base + L.o);
+  m->u = (float*)(base + L.u);
+  m->logits = (float*)(base + L.logits);
+  m->chunk = L.chunk;
+  m->n_split_max = L.n_split;
+  *out = m;
+  return SPECDEC_OK;
+}
+
+void specdec_model_destroy(specdec_model* model) { delete model; }
+
+size_t specdec_kv_bytes(const specdec_model_desc* desc, int32_t n_layers_used, int32_t batch, int32_t capacity) {
+  if (check_desc(desc) != SPECDEC_OK || n_layers_used <= 0 || batch <= 0 || capacity <= 0) return 0;
+  return (size_t)n_layers_used * batch * desc->n_kv_heads * 2 * (size_t)capacity * desc->head_dim *
+         elem_bytes(desc->dtype);
+}
+
+int32_t specdec_kv_state_count(int32_t batch) { return batch > 0 ? 4 * batch + 4 : 0; }
+
+specdec_status specdec_kv_init(specdec_kv* kv, const specdec_model* model, int32_t batch, int32_t capacity,
+                               void* data, size_t data_bytes, int32_t* state, void* stream) {
+  if (!kv || !model || !data || !state || batch <= 0 || capacity <= 0) return SPECDEC_ERR_INVALID_ARG;
+  if (capacity % 64) return SPECDEC_ERR_SHAPE;
+  if (data_bytes < specdec_kv_bytes(&model->desc, model->n_layers, batch, capacity)) return SPECDEC_ERR_INVALID_ARG;
+  kv->data = data;
+  kv->state = state;
+  kv->batch = batch;
+  kv->capacity = capacity;
+  kv->n_layers = model->n_layers;
+  kv->n_kv_heads = model->desc.n_kv_heads;
+  kv->head_dim = model->desc.head_dim;
+  kv->dtype = model->desc.dtype;
+  kv->len_upper = 0;
+  return hip_status(hipMemsetAsync(state, 0, sizeof(int32_t) * specdec_kv_state_count(batch), (hipStream_t)stream));
+}
+
+specdec_status specdec_kv_write_context(specdec_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t n,
+                                        const void* k, const void* v, void* stream) {
+  if (!kv || !kv->data || !k || !v || layer < 0 || layer >= kv->n_layers || b < 0 || b >= kv->batch || pos0 < 0 ||
+      n < 0)
+    return SPECDEC_ERR_INVALID_ARG;
+  if (pos0 + n > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
+  return hip_status(launch_kv_copy(kv_layout(kv), layer, b, pos0, n, k, v, nullptr, nullptr, (hipStream_t)stream));
+}
+
+specdec_status specdec_kv_read_context(const specdec_kv* kv, int32_t layer, int32_t b, int32_t pos0, int32_t n,
+                                       void* k, void* v, void* stream) {
+  if (!kv || !kv->data || !k || !v || layer < 0 || layer >= kv->n_layers || b < 0 || b >= kv->batch || pos0 < 0 ||
+      n < 0)
+    return SPECDEC_ERR_INVALID_ARG;
+  if (pos0 + n > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
+  return hip_status(launch_kv_copy(kv_layout(kv), layer, b, pos0, n, nullptr, nullptr, k, v, (hipStream_t)stream));
+}
+
+specdec_status specdec_kv_set_state(specdec_kv* kv, const int32_t* len, const int32_t* pending,
+                                    const int32_t* n_pending, void* stream) {
+  if (!kv || !kv->state || !len || !pending || !n_pending) return SPECDEC_ERR_INVALID_ARG;
+  const int B = kv->batch;
+  std::vector<int32_t> host(specdec_kv_state_count(B), 0);
+  int64_t mx = 0;
+  for (int b = 0; b < B; ++b) {
+    if (len[b] < 0 || len[b] > kv->capacity || n_pending[b] < 1 || n_pending[b] > 2) return SPECDEC_ERR_INVALID_ARG;
+    host[b] = len[b];
+    host[B + 2 * b] = pending[2 * b];
+    host[B + 2 * b + 1] = pending[2 * b + 1];
+    host[3 * B + b] = n_pending[b];
+    mx = std::max<int64_t>(mx, len[b]);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  SD_TRY(hipMemcpyAsync(kv->state, host.data(), host.size() * 4, hipMemcpyHostToDevice, s));
+  SD_TRY(hipStreamSynchronize(s));
+  kv->len_upper = mx;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_kv_read_state(specdec_kv* kv, int32_t* len, int32_t* pending, int32_t* n_pending,
+                                     int32_t* status, void* stream) {
+  if (!kv || !kv->state) return SPECDEC_ERR_INVALID_ARG;
+  const int B = kv->batch;
+  std::vector<int32_t> host(specdec_kv_state_count(B), 0);
+  hipStream_t s = (hipStream_t)stream;
+  SD_TRY(hipMemcpyAsync(host.data(), kv->state, host.size() * 4, hipMemcpyDeviceToHost, s));
+  SD_TRY(hipStreamSynchronize(s));
+  int64_t mx = 0;
+  for (int b = 0; b < B; ++b) {
+    if (len) len[b] = host[b];
+    if (pending) { pending[2 * b] = host[B + 2 * b]; pending[2 * b + 1] = host[B + 2 * b + 1]; }
+    if (n_pending) n_pending[b] = host[3 * B + b];
+    mx = std::max<int64_t>(mx, host[b]);
+  }
+  if (status) *status = host[4 * B];
+  kv->len_upper = mx;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_prefill(const specdec_model* model, specdec_kv* kv, int32_t n, const int32_t* tokens,
+                               void* stream) {
+  specdec_status st = check_kv(model, kv);
+  if (st != SPECDEC_OK) return st;
+  if (!tokens || n < 1) return SPECDEC_ERR_INVALID_ARG;
+  const int B = kv->batch;
+  if (kv->len_upper + n - 1 > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
+  hipStream_t s = (hipStream_t)stream;
+  const int C = std::max(1, std::min(model->max_rows / B, 64));
+  if (model->max_rows < B) return SPECDEC_ERR_SHAPE;
+  for (int c0 = 0; c0 < n - 1; c0 += C) {
+    const int rps = std::min(C, n - 1 - c0);
+    RowsArgs ra{};
+    ra.mode = ROWS_PREFILL;
+    ra.M = B * rps;
+    ra.rps = rps;
+    ra.tok_src = tokens;
+    ra.ld_tok = n;
+    ra.c0 = c0;
+    st = forward(model, kv, ra, (int)std::min<int64_t>(kv->len_upper + c0 + rps, kv->capacity), model->logits, s);
+    if (st != SPECDEC_OK) return st;
+  }
+  hipLaunchKernelGGL(prefill_finish_kernel, dim3(1), dim3(64), 0, s, B, n, tokens, kv_len(kv), kv_pending(kv),
+                     kv_npending(kv));
+  SD_TRY(hipGetLastError());
+  kv->len_upper += n - 1;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, int32_t gamma, int32_t slot,
+                                  float temperature, uint64_t seed, uint64_t step, const uint32_t* rand,
+                                  float* q_out, int32_t* d_out, int32_t ld_d, float* logits_out, void* stream) {
+  specdec_status st = check_kv(draft, kv);
+  if (st != SPECDEC_OK) return st;
+  if (!d_out || gamma < 1 || slot < 0 || slot >= gamma || ld_d < gamma || !(temperature >= 0.f))
+    return SPECDEC_ERR_INVALID_ARG;
+  if (temperature > 0.f && !q_out) return SPECDEC_ERR_INVALID_ARG;
+  const int B = kv->batch;
+  if (kv->len_upper + slot + 2 > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
+  hipStream_t s = (hipStream_t)stream;
+  RowsArgs ra{};
+  if (slot == 0) {
+    ra.mode = ROWS_DRAFT_FIRST;
+    ra.rps = 2;
+  } else {
+    ra.mode = ROWS_DRAFT_NEXT;
+    ra.rps = 1;
+    ra.tok_src = d_out;
+    ra.ld_tok = ld_d;
+    ra.slot = slot;
+  }
+  ra.M = B * ra.rps;
+  if (ra.M > draft->max_rows) return SPECDEC_ERR_SHAPE;
+  st = forward(draft, kv, ra, (int)(kv->len_upper + slot + 2), draft->logits, s);
+  if (st != SPECDEC_OK) return st;
+  DraftFinishArgs f{};
+  f.B = B;
+  f.rps = ra.rps;
+  f.V = draft->desc.vocab;
+  f.logits = draft->logits;
+  f.temperature = temperature;
+  f.seed = seed;
+  f.step = step;
+  f.rand = rand;
+  f.slot = slot;
+  f.gamma = gamma;
+  f.q_out = q_out;
+  f.d_out = d_out;
+  f.ld_d = ld_d;
+  f.logits_out = logits_out;
+  f.status = kv_status(kv);
+  return hip_status(launch_draft_finish(f, s));
+}
+
+specdec_status specdec_verify(const specdec_model* target, specdec_kv* kv, int32_t gamma, const int32_t* d,
+                              int32_t ld_d, float* logits_out, void* stream) {
+  specdec_status st = check_kv(target, kv);
+  if (st != SPECDEC_OK) return st;
+  if (!logits_out || gamma < 0 || (gamma > 0 && (!d || ld_d < gamma))) return SPECDEC_ERR_INVALID_ARG;
+  const int B = kv->batch;
+  if (kv->len_upper + gamma + 1 > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
+  RowsArgs ra{};
+  ra.mode = ROWS_VERIFY;
+  ra.rps = gamma + 1;
+  ra.M = B * ra.rps;
+  ra.tok_src = d;
+  ra.ld_tok = ld_d;
+  if (ra.M > target->max_rows) return SPECDEC_ERR_SHAPE;
+  return forward(target, kv, ra, (int)(kv->len_upper + gamma + 1), logits_out, (hipStream_t)stream);
+}
+
+specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
+                              const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
+                              uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
+                              int32_t* status, void* stream) {
+  if (batch <= 0 || gamma < 0 || vocab <= 0 || !p || !n_accepted || !next_token || !(temperature >= 0.f))
+    return SPECDEC_ERR_INVALID_ARG;
+  if (input_kind != SPECDEC_INPUT_PROBS && input_kind != SPECDEC_INPUT_LOGITS) return SPECDEC_ERR_INVALID_ARG;
+  if (gamma > 0 && (!d || ld_d < gamma)) return SPECDEC_ERR_INVALID_ARG;
+  if (temperature > 0.f && gamma > 0 && !q) return SPECDEC_ERR_INVALID_ARG;
+  if (gamma > 31) return SPECDEC_ERR_UNSUPPORTED;
+  AcceptArgs a{};
+  a.B = batch;
+  a.gamma = gamma;
+  a.V = vocab;
+  a.input_kind = input_kind;
+  a.temperature = temperature;
+  a.p = p;
+  a.q = q;
+  a.d = d;
+  a.ld_d = ld_d;
+  a.rand = rand;
+  a.seed = seed;
+  a.step = step;
+  a.n_accepted = n_accepted;
+  a.next_token = next_token;
+  a.status = status;
+  return hip_status(launch_accept(a, (hipStream_t)stream));
+}
+
+specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, const int32_t* n_accepted,
+                                 const int32_t* d, int32_t ld_d, const int32_t* next_token, void* stream) {
+  if (!kv || !kv->state || !n_accepted || !next_token || gamma < 1) return SPECDEC_ERR_INVALID_ARG;
+  if (role != SPECDEC_ROLE_TARGET && role != SPECDEC_ROLE_DRAFT) return SPECDEC_ERR_INVALID_ARG;
+  if (role == SPECDEC_ROLE_DRAFT && (!d || ld_d < gamma)) return SPECDEC_ERR_INVALID_ARG;
+  CommitArgs c{};
+  c.B = kv->batch;
+  c.gamma = gamma;
+  c.role = role;
+  c.len = kv_len(kv);
+  c.pending = kv_pending(kv);
+  c.n_pending = kv_npending(kv);
+  c.n_accepted = n_accepted;
+  c.d = d;
+  c.ld_d = ld_d;
+  c.next_token = next_token;
+  specdec_status st = hip_status(launch_commit(c, (hipStream_t)stream));
+  if (st == SPECDEC_OK) kv->len_upper += gamma + 1;
+  return st;
+}
+
+specdec_status specdec_sample(int32_t batch, int32_t vocab, const float* probs, int64_t ld, const uint32_t* rand,
+                              uint64_t seed, uint64_t step, int32_t purpose, int32_t index, int32_t* out,
+                              void* stream) {
+  if (batch <= 0 || vocab <= 0 || !probs || !out || ld < vocab) return SPECDEC_ERR_INVALID_ARG;
+  return hip_status(launch_sample(batch, vocab, probs, ld, rand, seed, step, purpose, index, out, (hipStream_t)stream));
+}
+
+specdec_status specdec_draw_u32(int32_t batch, uint64_t seed, uint64_t step, int32_t purpose, int32_t index,
+                                uint32_t* out, void* stream) {
+  if (batch <= 0 || !out || purpose < 0 || purpose > 0xffff || index < 0 || index > 0xffff)
+    return SPECDEC_ERR_INVALID_ARG;
+  return hip_status(launch_draw(batch, seed, step, purpose, index, out, (hipStream_t)stream));
+}
+
+specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host_out) {
+  if (!kv || !kv->state) return SPECDEC_ERR_INVALID_ARG;
+  int32_t v = 0;
+  hipStream_t s = (hipStream_t)stream;
+  SD_TRY(hipMemcpyAsync(&v, kv_status(kv), 4, hipMemcpyDeviceToHost, s));
+  SD_TRY(hipStreamSynchronize(s));
+  if (host_out) *host_out = v;
+  return (specdec_status)v;
+}
+
+const char* specdec_status_string(specdec_status s) {
+  switch (s) {
+    case SPECDEC_OK: return "ok";
+    case SPECDEC_ERR_INVALID_ARG: return "invalid argument";
+    case SPECDEC_ERR_SHAPE: return "unsupported shape";
+    case SPECDEC_ERR_KV_CAPACITY: return "KV capacity exceeded";
+    case SPECDEC_ERR_NONFINITE: return "non-finite probability or logit";
+    case SPECDEC_ERR_HIP: return "HIP runtime error";
+    case SPECDEC_ERR_UNSUPPORTED: return "unsupported request";
+    case SPECDEC_ERR_BAD_TOKEN: return "token id out of range";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

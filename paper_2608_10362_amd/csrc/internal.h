@@ -1,0 +1,138 @@
+// Host-side interfaces between the C ABI (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "specdec.h"
+#include "device_common.h"
+
+namespace specdec {
+
+// ------------------------------------------------------------------ GEMM
+// y = (x (.) gain) W^T, optional per-row scale s_m = 1/sqrt(mean_k h_mk^2 + eps)
+// taken from partial sums of squares, W bf16 or f32 row-major [N, K] split in
+// up to three row segments (Wq|Wk|Wv, or gate|up for SwiGLU).
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+constexpr int kMaxGemmRows = 64;  // rows of x per GEMM launch (callers split larger M)
+
+struct GemmArgs {
+  const float* x;      // [M, ldx]
+  int ldx;
+  const void* gain;    // [K] storage type, or null
+  const float* ss_in;  // [n_ss, ss_ld] partial sums of squares of x rows, or null (no row scale)
+  int n_ss, ss_ld;
+  float eps;
+  int M, K;
+  const void* w[3];
+  int n_seg[3];
+  int n_rows;          // total rows over segments (STORE/RESID); F for SWIGLU
+  int kind;
+  float* out;          // STORE: [M, ldo] ; SWIGLU: [M, ldo] ; RESID: residual [M, ldo] updated in place
+  int ldo;
+  float* ss_out;       // RESID: [n_blocks, ss_ld] sums of squares of the new residual rows
+};
+// Number of row blocks the launcher uses for this GEMM (for ss partial counts).
+int gemm_row_blocks(int dtype, int kind, int n_rows, int M);
+hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------------ rows / embedding
+enum RowMode { ROWS_VERIFY = 0, ROWS_DRAFT_FIRST = 1, ROWS_DRAFT_NEXT = 2, ROWS_PREFILL = 3 };
+struct RowsArgs {
+  int mode, M, rps;       // rows, rows per sequence
+  const int32_t* len;     // [B]
+  const int32_t* pending; // [2B]
+  const int32_t* n_pending;
+  int32_t* status;
+  const int32_t* tok_src; // VERIFY/DRAFT_NEXT: drafts (ld_tok); PREFILL: tokens [B, ld_tok]
+  int ld_tok;
+  int slot;               // DRAFT_NEXT
+  int c0;                 // PREFILL: first token index of this chunk
+  int capacity, vocab, d_model, head_dim;
+  double rope_base;
+  const void* embed;      // [V, d] storage type
+  RowDesc* rows;          // out [M]
+  float* rope_cs;         // out [M, head_dim]: cos j<hd/2 then sin
+  float* h;               // out [M, d]
+  float* ss;              // out [M] sum of squares of h rows
+};
+hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------------ attention
+struct KvLayout {
+  void* data;
+  int batch, capacity, n_kv_heads, head_dim, dtype;
+  size_t layer_elems() const { return (size_t)batch * n_kv_heads * 2 * (size_t)capacity * head_dim; }
+};
+struct AttnArgs {
+  const RowDesc* rows;
+  int M, rps, n_heads, n_kv_heads, head_dim;
+  const float* qkv;      // [M, (h + 2 h_kv) hd] pre-RoPE projections
+  const float* rope_cs;  // [M, hd]
+  float* qr;             // [M, h hd] RoPE'd queries (workspace)
+  KvLayout kv;
+  int layer;
+  int max_ctx;           // host upper bound of (pos + 1) over rows
+  int chunk;             // keys per split
+  int n_split;           // splits = ceil(max_ctx / chunk)
+  float* o_part;         // [M, h, n_split, hd]
+  float* ml_part;        // [M, h, n_split, 2]
+  float* o;              // [M, h hd]
+  int32_t* status;
+};
+int attention_chunk(int head_dim);  // keys per split of the attention kernel
+hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------------ sampling / bookkeeping
+struct DraftFinishArgs {
+  int B, rps, V;
+  const float* logits;   // [M, V]
+  float temperature;
+  uint64_t seed, step;
+  const uint32_t* rand;  // [B] or null
+  int slot, gamma;
+  float* q_out;          // [B, gamma, V] or null
+  int32_t* d_out;
+  int ld_d;
+  float* logits_out;     // [B, V] or null
+  int32_t* status;
+};
+hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s);
+
+struct AcceptArgs {
+  int B, gamma, V, input_kind;
+  float temperature;
+  const float* p;
+  const float* q;
+  const int32_t* d;
+  int ld_d;
+  const uint32_t* rand;
+  uint64_t seed, step;
+  int32_t* n_accepted;
+  int32_t* next_token;
+  int32_t* status;
+};
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+
+hipError_t launch_sample(int B, int V, const float* probs, int64_t ld, const uint32_t* rand, uint64_t seed,
+                         uint64_t step, int purpose, int index, int32_t* out, hipStream_t s);
+hipError_t launch_draw(int B, uint64_t seed, uint64_t step, int purpose, int index, uint32_t* out, hipStream_t s);
+
+struct CommitArgs {
+  int B, gamma, role;
+  int32_t* len;
+  int32_t* pending;
+  int32_t* n_pending;
+  const int32_t* n_accepted;
+  const int32_t* d;
+  int ld_d;
+  const int32_t* next_token;
+};
+hipError_t launch_commit(const CommitArgs& a, hipStream_t s);
+
+hipError_t launch_kv_copy(const KvLayout& kv, int layer, int b, int pos0, int n, const void* k, const void* v,
+                          void* k_out, void* v_out, hipStream_t s);
+
+}  // namespace specdec

@@ -1,0 +1,99 @@
+"""The C-ABI library loads, exports what include/specdec.h declares, and
+validates arguments on the host (no GPU needed: nothing here launches)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_10362_amd import binding, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2608_10362_amd import build
+        build.build()
+    return binding.lib()
+
+
+def _declared():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            txt = open(os.path.join(ROOT, "include", fn)).read()
+            names |= set(re.findall(r"SPECDEC_API[^;(]*?\b(specdec_\w+)\s*\(", txt))
+    return sorted(names)
+
+
+def test_header_declares_the_four_hot_path_calls():
+    names = _declared()
+    for n in ("specdec_draft_step", "specdec_verify", "specdec_accept", "specdec_kv_commit"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 19
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(binding._SIGS), "binding signatures out of sync with the header"
+
+
+def test_status_strings(lib):
+    for code, text in binding.STATUS.items():
+        assert binding.specdec_status_string(code) == text
+
+
+def test_sizes_and_shape_validation(lib):
+    d = binding.make_desc(synth.LLAMA_7B)
+    ws = lib.specdec_workspace_bytes(ctypes.byref(d), 5, 4096)
+    assert ws > 0 and ws % 256 == 0
+    assert lib.specdec_kv_bytes(ctypes.byref(d), 32, 1, 2048) == 32 * 32 * 2 * 2048 * 128 * 2
+    assert lib.specdec_kv_state_count(16) == 68
+    bad = binding.make_desc(synth.LLAMA_7B)
+    bad.head_dim = 96
+    assert lib.specdec_workspace_bytes(ctypes.byref(bad), 5, 4096) == 0
+    bad = binding.make_desc(synth.LLAMA_7B)
+    bad.n_kv_heads = 5
+    assert lib.specdec_workspace_bytes(ctypes.byref(bad), 5, 4096) == 0
+
+
+def test_model_create_argument_errors(lib):
+    d = binding.make_desc(synth.TINY)
+    h = ctypes.c_void_p()
+    w = binding.Weights()
+    fake = ctypes.c_void_p(256)  # never dereferenced: creation fails before any use
+    # null weights struct
+    assert lib.specdec_model_create(ctypes.byref(d), None, 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    # null per-layer arrays
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    # too many layers
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 3, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    # unsupported shape
+    bad = binding.make_desc(synth.TINY)
+    bad.d_model = 100
+    assert lib.specdec_model_create(ctypes.byref(bad), ctypes.byref(w), 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -2
+    # workspace too small
+    arr = (ctypes.c_void_p * 2)(256, 256)
+    pp = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    w2 = binding.Weights(256, 256, 256, *([pp] * 9))
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w2), 1, 8, 128, fake, 16, ctypes.byref(h)) == -1
+    assert not h.value
+
+
+def test_call_argument_errors_before_any_launch(lib):
+    kv = binding.KV()
+    # null handles / buffers are rejected synchronously
+    assert lib.specdec_verify(None, ctypes.byref(kv), 4, None, 4, None, None) == -1
+    assert lib.specdec_draft_step(None, ctypes.byref(kv), 4, 0, 1.0, 0, 0, None, None, None, 4, None, None) == -1
+    assert lib.specdec_accept(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, None) == -1
+    assert lib.specdec_accept(1, 4, 100, 7, 1.0, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
+                              4, None, 0, 0, ctypes.c_void_p(256), ctypes.c_void_p(256), None, None) == -1
+    assert lib.specdec_accept(1, 40, 100, 0, 1.0, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
+                              40, None, 0, 0, ctypes.c_void_p(256), ctypes.c_void_p(256), None, None) == -6
+    assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1
+    assert lib.specdec_sample(1, 10, None, 10, None, 0, 0, 0, 0, None, None) == -1
+    assert lib.specdec_draw_u32(1, 0, 0, 0x10000, 0, ctypes.c_void_p(256), None) == -1

@@ -1,0 +1,228 @@
+"""GPU parity of the forward passes (verify and draft step) against the oracle.
+
+Logits must agree within max-abs 1e-4 (float32 model) / 2e-2 (bf16 model),
+under teacher forcing: both sides get the same weights, resident context and
+drafted tokens.
+"""
+import numpy as np
+import pytest
+
+from oracle import model as om
+from oracle import sampling
+from oracle.specdec import greedy_decode
+from paper_2608_10362_amd import binding, synth
+from tests.gpu_util import f32, i32, install_context, log, oracle_caches, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-4
+TOL_BF16 = 2e-2
+
+
+# ---------------------------------------------------------------- tiny float32 model
+@pytest.fixture(scope="module")
+def tiny():
+    torch_cuda()
+    shape = synth.TINY
+    W = synth.make_weights(shape)
+    dw = binding.DeviceWeights(shape, W)
+    target = binding.Model(dw, 2, max_rows=64, max_ctx=512)
+    draft = binding.Model(dw, 1, max_rows=64, max_ctx=512)
+    return shape, W, target, draft
+
+
+def test_tiny_prefill_and_verify(tiny):
+    torch = torch_cuda()
+    shape, W, target, _ = tiny
+    B, g = 3, 4
+    prompts = synth.make_prompt(64, shape.vocab, batch=B)
+    drafts = synth.make_prompt(g, shape.vocab, batch=B, seed=77)
+    kv = binding.KVCache(target, B, 256)
+    binding.specdec_prefill(target, kv, i32(prompts))
+    st = kv.read_state()
+    assert (st["len"] == 63).all() and (st["pending"][:, 1] == prompts[:, -1]).all() and st["status"] == 0
+    logits = torch.empty((B, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv, g, i32(drafts), g, logits)
+    got = logits.cpu().numpy()
+    m = om.Model(shape, W)
+    worst = 0.0
+    for b in range(B):
+        c = om.KVCache(shape, 2, 256)
+        m.prefill(prompts[b, :-1], c)
+        ref = m.forward_block([prompts[b, -1]] + list(drafts[b]), c.length, c)
+        err = float(np.abs(got[b] - ref).max())
+        worst = max(worst, err)
+        for l in range(2):
+            k, v = kv.read_context(l, b, 0, 68)
+            assert np.abs(k.cpu().numpy() - c.k[l][:68]).max() < TOL_F32
+            assert np.abs(v.cpu().numpy() - c.v[l][:68]).max() < TOL_F32
+    log(f"tiny verify max-abs logit error {worst:.3g}")
+    assert worst < TOL_F32
+
+
+def test_tiny_draft_steps(tiny):
+    torch = torch_cuda()
+    shape, W, _, draft = tiny
+    g, T, seed, step = 4, 1.0, 2, 9
+    prompt = synth.make_prompt(40, shape.vocab)
+    kv = binding.KVCache(draft, 1, 256)
+    binding.specdec_prefill(draft, kv, i32(prompt))
+    m = om.Model(shape, W, n_layers=1)
+    c = om.KVCache(shape, 1, 256)
+    m.prefill(prompt[0, :-1], c)
+    for n_pending in (1, 2):
+        if n_pending == 2:  # the draft is one position behind after an all-accepted iteration
+            kv.set_state([38], [[prompt[0, -2], prompt[0, -1]]], [2])
+            pend, start = [prompt[0, -2], prompt[0, -1]], 38
+        else:
+            kv.set_state([39], [[0, prompt[0, -1]]], [1])
+            pend, start = [prompt[0, -1]], 39
+        c2 = c.copy()
+        d = torch.zeros((1, g), dtype=torch.int32, device="cuda")
+        q = torch.zeros((1, g, shape.vocab), dtype=torch.float32, device="cuda")
+        lo = torch.zeros((1, shape.vocab), dtype=torch.float32, device="cuda")
+        mismatched = 0
+        for s in range(g):
+            binding.specdec_draft_step(draft, kv, g, s, T, seed, step, None, q, d, g, lo)
+            if s == 0:
+                ref = m.forward_block(pend, start, c2)[-1]
+            else:
+                ref = m.decode_step(int(d[0, s - 1].item()), start + len(pend) + s - 1, c2)
+            err = float(np.abs(lo.cpu().numpy()[0] - ref).max())
+            q_ref = sampling.softmax(ref, T)
+            qerr = float(np.abs(q.cpu().numpy()[0, s] - q_ref).max())
+            tok_ref = sampling.draft_sample_philox(q_ref.astype(np.float32), seed, 0, step, s)
+            mismatched += int(d[0, s].item()) != tok_ref
+            log(f"draft n_pending={n_pending} slot={s} logit err {err:.3g} q err {qerr:.3g}")
+            assert err < TOL_F32 and qerr < 1e-5
+        assert mismatched == 0
+
+
+def test_tiny_greedy_specdec_equals_oracle_greedy_decode(tiny):
+    torch = torch_cuda()
+    shape, W, target, draft = tiny
+    g, n_new = 4, 32
+    prompt = synth.make_prompt(64, shape.vocab)
+    ref = greedy_decode(om.Model(shape, W), prompt[0], n_new, capacity=256)
+    kv_t = binding.KVCache(target, 1, 256)
+    kv_d = binding.KVCache(draft, 1, 256)
+    binding.specdec_prefill(target, kv_t, i32(prompt))
+    binding.specdec_prefill(draft, kv_d, i32(prompt))
+    sd = binding.SpecDecoder(target, draft, kv_t, kv_d, g, 0.0, seed=2)
+    out, step = [], 0
+    while len(out) < n_new:
+        sd.step(step)
+        A = int(sd.n_acc[0].item())
+        out += [int(x) for x in sd.d[0, :A].cpu().numpy()] + [int(sd.next[0].item())]
+        step += 1
+    log(f"greedy SD: {step} iterations for {len(out)} tokens")
+    assert out[:n_new] == ref
+    st_t, st_d = kv_t.read_state(), kv_d.read_state()
+    assert st_t["len"][0] == 63 + len(out) and st_t["status"] == 0
+    assert st_d["len"][0] + st_d["n_pending"][0] == st_t["len"][0] + 1
+
+
+def test_tiny_verify_equals_sequential_steps(tiny):
+    torch = torch_cuda()
+    shape, W, target, _ = tiny
+    g = 4
+    prompt = synth.make_prompt(30, shape.vocab)
+    toks = [int(prompt[0, -1])] + [11, 200, 3, 509]
+    kv = binding.KVCache(target, 1, 256)
+    binding.specdec_prefill(target, kv, i32(prompt))
+    block = torch.empty((1, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv, g, i32(np.array([toks[1:]])), g, block)
+    one = torch.empty((1, 1, shape.vocab), dtype=torch.float32, device="cuda")
+    rows = []
+    for i, t in enumerate(toks):
+        kv.set_state([29 + i], [[0, t]], [1])
+        binding.specdec_verify(target, kv, 0, None, 0, one)
+        rows.append(one.cpu().numpy()[0, 0].copy())
+    seq = np.stack(rows)
+    diff = float(np.abs(block.cpu().numpy()[0] - seq).max())
+    log(f"verify block vs sequential steps max diff {diff:.3g} (bitwise={diff == 0.0})")
+    assert diff <= 1e-6
+
+
+# ---------------------------------------------------------------- bf16 Llama-shaped prefixes
+def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None):
+    torch = torch_cuda()
+    B = len(lengths)
+    capacity = capacity or int(np.ceil((max(lengths) + g + 1) / 64) * 64)
+    log(f"bf16 case d={shape.d_model} L={n_layers} B={B} ctx={list(lengths)[:4]} g={g}")
+    W = synth.make_weights(shape, n_layers=n_layers)
+    ctx = synth.make_kv_context(shape, n_layers, lengths)
+    dw = binding.DeviceWeights(shape, W)
+    target = binding.Model(dw, n_layers, max_rows=B * (g + 1), max_ctx=capacity)
+    kv = binding.KVCache(target, B, capacity)
+    install_context(kv, ctx, lengths, n_layers, shape.dtype)
+    pend = synth.make_prompt(1, shape.vocab, batch=B, seed=seed + 31)[:, 0]
+    kv.set_state(np.asarray(lengths, np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
+    drafts = synth.make_prompt(g, shape.vocab, batch=B, seed=seed + 32)
+    logits = torch.empty((B, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv, g, i32(drafts), g, logits)
+    got = logits.cpu().numpy()
+    assert kv.read_state()["status"] == 0
+    m = om.Model(shape, W, n_layers=n_layers)
+    caches = oracle_caches(shape, n_layers, ctx, lengths, capacity)
+    worst = 0.0
+    for b in range(B):
+        ref = m.forward_block([int(pend[b])] + list(drafts[b]), int(lengths[b]), caches[b])
+        worst = max(worst, float(np.abs(got[b] - ref).max()))
+        # the drafted tokens' K/V were appended at [len, len+g]
+        k, v = kv.read_context(n_layers - 1, b, int(lengths[b]), g + 1)
+        kf = k.float().cpu().numpy()
+        assert np.abs(kf - caches[b].k[n_layers - 1][lengths[b]:lengths[b] + g + 1]).max() < 0.05
+    log(f"bf16 verify max-abs logit error {worst:.3g}")
+    assert worst < TOL_BF16
+    return worst
+
+
+def test_bf16_1b_shape_verify():
+    _bf16_case(synth.LLAMA_1B, 2, [517], g=4)
+
+
+def test_bf16_1b_shape_ragged_batch():
+    _bf16_case(synth.LLAMA_1B, 2, [1, 64, 300, 129], g=4, seed=1)
+
+
+@pytest.mark.parametrize("g", [2, 4, 8])
+def test_bf16_7b_shape_verify(g):
+    _bf16_case(synth.LLAMA_7B, 2, [2048], g=g)
+
+
+def test_bf16_7b_shape_multi_request_ragged():
+    # 16 sequences, ragged contexts, gamma 6: 112 rows (GEMMs run in two row launches)
+    lengths = synth.make_ragged_lengths(16, 40, 400)
+    _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=2)
+
+
+# ---------------------------------------------------------------- context copy and errors
+def test_kv_context_roundtrip_is_exact(tiny):
+    torch = torch_cuda()
+    shape, _, target, _ = tiny
+    kv = binding.KVCache(target, 2, 128)
+    k = torch.randn((50, shape.n_kv_heads, shape.head_dim), device="cuda")
+    v = torch.randn((50, shape.n_kv_heads, shape.head_dim), device="cuda")
+    kv.write_context(1, 1, 10, k, v)
+    k2, v2 = kv.read_context(1, 1, 10, 50)
+    assert torch.equal(k, k2) and torch.equal(v, v2)
+    with pytest.raises(binding.SpecdecError):
+        kv.read_context(1, 1, 100, 50)
+
+
+def test_device_and_host_errors(tiny):
+    torch = torch_cuda()
+    shape, _, target, _ = tiny
+    kv = binding.KVCache(target, 1, 128)
+    kv.set_state([10], [[0, 5]], [1])
+    logits = torch.empty((1, 5, shape.vocab), dtype=torch.float32, device="cuda")
+    bad = i32(np.array([[1, 2, shape.vocab + 3, 4]]))
+    binding.specdec_verify(target, kv, 4, bad, 4, logits)
+    assert binding.specdec_device_status(kv) == -7
+    kv.set_state([124], [[0, 5]], [1])
+    with pytest.raises(binding.SpecdecError) as e:
+        binding.specdec_verify(target, kv, 4, i32(np.array([[1, 2, 3, 4]])), 4, logits)
+    assert e.value.status == -3
+    with pytest.raises(ValueError):
+        binding.specdec_verify(target, kv, 4, np.array([[1, 2, 3, 4]], np.int32), 4, logits)
