@@ -1,0 +1,344 @@
+#!/usr/bin/env python3
+"""Benchmark of one draft-and-verify iteration on one MI355X.
+
+Workload: the 7B-shaped bf16 target (32 layers, d 4096, 32 heads x 128, SwiGLU
+11008, vocab 32000) with a 4-layer draft (its first layers + shared embedding,
+final norm and LM head), batch 1, resident context of 2048 positions,
+gamma = 4, temperature 1.0.  A step is the whole iteration: gamma draft steps,
+the verify pass, accept / resample, and the KV commit of both caches; every
+step starts from the same context (the cache state is restored on the device
+before each step), so all steps do identical work.
+
+Reported value: verify-step tokens/s = batch*(gamma+1) / t_verify, where
+t_verify covers specdec_verify + specdec_accept inside each timed step.
+Weights and contexts are synthetic (seeded N(0, 0.02^2) weights drawn on the
+device, N(0, (0.02 sqrt d)^2) K/V); the paper's trained models and datasets
+are not used.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "verify-step tokens/s (7B-shape, gamma=4, bs1); achieved HBM GB/s vs peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--gamma", type=int, default=4)
+    ap.add_argument("--ctx", type=int, default=2048)
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--draft-layers", type=int, default=4)
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=5)
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- synthetic model on the device
+def device_weights(shape, seed=0):
+    """Seeded N(0, 0.02^2) bf16 weights drawn on the device (RMSNorm gains 1.0)."""
+    import torch
+    from paper_2608_10362_amd import binding
+    gen = torch.Generator(device="cuda")
+    idx = [0]
+
+    def mat(*shp):
+        gen.manual_seed(seed * 1000003 + idx[0])
+        idx[0] += 1
+        t = torch.empty(shp, dtype=torch.float32, device="cuda").normal_(0.0, 0.02, generator=gen)
+        return t.to(torch.bfloat16)
+
+    def gain(n):
+        idx[0] += 1
+        return torch.ones(n, dtype=torch.bfloat16, device="cuda")
+
+    d, f = shape.d_model, shape.ffn_dim
+    w = {"embed": mat(shape.vocab, d), "layers": []}
+    for _ in range(shape.n_layers):
+        w["layers"].append({"attn_norm": gain(d), "wq": mat(shape.q_dim, d), "wk": mat(shape.kv_dim, d),
+                            "wv": mat(shape.kv_dim, d), "wo": mat(d, shape.q_dim), "ffn_norm": gain(d),
+                            "w_gate": mat(f, d), "w_up": mat(f, d), "w_down": mat(d, f)})
+    w["final_norm"] = gain(d)
+    w["lm_head"] = mat(shape.vocab, d)
+    return binding.DeviceWeights(shape, w)
+
+
+def install_context(kv, n_layers, shape, lengths, seed=5):
+    import torch
+    gen = torch.Generator(device="cuda")
+    sigma = 0.02 * shape.d_model ** 0.5
+    for l in range(n_layers):
+        for b, L in enumerate(lengths):
+            gen.manual_seed(seed * 7919 + l * 131 + b)
+            k = (torch.randn((L, shape.n_kv_heads, shape.head_dim), generator=gen, device="cuda") * sigma)
+            v = (torch.randn((L, shape.n_kv_heads, shape.head_dim), generator=gen, device="cuda") * sigma)
+            kv.write_context(l, b, 0, k.to(torch.bfloat16), v.to(torch.bfloat16))
+
+
+# ---------------------------------------------------------------- algorithmic bytes
+def kernel_bytes(shape, ctx_read):
+    """Algorithmic HBM bytes per launch of each kernel kind (weights streamed once,
+    KV read for the keys a launch attends to); activations (a few hundred KB) left out."""
+    d, f, V = shape.d_model, shape.ffn_dim, shape.vocab
+    e = 2
+    return {
+        "qkv": ((shape.q_dim + 2 * shape.kv_dim) * d + d) * e,
+        "o_proj": d * shape.q_dim * e,
+        "gate_up": (2 * f * d + d) * e,
+        "down": d * f * e,
+        "lm_head": (V * d + d) * e,
+        "attention": ctx_read * shape.n_kv_heads * shape.head_dim * 2 * e,
+    }
+
+
+def verify_step_bytes(shape, ctx, gamma, batch):
+    """Bytes one verify step must move: every weight once, the committed KV, the new KV."""
+    L, d, f, V = shape.n_layers, shape.d_model, shape.ffn_dim, shape.vocab
+    e = 2
+    per_layer = ((shape.q_dim + 2 * shape.kv_dim) * d + d * shape.q_dim + 3 * f * d + 2 * d) * e
+    weights = L * per_layer + (V * d + d) * e + batch * (gamma + 1) * d * e
+    kv_row = shape.n_kv_heads * shape.head_dim * 2 * e * L
+    return weights + batch * ctx * kv_row + batch * (gamma + 1) * kv_row
+
+
+# ---------------------------------------------------------------- CPU oracle baseline
+def cpu_baseline(shape, ctx, gamma):
+    """The oracle's verify pass on the host: time 1 and 2 layers (+ final norm and
+    LM head) of the 7B shape at the same context, extrapolate the per-layer time to
+    all layers."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import model as om
+    from paper_2608_10362_amd import synth
+
+    W = synth.make_weights(shape, n_layers=2, threads=min(16, os.cpu_count() or 1))
+    ctxkv = synth.make_kv_context(shape, 2, [ctx], threads=min(16, os.cpu_count() or 1))
+    toks = [int(t) for t in synth.make_prompt(gamma + 1, shape.vocab)[0]]
+    times = {}
+    for L in (1, 2):
+        best = []
+        for _ in range(2):
+            c = om.KVCache(shape, L, ctx + gamma + 1)
+            for l in range(L):
+                c.load(l, ctxkv[l][0]["k"], ctxkv[l][0]["v"])
+            c.length = ctx
+            m = om.Model(shape, W, n_layers=L)
+            t0 = time.perf_counter()
+            m.forward_block(toks, ctx, c)
+            best.append(time.perf_counter() - t0)
+        times[L] = float(np.median(best))
+    t_layer = max(times[2] - times[1], 1e-9)
+    t_rest = max(times[1] - t_layer, 0.0)
+    t_full = t_rest + shape.n_layers * t_layer
+    threads = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+    return {"value": (gamma + 1) / t_full, "unit": "tokens/s", "cores": int(max(threads) if threads else 1),
+            "kind": "oracle",
+            "sample": (f"float64 numpy oracle verify pass (gamma={gamma}, ctx {ctx}) over 1 and 2 layers of the "
+                       f"7B shape + LM head, median of 2 runs each ({times[1]:.2f} s, {times[2]:.2f} s); per-layer "
+                       f"time x {shape.n_layers} layers -> {t_full:.1f} s per verify step")}
+
+
+# ---------------------------------------------------------------- main
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_10362_amd import binding, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    binding.lib()
+    shape = synth.LLAMA_7B
+    B, g, ctx, T = args.batch, args.gamma, args.ctx, args.temperature
+    cap = ((ctx + g + 2 + 63) // 64) * 64
+    t0 = time.time()
+    dw = device_weights(shape)
+    target = binding.Model(dw, shape.n_layers, max_rows=max(B * (g + 1), 2 * B), max_ctx=cap)
+    draft = binding.Model(dw, args.draft_layers, max_rows=max(B * (g + 1), 2 * B), max_ctx=cap)
+    kv_t = binding.KVCache(target, B, cap)
+    kv_d = binding.KVCache(draft, B, cap)
+    install_context(kv_t, shape.n_layers, shape, [ctx] * B)
+    install_context(kv_d, args.draft_layers, shape, [ctx] * B)
+    pend = synth.make_prompt(1, shape.vocab, batch=B)[:, 0]
+    import numpy as np
+    st = (np.full(B, ctx, np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
+    kv_t.set_state(*st)
+    kv_d.set_state(*st)
+    saved_t, saved_d = kv_t.state.clone(), kv_d.state.clone()
+    sd = binding.SpecDecoder(target, draft, kv_t, kv_d, g, T, seed=synth.SEED_SAMPLING)
+    torch.cuda.synchronize()
+    log(f"set-up {time.time() - t0:.1f} s (weights {sum(t.numel() for t in dw.t.values()) * 2 / 1e9:.2f} GB "
+        f"+ layers)")
+
+    def restore():
+        kv_t.state.copy_(saved_t)
+        kv_d.state.copy_(saved_d)
+        kv_t.kv.len_upper = ctx
+        kv_d.kv.len_upper = ctx
+
+    def draft_part(i):
+        restore()
+        sd.draft_phase(i)
+
+    def verify_part(i):
+        sd.verify_phase(i)
+
+    def commit_part():
+        sd.commit_phase()
+
+    # eager reference step (also the result the graphs must reproduce)
+    draft_part(0)
+    verify_part(0)
+    commit_part()
+    torch.cuda.synchronize()
+    ref = (sd.d.clone(), sd.logits.clone(), sd.n_acc.clone(), sd.next.clone())
+
+    use_graph = not args.no_graph
+    graphs = None
+    if use_graph:
+        try:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                draft_part(0); verify_part(0); commit_part()
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            gd, gv, gc = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gd):
+                draft_part(0)
+            with torch.cuda.graph(gv):
+                verify_part(0)
+            with torch.cuda.graph(gc):
+                commit_part()
+            graphs = (gd, gv, gc)
+            # every replay must reproduce the eager step exactly
+            for r in range(3):
+                gd.replay(); gv.replay(); gc.replay()
+                torch.cuda.synchronize()
+                same = (torch.equal(sd.d, ref[0]) and torch.equal(sd.logits, ref[1]) and
+                        torch.equal(sd.n_acc, ref[2]) and torch.equal(sd.next, ref[3]))
+                if not same:
+                    raise RuntimeError(f"graph replay {r} differs from the eager step")
+                draft_part(0); verify_part(0); commit_part()  # eager work between replays
+                torch.cuda.synchronize()
+        except Exception as e:  # report and time eagerly
+            log(f"graph capture disabled: {e}")
+            graphs, use_graph = None, False
+
+    def run_step(i, ev=None):
+        if graphs:
+            graphs[0].replay()
+            if ev: ev[0].record()
+            graphs[1].replay()
+            if ev: ev[1].record()
+            graphs[2].replay()
+        else:
+            draft_part(i)
+            if ev: ev[0].record()
+            verify_part(i)
+            if ev: ev[1].record()
+            commit_part()
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.steps):
+        run_step(args.warmup + i, evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    verify_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    step_ms = total_ms / args.steps
+    status = min(int(sd.status.item()), kv_t.read_state()["status"], kv_d.read_state()["status"])
+
+    # mean accepted length over eager steps with distinct random draws (outside the timed region)
+    acc = []
+    for i in range(8):
+        draft_part(1000 + i); verify_part(1000 + i); commit_part()
+        acc.append(sd.n_acc.clone())
+    mean_A = float(torch.stack(acc).float().mean().item())
+
+    # per-kernel durations (HIP events on the library's stream, eager launches)
+    binding.specdec_timing_enable(True)
+    for i in range(args.profile_steps):
+        draft_part(i); verify_part(i); commit_part()
+    torch.cuda.synchronize()
+    per = binding.specdec_timing_read()
+    binding.specdec_timing_enable(False)
+    kb_verify = kernel_bytes(shape, ctx + g + 1)
+    kernels = {}
+    for k, (ms, n) in per.items():
+        if n == 0:
+            continue
+        avg_us = ms * 1e3 / n
+        entry = {"avg_us": round(avg_us, 3), "launches_per_step": n / args.profile_steps,
+                 "ms_per_step": round(ms / args.profile_steps, 4)}
+        if k in kb_verify and k != "attention":
+            entry["GBps"] = round(kb_verify[k] / (avg_us * 1e-6) / 1e9, 1)
+        kernels[k] = entry
+    dom = max((k for k in kernels if k in kb_verify and k != "attention"), key=lambda k: kernels[k]["ms_per_step"])
+    dom_bytes = kb_verify[dom]
+    achieved = dom_bytes / (kernels[dom]["avg_us"] * 1e-6) / 1e9
+    vbytes = verify_step_bytes(shape, ctx, g, B)
+    verify_GBps = vbytes / (verify_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(B * (g + 1) / (verify_ms * 1e-3), 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"7B-shaped bf16 target verify + {args.draft_layers}-layer draft, gamma={g}, "
+                               f"batch {B}, context {ctx}, temperature {T}",
+                   "gamma": g, "batch": B, "ctx": ctx, "temperature": T, "draft_layers": args.draft_layers,
+                   "hip_graph": use_graph},
+        "roofline": {"bound": "hbm", "kernel": f"gemm {dom}", "achieved": round(achieved, 1),
+                     "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": None, "bytes_per_launch": dom_bytes},
+        "verify_ms": round(verify_ms, 4),
+        "verify_hbm_GBps": round(verify_GBps, 1),
+        "verify_hbm_frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
+        "verify_bytes": vbytes,
+        "generated_tokens_per_s": round(B * (mean_A + 1) / (step_ms * 1e-3), 2),
+        "mean_accepted": round(mean_A, 3),
+        "device_status": status,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(shape, ctx, g)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -244,6 +244,34 @@ SPECDEC_API specdec_status specdec_sample(int32_t batch, int32_t vocab, const fl
 SPECDEC_API specdec_status specdec_draw_u32(int32_t batch, uint64_t seed, uint64_t step, int32_t purpose, int32_t index,
                                 uint32_t* out, void* stream);
 
+/* ---------------------------------------------------------------- measurement */
+
+/* Kernel kinds for specdec_timing_read. */
+enum {
+  SPECDEC_KERNEL_EMBED = 0,        /* row set-up + embedding gather */
+  SPECDEC_KERNEL_QKV = 1,          /* RMSNorm + Q|K|V projection GEMM */
+  SPECDEC_KERNEL_ROPE_APPEND = 2,  /* RoPE + KV append */
+  SPECDEC_KERNEL_ATTENTION = 3,    /* split-KV attention + combine */
+  SPECDEC_KERNEL_O_PROJ = 4,       /* O projection GEMM + residual */
+  SPECDEC_KERNEL_GATE_UP = 5,      /* RMSNorm + gate|up GEMM + SwiGLU */
+  SPECDEC_KERNEL_DOWN = 6,         /* down projection GEMM + residual */
+  SPECDEC_KERNEL_LM_HEAD = 7,      /* final RMSNorm + LM head GEMM */
+  SPECDEC_KERNEL_DRAFT_FINISH = 8, /* draft softmax + sample */
+  SPECDEC_KERNEL_ACCEPT = 9,       /* accept / resample */
+  SPECDEC_KERNEL_COMMIT = 10,      /* KV commit */
+  SPECDEC_KERNEL_KINDS = 11
+};
+
+/* Measurement hook (process-wide, off by default, never used inside graph
+ * capture): while enabled, every kernel launch of the hot path is bracketed by
+ * a pair of HIP events recorded on the launch's own stream. */
+SPECDEC_API specdec_status specdec_timing_enable(int32_t enable);
+/* Synchronize on the recorded events and return, per kernel kind, the summed
+ * duration in milliseconds and the number of launches since the last read
+ * (host arrays of SPECDEC_KERNEL_KINDS entries; either may be NULL); resets
+ * the accumulators. */
+SPECDEC_API specdec_status specdec_timing_read(double* total_ms, int64_t* launches);
+
 /* Synchronize the stream and return the sticky status word of `kv` (also
  * written to *host_out if non-NULL). */
 SPECDEC_API specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host_out);

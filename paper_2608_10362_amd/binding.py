@@ -97,7 +97,12 @@ _SIGS = {
                                         ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_device_status": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "specdec_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
+    "specdec_timing_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
 }
+
+KERNEL_KINDS = ("embed", "qkv", "rope_append", "attention", "o_proj", "gate_up", "down", "lm_head", "draft_finish",
+                "accept", "commit")
 
 
 def lib() -> ctypes.CDLL:
@@ -374,6 +379,18 @@ def specdec_device_status(kv: KVCache, stream=None) -> int:
 
 def specdec_status_string(status: int) -> str:
     return lib().specdec_status_string(status).decode()
+
+
+def specdec_timing_enable(enable: bool):
+    _check(lib().specdec_timing_enable(1 if enable else 0), "specdec_timing_enable")
+
+
+def specdec_timing_read():
+    """{kind: (total_ms, launches)} since the last read (synchronizes on the events)."""
+    ms = np.zeros(len(KERNEL_KINDS), np.float64)
+    n = np.zeros(len(KERNEL_KINDS), np.int64)
+    _check(lib().specdec_timing_read(ms.ctypes.data, n.ctypes.data), "specdec_timing_read")
+    return {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KERNEL_KINDS)}
 
 
 # ---------------------------------------------------------------- one iteration

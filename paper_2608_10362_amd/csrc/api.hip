@@ -23,6 +23,7 @@ struct specdec_model {
   RowDesc* rows;
   float* rope_cs;
   float* h;
+  float* xg;
   float* ss;
   int ss_ld, ss_parts_max;
   float* qkv;
@@ -37,6 +38,45 @@ struct specdec_model {
 
 namespace {
 
+// ---------------------------------------------------------------- kernel timing hook
+struct Timing {
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  struct Rec { int kind; hipEvent_t b, e; };
+  std::vector<Rec> recs;
+  hipEvent_t get() {
+    if (!pool.empty()) { hipEvent_t ev = pool.back(); pool.pop_back(); return ev; }
+    hipEvent_t ev = nullptr;
+    if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+    return ev;
+  }
+};
+Timing g_timing;
+
+// Brackets the launches of one kernel kind with events when timing is on.
+struct Timed {
+  int kind;
+  hipStream_t s;
+  hipEvent_t b = nullptr;
+  Timed(int k, hipStream_t st) : kind(k), s(st) {
+    if (g_timing.enabled && (b = g_timing.get()) && hipEventRecord(b, s) != hipSuccess) {
+      g_timing.pool.push_back(b);
+      b = nullptr;
+    }
+  }
+  ~Timed() {
+    if (!b) return;
+    hipEvent_t e = g_timing.get();
+    if (!e) { g_timing.pool.push_back(b); return; }
+    if (hipEventRecord(e, s) != hipSuccess) {
+      g_timing.pool.push_back(b);
+      g_timing.pool.push_back(e);
+      return;
+    }
+    g_timing.recs.push_back({kind, b, e});
+  }
+};
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -44,7 +84,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, ss, qkv, qr, o_part, ml_part, o, u, logits, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -53,13 +93,14 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   const size_t R = (size_t)max_rows;
   const int hd = d->head_dim, H = d->n_heads, G = d->n_kv_heads;
   w.ss_parts = std::max(1, gemm_row_blocks(d->dtype, EPI_RESID, d->d_model, max_rows));
-  w.chunk = attention_chunk(hd);
+  w.chunk = attention_chunk(d->dtype, hd);
   w.n_split = (max_ctx + w.chunk - 1) / w.chunk;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t at = off; off = align_up(off + bytes); return at; };
   w.rows = take(R * sizeof(RowDesc));
   w.rope = take(R * hd * 4);
   w.h = take(R * d->d_model * 4);
+  w.xg = take(R * d->d_model * 4);
   w.ss = take((size_t)w.ss_parts * R * 4);
   w.qkv = take(R * (H + 2 * G) * hd * 4);
   w.qr = take(R * H * hd * 4);
@@ -118,6 +159,7 @@ hipError_t gemm_rows(int dtype, GemmArgs g, int M, hipStream_t s) {
     c.out = g.out + (size_t)m0 * g.ldo;
     if (g.ss_in) c.ss_in = g.ss_in + m0;
     if (g.ss_out) c.ss_out = g.ss_out + m0;
+    if (g.xg_out) c.xg_out = g.xg_out + (size_t)m0 * g.ldo;
     hipError_t e = launch_gemm(dtype, c, s);
     if (e != hipSuccess) return e;
   }
@@ -146,15 +188,21 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   ra.head_dim = hd;
   ra.rope_base = d.rope_base;
   ra.embed = m->embed;
+  ra.gain = m->attn_norm[0];
+  ra.xg = m->xg;
   ra.rows = m->rows;
   ra.rope_cs = m->rope_cs;
   ra.h = m->h;
   ra.ss = m->ss;
-  SD_TRY(launch_rows_embed(dt, ra, s));
+  {
+    Timed t(SPECDEC_KERNEL_EMBED, s);
+    SD_TRY(launch_rows_embed(dt, ra, s));
+  }
 
   GemmArgs base{};
   base.eps = d.rms_eps;
   base.ss_ld = m->ss_ld;
+  base.gain_bf16 = dt == SPECDEC_BF16;
   int n_ss = 1;
   const int n_resid_blocks = gemm_row_blocks(dt, EPI_RESID, d.d_model, M);
 
@@ -179,43 +227,65 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
 
   for (int l = 0; l < m->n_layers; ++l) {
     GemmArgs q = base;  // RMSNorm + Q|K|V projections
-    q.x = m->h; q.ldx = d.d_model; q.gain = m->attn_norm[l]; q.ss_in = m->ss; q.n_ss = n_ss;
+    q.x = m->xg; q.ldx = d.d_model; q.ss_in = m->ss; q.n_ss = n_ss;
     q.K = d.d_model;
     q.w[0] = m->wq[l]; q.w[1] = m->wk[l]; q.w[2] = m->wv[l];
     q.n_seg[0] = H * hd; q.n_seg[1] = G * hd; q.n_seg[2] = G * hd;
     q.n_rows = (H + 2 * G) * hd; q.kind = EPI_STORE; q.out = m->qkv; q.ldo = (H + 2 * G) * hd;
-    SD_TRY(gemm_rows(dt, q, M, s));
+    {
+      Timed t(SPECDEC_KERNEL_QKV, s);
+      SD_TRY(gemm_rows(dt, q, M, s));
+    }
 
     at.layer = l;
-    SD_TRY(launch_rope_append(at, s));
-    SD_TRY(launch_attention(at, s));
+    {
+      Timed t(SPECDEC_KERNEL_ROPE_APPEND, s);
+      SD_TRY(launch_rope_append(at, s));
+    }
+    {
+      Timed t(SPECDEC_KERNEL_ATTENTION, s);
+      SD_TRY(launch_attention(at, s));
+    }
 
     GemmArgs o = base;  // O projection + residual
     o.x = m->o; o.ldx = H * hd; o.K = H * hd;
     o.w[0] = m->wo[l]; o.n_seg[0] = d.d_model; o.n_rows = d.d_model; o.kind = EPI_RESID;
-    o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss;
-    SD_TRY(gemm_rows(dt, o, M, s));
+    o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss; o.xg_out = m->xg; o.gain_out = m->ffn_norm[l];
+    {
+      Timed t(SPECDEC_KERNEL_O_PROJ, s);
+      SD_TRY(gemm_rows(dt, o, M, s));
+    }
     n_ss = n_resid_blocks;
 
     GemmArgs gu = base;  // RMSNorm + gate|up + SwiGLU
-    gu.x = m->h; gu.ldx = d.d_model; gu.gain = m->ffn_norm[l]; gu.ss_in = m->ss; gu.n_ss = n_ss;
+    gu.x = m->xg; gu.ldx = d.d_model; gu.ss_in = m->ss; gu.n_ss = n_ss;
     gu.K = d.d_model;
     gu.w[0] = m->w_gate[l]; gu.w[1] = m->w_up[l]; gu.n_seg[0] = d.ffn_dim; gu.n_seg[1] = d.ffn_dim;
     gu.n_rows = d.ffn_dim; gu.kind = EPI_SWIGLU; gu.out = m->u; gu.ldo = d.ffn_dim;
-    SD_TRY(gemm_rows(dt, gu, M, s));
+    {
+      Timed t(SPECDEC_KERNEL_GATE_UP, s);
+      SD_TRY(gemm_rows(dt, gu, M, s));
+    }
 
     GemmArgs dn = base;  // down projection + residual
     dn.x = m->u; dn.ldx = d.ffn_dim; dn.K = d.ffn_dim;
     dn.w[0] = m->w_down[l]; dn.n_seg[0] = d.d_model; dn.n_rows = d.d_model; dn.kind = EPI_RESID;
-    dn.out = m->h; dn.ldo = d.d_model; dn.ss_out = m->ss;
-    SD_TRY(gemm_rows(dt, dn, M, s));
+    dn.out = m->h; dn.ldo = d.d_model; dn.ss_out = m->ss; dn.xg_out = m->xg;
+    dn.gain_out = l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm;
+    {
+      Timed t(SPECDEC_KERNEL_DOWN, s);
+      SD_TRY(gemm_rows(dt, dn, M, s));
+    }
   }
 
   GemmArgs hd_ = base;  // final RMSNorm + LM head
-  hd_.x = m->h; hd_.ldx = d.d_model; hd_.gain = m->final_norm; hd_.ss_in = m->ss; hd_.n_ss = n_ss;
+  hd_.x = m->xg; hd_.ldx = d.d_model; hd_.ss_in = m->ss; hd_.n_ss = n_ss;
   hd_.K = d.d_model; hd_.w[0] = m->lm_head; hd_.n_seg[0] = d.vocab; hd_.n_rows = d.vocab;
   hd_.kind = EPI_STORE; hd_.out = logits; hd_.ldo = d.vocab;
-  SD_TRY(gemm_rows(dt, hd_, M, s));
+  {
+    Timed t(SPECDEC_KERNEL_LM_HEAD, s);
+    SD_TRY(gemm_rows(dt, hd_, M, s));
+  }
   return SPECDEC_OK;
 }
 
@@ -279,6 +349,7 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   m->rows = (RowDesc*)(base + L.rows);
   m->rope_cs = (float*)(base + L.rope);
   m->h = (float*)(base + L.h);
+  m->xg = (float*)(base + L.xg);
   m->ss = (float*)(base + L.ss);
   m->ss_ld = max_rows;
   m->ss_parts_max = L.ss_parts;
@@ -452,6 +523,7 @@ specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, in
   f.ld_d = ld_d;
   f.logits_out = logits_out;
   f.status = kv_status(kv);
+  Timed t(SPECDEC_KERNEL_DRAFT_FINISH, s);
   return hip_status(launch_draft_finish(f, s));
 }
 
@@ -498,6 +570,7 @@ specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32
   a.n_accepted = n_accepted;
   a.next_token = next_token;
   a.status = status;
+  Timed t(SPECDEC_KERNEL_ACCEPT, (hipStream_t)stream);
   return hip_status(launch_accept(a, (hipStream_t)stream));
 }
 
@@ -517,7 +590,11 @@ specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, co
   c.d = d;
   c.ld_d = ld_d;
   c.next_token = next_token;
-  specdec_status st = hip_status(launch_commit(c, (hipStream_t)stream));
+  specdec_status st;
+  {
+    Timed t(SPECDEC_KERNEL_COMMIT, (hipStream_t)stream);
+    st = hip_status(launch_commit(c, (hipStream_t)stream));
+  }
   if (st == SPECDEC_OK) kv->len_upper += gamma + 1;
   return st;
 }
@@ -544,6 +621,31 @@ specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host
   SD_TRY(hipStreamSynchronize(s));
   if (host_out) *host_out = v;
   return (specdec_status)v;
+}
+
+specdec_status specdec_timing_enable(int32_t enable) {
+  g_timing.enabled = enable != 0;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_timing_read(double* total_ms, int64_t* launches) {
+  double ms[SPECDEC_KERNEL_KINDS] = {0};
+  int64_t n[SPECDEC_KERNEL_KINDS] = {0};
+  specdec_status st = SPECDEC_OK;
+  for (auto& r : g_timing.recs) {
+    float t = 0.f;
+    if (hipEventSynchronize(r.e) != hipSuccess || hipEventElapsedTime(&t, r.b, r.e) != hipSuccess) st = SPECDEC_ERR_HIP;
+    ms[r.kind] += t;
+    n[r.kind] += 1;
+    g_timing.pool.push_back(r.b);
+    g_timing.pool.push_back(r.e);
+  }
+  g_timing.recs.clear();
+  for (int k = 0; k < SPECDEC_KERNEL_KINDS; ++k) {
+    if (total_ms) total_ms[k] = ms[k];
+    if (launches) launches[k] = n[k];
+  }
+  return st;
 }
 
 const char* specdec_status_string(specdec_status s) {

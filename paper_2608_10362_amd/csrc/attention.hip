@@ -28,35 +28,35 @@ __device__ __forceinline__ KT* k_block(const KvLayout& kv, int layer, int b, int
 }
 
 // ---------------------------------------------------------------- RoPE + append
+// Block (head slot, row): slots [0, H) rotate a query head into qr, [H, H+G)
+// rotate a key head and store it at the row's position, [H+G, H+2G) store a
+// value head (transposed).  Thread j handles the pair (j, j + hd/2).
 template <typename KT>
-__global__ __launch_bounds__(256) void rope_append_kernel(AttnArgs a) {
-  const int r = blockIdx.x;
-  const RowDesc rd = a.rows[r];
+__global__ __launch_bounds__(64) void rope_append_kernel(AttnArgs a) {
+  const int hs = blockIdx.x, r = blockIdx.y, j = threadIdx.x;
   const int hd = a.head_dim, half = hd / 2, H = a.n_heads, G = a.n_kv_heads;
+  if (j >= half) return;
+  const RowDesc rd = a.rows[r];
+  const float* src = a.qkv + (size_t)r * (H + 2 * G) * hd + (size_t)hs * hd;
+  const float x1 = src[j], x2 = src[j + half];
+  if (hs >= H + G) {  // value head
+    if (!rd.valid) return;
+    KT* vb = k_block<KT>(a.kv, a.layer, rd.b, hs - H - G) + (size_t)a.kv.capacity * hd;
+    Storage<KT>::store(vb + (size_t)j * a.kv.capacity + rd.pos, x1);
+    Storage<KT>::store(vb + (size_t)(j + half) * a.kv.capacity + rd.pos, x2);
+    return;
+  }
   const float* cs = a.rope_cs + (size_t)r * hd;
-  const float* src = a.qkv + (size_t)r * (H + 2 * G) * hd;
-  float* qr = a.qr + (size_t)r * H * hd;
-  for (int i = threadIdx.x; i < H * half; i += blockDim.x) {
-    const int head = i / half, j = i % half;
-    const float x1 = src[head * hd + j], x2 = src[head * hd + j + half];
-    const float c = cs[j], s = cs[half + j];
-    qr[head * hd + j] = x1 * c - x2 * s;
-    qr[head * hd + j + half] = x2 * c + x1 * s;
-  }
-  if (!rd.valid) return;
-  for (int i = threadIdx.x; i < G * half; i += blockDim.x) {
-    const int g = i / half, j = i % half;
-    const float* kp = src + (H + g) * hd;
-    const float x1 = kp[j], x2 = kp[j + half];
-    const float c = cs[j], s = cs[half + j];
-    KT* kb = k_block<KT>(a.kv, a.layer, rd.b, g) + (size_t)rd.pos * hd;
-    Storage<KT>::store(kb + j, x1 * c - x2 * s);
-    Storage<KT>::store(kb + j + half, x2 * c + x1 * s);
-  }
-  for (int i = threadIdx.x; i < G * hd; i += blockDim.x) {
-    const int g = i / hd, dd = i % hd;
-    KT* vb = k_block<KT>(a.kv, a.layer, rd.b, g) + (size_t)a.kv.capacity * hd;
-    Storage<KT>::store(vb + (size_t)dd * a.kv.capacity + rd.pos, src[(H + G + g) * hd + dd]);
+  const float c = cs[j], s = cs[half + j];
+  const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
+  if (hs < H) {
+    float* q = a.qr + ((size_t)r * H + hs) * hd;
+    q[j] = y1;
+    q[j + half] = y2;
+  } else if (rd.valid) {
+    KT* kb = k_block<KT>(a.kv, a.layer, rd.b, hs - H) + (size_t)rd.pos * hd;
+    Storage<KT>::store(kb + j, y1);
+    Storage<KT>::store(kb + j + half, y2);
   }
 }
 
@@ -156,6 +156,183 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- MFMA split-KV partials (bf16 cache)
+// One wave per (16-query tile, 64-key split, kv head, sequence).  S = Q K^T
+// and O = P V run on v_mfma_f32_16x16x32_bf16 with the float32 operands (Q,
+// P) split into hi + lo bf16 parts; K fragments are 16-byte loads of K rows,
+// V fragments 16-byte loads of the transposed V rows.  Lane l holds rows
+// 4(l/16)+r of S and O, so the per-row max / sum live in the same lanes.
+constexpr int kSplitKeys = 64;
+
+__device__ __forceinline__ void split_hilo(const float* v, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const __bf16 h = (__bf16)v[j];
+    hi[j] = h;
+    lo[j] = (__bf16)(v[j] - (float)h);
+  }
+}
+
+__device__ __forceinline__ float group16_max(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ float group16_sum(float v) {
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+template <int HD>
+__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
+  constexpr int KST = HD / 32;  // k-steps of Q K^T
+  constexpr int DT = HD / 16;   // 16-wide dimension tiles of P V
+  constexpr int NT = kSplitKeys / 16;
+  __shared__ float pbuf[16][kSplitKeys + 4];
+  const int lane = threadIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int H = a.n_heads, G = a.n_kv_heads, group = H / G;
+  const int rps = a.rps, r0 = b * rps, nq = rps * group;
+  const int split = blockIdx.x % a.n_split, mt = blockIdx.x / a.n_split;
+  if (mt * 16 >= nq) return;
+  int nk = 0;
+  for (int i = 0; i < rps; ++i) {
+    const RowDesc rd = a.rows[r0 + i];
+    if (rd.valid) nk = max(nk, rd.pos + 1);
+  }
+  const int k0 = split * kSplitKeys;
+  if (k0 >= nk) return;
+  const int c16 = lane & 15, grp = lane >> 4;
+  const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
+  const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;
+
+  // K and V fragments of the whole split, issued first (the bytes in flight).
+  u32x4 kf[NT][KST];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int key = k0 + 16 * t + c16;
+#pragma unroll
+    for (int c = 0; c < KST; ++c)
+      kf[t][c] = key < nk ? *(const u32x4*)(kb + (size_t)key * HD + 32 * c + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
+  }
+  u32x4 vf[2][DT];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int key = k0 + 32 * s + 8 * grp;  // first of this lane's 8 keys
+    const int nvalid = min(8, nk - key);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (nvalid > 0) {
+        v = *(const u32x4*)(vb + (size_t)(dt * 16 + c16) * a.kv.capacity + key);
+        if (nvalid < 8) {  // keys past the context: zero (never multiply stale memory)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (2 * j >= nvalid) v[j] = 0u;
+            else if (2 * j + 1 >= nvalid) v[j] &= 0xffffu;
+          }
+        }
+      }
+      vf[s][dt] = v;
+    }
+  }
+
+  // Q fragments (A operand): query qa = mt*16 + l%16, pre-scaled by 1/sqrt(hd).
+  const float scale = 1.0f / sqrtf((float)HD);
+  bf16x8 qhi[KST], qlo[KST];
+  {
+    const int qa = mt * 16 + c16;
+    const float* qp = nullptr;
+    if (qa < nq) {
+      const int row = r0 + qa / group, head = g * group + qa % group;
+      qp = a.qr + ((size_t)row * H + head) * HD;
+    }
+#pragma unroll
+    for (int c = 0; c < KST; ++c) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = qp ? qp[32 * c + 8 * grp + j] * scale : 0.f;
+      split_hilo(v, qhi[c], qlo[c]);
+    }
+  }
+  // positions of the 4 query rows this lane holds in the C layout (-1: none)
+  int qpos[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qc = mt * 16 + 4 * grp + r;
+    qpos[r] = -1;
+    if (qc < nq) {
+      const RowDesc rd = a.rows[r0 + qc / group];
+      if (rd.valid) qpos[r] = rd.pos;
+    }
+  }
+
+  floatx4 sf[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < KST; ++c) {
+      const bf16x8 kk = __builtin_bit_cast(bf16x8, kf[t][c]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qhi[c], kk, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qlo[c], kk, acc, 0, 0, 0);
+    }
+    const int key = k0 + 16 * t + c16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (key > qpos[r]) acc[r] = -INFINITY;
+    sf[t] = acc;
+  }
+  float mx[4], sm[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) m = fmaxf(m, sf[t][r]);
+    mx[r] = group16_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float p = mx[r] == -INFINITY || sf[t][r] == -INFINITY ? 0.f : expf(sf[t][r] - mx[r]);
+      pbuf[4 * grp + r][16 * t + c16] = p;
+      s += p;
+    }
+    sm[r] = group16_sum(s);
+  }
+  __syncthreads();  // one wave per block: P written by all lanes before the transposed reads
+
+  floatx4 of[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) of[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    float pv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pv[j] = pbuf[c16][32 * s + 8 * grp + j];
+    bf16x8 phi, plo;
+    split_hilo(pv, phi, plo);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x8 vv = __builtin_bit_cast(bf16x8, vf[s][dt]);
+      of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vv, of[dt], 0, 0, 0);
+      of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vv, of[dt], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qc = mt * 16 + 4 * grp + r;
+    if (qpos[r] < 0 || mx[r] == -INFINITY) continue;
+    const int row = r0 + qc / group, head = g * group + qc % group;
+    const size_t slot = ((size_t)row * H + head) * a.n_split + split;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) a.o_part[slot * HD + dt * 16 + c16] = of[dt][r];
+    if (c16 == 0) {
+      a.ml_part[2 * slot] = mx[r];
+      a.ml_part[2 * slot + 1] = sm[r];
+    }
+  }
+}
+
 // ---------------------------------------------------------------- combine
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   const int head = blockIdx.x, r = blockIdx.y;
@@ -210,24 +387,37 @@ size_t attn_smem_bytes(int chunk, int hd) {
 
 }  // namespace
 
-int attention_chunk(int head_dim) { return head_dim >= 128 ? 32 : (head_dim >= 64 ? 64 : 128); }
+int attention_chunk(int dtype, int head_dim) {
+  if (dtype == SPECDEC_BF16) return kSplitKeys;
+  return head_dim >= 128 ? 32 : (head_dim >= 64 ? 64 : 128);
+}
 
 hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s) {
+  dim3 grid(a.n_heads + 2 * a.n_kv_heads, a.M);
   if (a.kv.dtype == SPECDEC_BF16)
-    hipLaunchKernelGGL((rope_append_kernel<uint16_t>), dim3(a.M), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((rope_append_kernel<uint16_t>), grid, dim3(64), 0, s, a);
   else
-    hipLaunchKernelGGL((rope_append_kernel<float>), dim3(a.M), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((rope_append_kernel<float>), grid, dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int B = a.M / a.rps;
-  const size_t smem = attn_smem_bytes(a.chunk, a.head_dim);
-  dim3 grid(a.n_split, a.n_kv_heads, B);
-  if (a.kv.dtype == SPECDEC_BF16)
-    hipLaunchKernelGGL((attn_partial_kernel<uint16_t>), grid, dim3(256), smem, s, a);
-  else
+  if (a.kv.dtype == SPECDEC_BF16) {
+    if (a.chunk != kSplitKeys) return hipErrorInvalidValue;
+    const int nq = a.rps * (a.n_heads / a.n_kv_heads);
+    dim3 grid(a.n_split * ((nq + 15) / 16), a.n_kv_heads, B);
+    switch (a.head_dim) {
+      case 32: hipLaunchKernelGGL((attn_mfma_kernel<32>), grid, dim3(64), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((attn_mfma_kernel<64>), grid, dim3(64), 0, s, a); break;
+      case 128: hipLaunchKernelGGL((attn_mfma_kernel<128>), grid, dim3(64), 0, s, a); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    const size_t smem = attn_smem_bytes(a.chunk, a.head_dim);
+    dim3 grid(a.n_split, a.n_kv_heads, B);
     hipLaunchKernelGGL((attn_partial_kernel<float>), grid, dim3(256), smem, s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), 0, s, a);

@@ -23,17 +23,22 @@ constexpr int kMfmaWaves = kMfmaThreads / kWave;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
 
+__device__ __forceinline__ float load_gain(const void* g, int bf16, int n) {
+  return bf16 ? bf16_bits_to_f32(((const uint16_t*)g)[n]) : ((const float*)g)[n];
+}
+
 // ---------------------------------------------------------------- shared pieces
+// Row scale s_m = 1/sqrt(sum_p ss[p][m] / K + eps): one wave per row, lanes
+// stride over the partial sums, fixed shuffle tree (deterministic).
 template <int MP>
-__device__ __forceinline__ void row_scale_prologue(const GemmArgs& a, float* scale) {
-  for (int m = threadIdx.x; m < MP; m += blockDim.x) {
-    float s = 1.0f;
-    if (a.ss_in && m < a.M) {
-      float t = 0.f;
-      for (int p = 0; p < a.n_ss; ++p) t += a.ss_in[(size_t)p * a.ss_ld + m];
-      s = 1.0f / sqrtf(t / (float)a.K + a.eps);
-    }
-    scale[m] = s;
+__device__ __forceinline__ void row_scale(const GemmArgs& a, float* scale) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int m = wave; m < MP; m += nw) {
+    float t = 0.f;
+    if (a.ss_in && m < a.M)
+      for (int p = lane; p < a.n_ss; p += kWave) t += a.ss_in[(size_t)p * a.ss_ld + m];
+    t = wave_sum(t);
+    if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
   }
 }
 
@@ -56,6 +61,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfi
         float* hp = a.out + (size_t)m * a.ldo + n;
         hv = *hp + yfin[m][c];
         *hp = hv;
+        a.xg_out[(size_t)m * a.ldo + n] = hv * load_gain(a.gain_out, a.gain_bf16, n);
       }
       yfin[m][c] = hv;
     }
@@ -105,7 +111,7 @@ __device__ __forceinline__ const WT* weight_row(const GemmArgs& a, int kind, int
 // per batch of loads.  MFMA operand layout (16x16x32): lane l holds
 // A[l%16][8(l/16)+j] (x rows), B[8(l/16)+j][l%16] (= W[n0 + l%16][k0 + 8(l/16) + j]),
 // D[4(l/16)+r][l%16].
-template <int T, int MT, int UB, int KIND>
+template <int T, int MT, int UB, bool PIPE, int KIND>
 __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a) {
   constexpr int NC = 16 * T;
   constexpr int MP = 16 * MT;
@@ -117,8 +123,6 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a) {
   const int blk = blockIdx.x;
   const int kg = lane >> 4, mrow = lane & 15;
 
-  row_scale_prologue<MP>(a, scale);
-
   const uint16_t* wrow[T];
   bool rok[T];
 #pragma unroll
@@ -127,7 +131,6 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a) {
   const int K = a.K;
   const int KS = (K + 31) / 32;
   const int ks0 = (wave * KS) / kMfmaWaves, ks1 = ((wave + 1) * KS) / kMfmaWaves;
-  const uint16_t* gain = (const uint16_t*)a.gain;
 
   floatx4 acc[T][MT];
 #pragma unroll
@@ -135,9 +138,11 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kb = ks0; kb < ks1; kb += UB) {
-    u32x4 wv[UB][T];
-    f32x4 xv[UB][MT][2];
+  // Two register buffers of UB k-steps: the loads of batch i+1 are in flight
+  // while batch i is multiplied.
+  u32x4 wA[UB][T], wB[UB][T];
+  f32x4 xA[UB][MT][2], xB[UB][MT][2];
+  auto load = [&](int kb, u32x4 (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int k = (kb + u) * 32 + kg * 8;
@@ -160,40 +165,50 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a) {
         }
       }
     }
+  };
+  auto compute = [&](u32x4 (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int k = (kb + u) * 32 + kg * 8;
-      float gv[8];
-      if (gain && (kb + u) < ks1 && k < K) {
-        u32x4 graw = *(const u32x4*)(gain + k);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          gv[2 * j] = __uint_as_float(graw[j] << 16);
-          gv[2 * j + 1] = __uint_as_float(graw[j] & 0xffff0000u);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) gv[j] = 1.0f;
-      }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         bf16x8 hi, lo;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          float v = xv[u][mt][j >> 2][j & 3] * gv[j];
-          __bf16 h = (__bf16)v;
+          const float v = xv[u][mt][j >> 2][j & 3];
+          const __bf16 h = (__bf16)v;
           hi[j] = h;
           lo[j] = (__bf16)(v - (float)h);
         }
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-          bf16x8 b = __builtin_bit_cast(bf16x8, wv[u][t]);
+          const bf16x8 b = __builtin_bit_cast(bf16x8, wv[u][t]);
           acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, b, acc[t][mt], 0, 0, 0);
           acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, b, acc[t][mt], 0, 0, 0);
         }
       }
     }
+  };
+  int kb = ks0;
+  if (PIPE) {
+    if (kb < ks1) load(kb, wA, xA);
+    while (kb < ks1) {
+      if (kb + UB < ks1) load(kb + UB, wB, xB);
+      compute(wA, xA);
+      kb += UB;
+      if (kb >= ks1) break;
+      if (kb + UB < ks1) load(kb + UB, wA, xA);
+      compute(wB, xB);
+      kb += UB;
+    }
+  } else {
+    for (; kb < ks1; kb += UB) {
+      load(kb, wA, xA);
+      compute(wA, xA);
+    }
   }
+
+  // The row scale is only needed by the epilogue: computed after the weight stream.
+  row_scale<MP>(a, scale);
 
   // Cross-wave reduction, fragment by fragment, in a fixed wave order.
 #pragma unroll
@@ -226,8 +241,7 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
   __shared__ float scale[MPMAX];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int blk = blockIdx.x;
-  row_scale_prologue<MPMAX>(a, scale);
-  const float* gain = (const float*)a.gain;
+  row_scale<MPMAX>(a, scale);
   for (int c = wave; c < NC; c += 4) {
     bool ok;
     const float* wr = weight_row<float>(a, KIND, blk, NC, c, ok);
@@ -237,7 +251,7 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
       for (int i = 0; i < 8; ++i) acc[i] = 0.f;
       if (ok) {
         for (int k = lane; k < a.K; k += kWave) {
-          float w = wr[k] * (gain ? gain[k] : 1.0f);
+          float w = wr[k];
 #pragma unroll
           for (int i = 0; i < 8; ++i)
             if (m0 + i < a.M) acc[i] += w * a.x[(size_t)(m0 + i) * a.ldx + k];
@@ -254,21 +268,30 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
   epilogue<NC, KIND>(a, blk, yfin, scale);
 }
 
-// k-steps per batch of loads: keeps the W and x registers of a batch near 64-96
-// VGPRs so that 16 waves (4 per SIMD, 128 registers each) fit without spills.
-constexpr int batch_ksteps(int T, int MT) { return T * MT == 1 ? 6 : ((8 / (T * MT)) > 0 ? 8 / (T * MT) : 1); }
+// k-steps per register buffer and whether two buffers are kept (the next
+// batch's loads in flight while the current one is multiplied): chosen so W
+// and x fragments stay within the 128 VGPRs a wave of a 16-wave block may use.
+template <int T, int MT> struct Batch;
+template <> struct Batch<1, 1> { static constexpr int UB = 4; static constexpr bool PIPE = true; };
+template <> struct Batch<1, 2> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
+template <> struct Batch<1, 4> { static constexpr int UB = 2; static constexpr bool PIPE = false; };
+template <> struct Batch<2, 1> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
+template <> struct Batch<2, 2> { static constexpr int UB = 1; static constexpr bool PIPE = true; };
+template <> struct Batch<2, 4> { static constexpr int UB = 1; static constexpr bool PIPE = false; };
+
+template <int T, int MT, int KIND>
+void launch_mfma_mt(const GemmArgs& a, int blocks, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_bf16_mfma<T, MT, Batch<T, MT>::UB, Batch<T, MT>::PIPE, KIND>), dim3(blocks),
+                     dim3(kMfmaThreads), 0, s, a);
+}
 
 template <int T, int KIND>
 hipError_t launch_mfma_t(const GemmArgs& a, int blocks, hipStream_t s) {
   const int MT = (a.M + 15) / 16;
-  if (MT <= 1)
-    hipLaunchKernelGGL((gemm_bf16_mfma<T, 1, batch_ksteps(T, 1), KIND>), dim3(blocks), dim3(kMfmaThreads), 0, s, a);
-  else if (MT <= 2)
-    hipLaunchKernelGGL((gemm_bf16_mfma<T, 2, batch_ksteps(T, 2), KIND>), dim3(blocks), dim3(kMfmaThreads), 0, s, a);
-  else if (MT <= 4)
-    hipLaunchKernelGGL((gemm_bf16_mfma<T, 4, batch_ksteps(T, 4), KIND>), dim3(blocks), dim3(kMfmaThreads), 0, s, a);
-  else
-    return hipErrorInvalidValue;
+  if (MT <= 1) launch_mfma_mt<T, 1, KIND>(a, blocks, s);
+  else if (MT <= 2) launch_mfma_mt<T, 2, KIND>(a, blocks, s);
+  else if (MT <= 4) launch_mfma_mt<T, 4, KIND>(a, blocks, s);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

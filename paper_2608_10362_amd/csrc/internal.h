@@ -18,10 +18,9 @@ enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 constexpr int kMaxGemmRows = 64;  // rows of x per GEMM launch (callers split larger M)
 
 struct GemmArgs {
-  const float* x;      // [M, ldx]
+  const float* x;      // [M, ldx] (for normalised inputs: h * gain, the producer applies the gain)
   int ldx;
-  const void* gain;    // [K] storage type, or null
-  const float* ss_in;  // [n_ss, ss_ld] partial sums of squares of x rows, or null (no row scale)
+  const float* ss_in;  // [n_ss, ss_ld] partial sums of squares of the h rows, or null (no row scale)
   int n_ss, ss_ld;
   float eps;
   int M, K;
@@ -32,6 +31,9 @@ struct GemmArgs {
   float* out;          // STORE: [M, ldo] ; SWIGLU: [M, ldo] ; RESID: residual [M, ldo] updated in place
   int ldo;
   float* ss_out;       // RESID: [n_blocks, ss_ld] sums of squares of the new residual rows
+  float* xg_out;       // RESID: [M, ldo] new residual times gain_out (input of the next RMSNorm'd GEMM)
+  const void* gain_out;
+  int gain_bf16;
 };
 // Number of row blocks the launcher uses for this GEMM (for ss partial counts).
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M);
@@ -52,9 +54,11 @@ struct RowsArgs {
   int capacity, vocab, d_model, head_dim;
   double rope_base;
   const void* embed;      // [V, d] storage type
+  const void* gain;       // [d] first layer's attention RMSNorm gain
   RowDesc* rows;          // out [M]
   float* rope_cs;         // out [M, head_dim]: cos j<hd/2 then sin
   float* h;               // out [M, d]
+  float* xg;              // out [M, d] h * gain
   float* ss;              // out [M] sum of squares of h rows
 };
 hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s);
@@ -81,7 +85,7 @@ struct AttnArgs {
   float* o;              // [M, h hd]
   int32_t* status;
 };
-int attention_chunk(int head_dim);  // keys per split of the attention kernel
+int attention_chunk(int dtype, int head_dim);  // keys per split of the attention kernel
 hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 

@@ -32,28 +32,25 @@ __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int o) {
 
 struct SampShared {
   uint64_t wave_tot[kSampThreads / kWave];
-  uint64_t total;
   int token;
 };
 
 // Block-wide fixed-point draw over j < V with weights rf(j) (floats >= 0).
-// Thread t owns the contiguous index range [t*per, (t+1)*per).  Returns the
-// token (same value in every thread), or -1 when all weights are zero.
+// Wave w owns the contiguous segment [w*seg, (w+1)*seg) (seg a multiple of
+// 64); lanes read it with unit stride.  Pass 1 sums the integer weights per
+// wave; the wave whose range of the running sum holds t then scans its
+// segment 64 entries at a time.  Returns the token (same value in every
+// thread), or -1 when all weights are zero.
 template <typename RF>
 __device__ int block_draw(RF rf, int V, uint32_t x, SampShared& sh) {
-  const int nt = blockDim.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = nt / kWave;
-  const int per = (V + nt - 1) / nt;
-  const int j0 = min(V, tid * per), j1 = min(V, j0 + per);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x / kWave;
+  const int seg = ((V + nw - 1) / nw + kWave - 1) / kWave * kWave;
+  const int j0 = min(V, wave * seg), j1 = min(V, j0 + seg);
   uint64_t mine = 0;
-  for (int j = j0; j < j1; ++j) mine += fp_weight(rf(j));
-  uint64_t incl = mine;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    uint64_t n = shfl_up_u64(incl, o);
-    if (lane >= o) incl += n;
-  }
+  for (int j = j0 + lane; j < j1; j += kWave) mine += fp_weight(rf(j));
+  mine = wave_sum_u64(mine);
   __syncthreads();
-  if (lane == kWave - 1) sh.wave_tot[wave] = incl;
+  if (lane == 0) sh.wave_tot[wave] = mine;
   if (tid == 0) sh.token = -1;
   __syncthreads();
   uint64_t before = 0, total = 0;
@@ -61,14 +58,25 @@ __device__ int block_draw(RF rf, int V, uint32_t x, SampShared& sh) {
     if (w < wave) before += sh.wave_tot[w];
     total += sh.wave_tot[w];
   }
-  const uint64_t excl = before + incl - mine;
   if (total != 0) {
     const uint64_t t = scale_word(x, total);
-    if (mine != 0 && excl <= t && t < excl + mine) {
-      uint64_t cum = excl;
-      for (int j = j0; j < j1; ++j) {
-        cum += fp_weight(rf(j));
-        if (cum > t) { sh.token = j; break; }
+    if (mine != 0 && before <= t && t < before + mine) {
+      uint64_t cum0 = before;
+      for (int c = j0; c < j1; c += kWave) {
+        const int j = c + lane;
+        uint64_t incl = j < j1 ? fp_weight(rf(j)) : 0ull;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint64_t n = shfl_up_u64(incl, o);
+          if (lane >= o) incl += n;
+        }
+        const unsigned long long hit = __ballot(cum0 + incl > t);
+        if (hit) {
+          const int first = __ffsll(hit) - 1;
+          if (lane == 0) sh.token = c + first;
+          break;
+        }
+        cum0 += __shfl(incl, kWave - 1, kWave);
       }
     }
   }
@@ -126,11 +134,14 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
     a.rope_cs[(size_t)r * hd + half + j] = (float)sin(ang);
   }
   const ET* e = (const ET*)a.embed + (size_t)tok * a.d_model;
+  const ET* gn = (const ET*)a.gain;
   float* h = a.h + (size_t)r * a.d_model;
+  float* xg = a.xg + (size_t)r * a.d_model;
   float ss = 0.f;
   for (int k = threadIdx.x; k < a.d_model; k += blockDim.x) {
     const float v = Storage<ET>::load(e + k);
     h[k] = v;
+    xg[k] = v * Storage<ET>::load(gn + k);
     ss += v * v;
   }
   ss = block_sum(ss, red);
