@@ -187,8 +187,7 @@ def main():
     saved_t, saved_d = kv_t.state.clone(), kv_d.state.clone()
     sd = binding.SpecDecoder(target, draft, kv_t, kv_d, g, T, seed=synth.SEED_SAMPLING)
     torch.cuda.synchronize()
-    log(f"set-up {time.time() - t0:.1f} s (weights {sum(t.numel() for t in dw.t.values()) * 2 / 1e9:.2f} GB "
-        f"+ layers)")
+    log(f"set-up {time.time() - t0:.1f} s (packed weight image {dw.packed.numel() / 1e9:.2f} GB)")
 
     def restore():
         kv_t.state.copy_(saved_t)
@@ -281,25 +280,33 @@ def main():
         acc.append(sd.n_acc.clone())
     mean_A = float(torch.stack(acc).float().mean().item())
 
-    # per-kernel durations (HIP events on the library's stream, eager launches)
+    # Whole-step profile: every launch bracketed by HIP events on the library's stream
+    # (adds a few us per launch; used for the step breakdown only).
     binding.specdec_timing_enable(True)
     for i in range(args.profile_steps):
         draft_part(i); verify_part(i); commit_part()
     torch.cuda.synchronize()
     per = binding.specdec_timing_read()
     binding.specdec_timing_enable(False)
+    step_profile = {k: {"ms_per_step": round(ms / args.profile_steps, 4),
+                        "launches_per_step": n / args.profile_steps} for k, (ms, n) in per.items() if n}
+
+    # Per-kernel durations of the verify pass: each kernel of layer 0 (and the head)
+    # re-launched back to back between HIP events on the library's stream.
+    draft_part(0); verify_part(0)
+    torch.cuda.synchronize()
     kb_verify = kernel_bytes(shape, ctx + g + 1)
+    per_layer = {"embed": 1, "qkv": shape.n_layers, "rope_append": shape.n_layers, "attention": shape.n_layers,
+                 "o_proj": shape.n_layers, "gate_up": shape.n_layers, "down": shape.n_layers, "lm_head": 1}
     kernels = {}
-    for k, (ms, n) in per.items():
-        if n == 0:
-            continue
-        avg_us = ms * 1e3 / n
-        entry = {"avg_us": round(avg_us, 3), "launches_per_step": n / args.profile_steps,
-                 "ms_per_step": round(ms / args.profile_steps, 4)}
-        if k in kb_verify and k != "attention":
-            entry["GBps"] = round(kb_verify[k] / (avg_us * 1e-6) / 1e9, 1)
+    for k, n in per_layer.items():
+        us = binding.specdec_time_kernel(target, k, reps=20)
+        entry = {"avg_us": round(us, 3), "launches_per_verify": n, "ms_per_verify": round(us * n / 1e3, 4)}
+        if k in kb_verify:
+            entry["bytes"] = kb_verify[k]
+            entry["GBps"] = round(kb_verify[k] / (us * 1e-6) / 1e9, 1)
         kernels[k] = entry
-    dom = max((k for k in kernels if k in kb_verify and k != "attention"), key=lambda k: kernels[k]["ms_per_step"])
+    dom = max((k for k in kernels if k in kb_verify and k != "attention"), key=lambda k: kernels[k]["ms_per_verify"])
     dom_bytes = kb_verify[dom]
     achieved = dom_bytes / (kernels[dom]["avg_us"] * 1e-6) / 1e9
     vbytes = verify_step_bytes(shape, ctx, g, B)
@@ -333,6 +340,7 @@ def main():
         "mean_accepted": round(mean_A, 3),
         "device_status": status,
         "kernels": kernels,
+        "step_profile": step_profile,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")

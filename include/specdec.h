@@ -121,14 +121,38 @@ typedef struct {
  * slot, batch*chunk for prefill) and contexts of up to `max_ctx` positions. */
 SPECDEC_API size_t specdec_workspace_bytes(const specdec_model_desc* desc, int32_t max_rows, int32_t max_ctx);
 
+/* Bytes of the packed weight image of a bf16 model's first n_layers_used
+ * layers (0 for float32 models, which run on the row-major weights).
+ * Image layout: the LM head, then per layer Wq, Wk, Wv, Wo, W_gate, W_up,
+ * W_down; each [N, K] matrix is stored as 16-row x 32-column fragments of
+ * 1 KB (fragment (t, s) at byte 1024*(t*ceil(K/32) + s); inside it, lane
+ * l = 16*g + i holds row 16t + i, columns 32s + 8g .. 32s + 8g + 7, zero past
+ * K), the operand order of v_mfma_f32_16x16x32_bf16, so that each wavefront
+ * load of the GEMMs reads 1 KB of contiguous memory.  A prefix of the image
+ * is the image of a layer prefix: a draft can use its target's image. */
+SPECDEC_API size_t specdec_packed_bytes(const specdec_model_desc* desc, int32_t n_layers_used);
+
+/* Write the packed image of the row-major `weights` (first n_layers_used
+ * layers) into `packed` (device, >= specdec_packed_bytes, 256-byte aligned).
+ * Asynchronous on stream; the row-major matrices may be freed once it has
+ * completed.  Errors: INVALID_ARG, SHAPE, UNSUPPORTED (float32 model). */
+SPECDEC_API specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specdec_weights* weights,
+                                                int32_t n_layers_used, void* packed, size_t packed_bytes,
+                                                void* stream);
+
 /* Create a handle over caller-owned weights.  n_layers_used <= desc->n_layers
- * selects a layer prefix (a draft).  `workspace` (device, >= specdec_workspace_bytes,
- * 256-byte aligned) belongs to the handle until specdec_model_destroy; two
- * handles may share one workspace only if their calls never overlap.
- * Launches nothing.
+ * selects a layer prefix (a draft).  bf16 models take their matrices from
+ * `packed` (an image written by specdec_pack_weights covering at least
+ * n_layers_used layers, e.g. the target's image for a draft) and only the
+ * embedding and RMSNorm gains from `weights`; float32 models pass
+ * packed = NULL and use the row-major matrices of `weights`.
+ * `workspace` (device, >= specdec_workspace_bytes, 256-byte aligned) belongs
+ * to the handle until specdec_model_destroy; two handles may share one
+ * workspace only if their calls never overlap.  Launches nothing.
  * Errors: INVALID_ARG (nulls), SHAPE (unsupported dims), HIP. */
 SPECDEC_API specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* weights,
-                                    int32_t n_layers_used, int32_t max_rows, int32_t max_ctx,
+                                    int32_t n_layers_used, const void* packed, size_t packed_bytes,
+                                    int32_t max_rows, int32_t max_ctx,
                                     void* workspace, size_t workspace_bytes, specdec_model** out);
 SPECDEC_API void specdec_model_destroy(specdec_model* model);
 
@@ -271,6 +295,18 @@ SPECDEC_API specdec_status specdec_timing_enable(int32_t enable);
  * (host arrays of SPECDEC_KERNEL_KINDS entries; either may be NULL); resets
  * the accumulators. */
 SPECDEC_API specdec_status specdec_timing_read(double* total_ms, int64_t* launches);
+
+/* Time one kernel in isolation: re-launch the layer-0 launch of kernel kind
+ * `kind` (for SPECDEC_KERNEL_LM_HEAD the head GEMM) recorded by the last
+ * forward pass (verify, draft step or prefill chunk) of `model`, `reps` times
+ * back to back between two HIP events on `stream`, and return the average
+ * duration in microseconds.  Measurement only: the re-launched kernels write
+ * the model's workspace, the same K/V values at that pass's cache positions,
+ * and (residual and head kinds) that pass's hidden state and logits, so the
+ * pass's outputs must be consumed before timing.  Synchronizes the stream.
+ * Errors: INVALID_ARG, UNSUPPORTED (kind not recorded yet), HIP. */
+SPECDEC_API specdec_status specdec_time_kernel(const specdec_model* model, int32_t kind, int32_t reps, void* stream,
+                                               double* avg_us);
 
 /* Synchronize the stream and return the sticky status word of `kv` (also
  * written to *host_out if non-NULL). */

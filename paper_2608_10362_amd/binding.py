@@ -60,9 +60,12 @@ _lib = None
 
 _SIGS = {
     "specdec_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32, ctypes.c_int32]),
+    "specdec_packed_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32]),
+    "specdec_pack_weights": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
+                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "specdec_model_create": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
-                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t,
-                                            ctypes.POINTER(ctypes.c_void_p)]),
+                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_void_p)]),
     "specdec_model_destroy": (None, [ctypes.c_void_p]),
     "specdec_kv_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "specdec_kv_state_count": (ctypes.c_int32, [ctypes.c_int32]),
@@ -99,6 +102,8 @@ _SIGS = {
     "specdec_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "specdec_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
     "specdec_timing_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "specdec_time_kernel": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p]),
 }
 
 KERNEL_KINDS = ("embed", "qkv", "rope_append", "attention", "o_proj", "gate_up", "down", "lm_head", "draft_finish",
@@ -181,14 +186,38 @@ def _to_device(arr, dtype: str, device):
 
 
 class DeviceWeights:
-    """Device copies of a model's weights (from synth's numpy dict, or torch tensors)."""
+    """Device copies of a model's weights (from synth's numpy dict, or torch tensors).
+
+    For bf16 models the matrices are packed once (specdec_pack_weights) into
+    ``self.packed``; the row-major matrices are then released unless
+    ``keep_rowmajor`` is set (the embedding and RMSNorm gains stay).
+    """
 
     KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+    MATS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
-    def __init__(self, shape, weights: Dict, device="cuda"):
+    def __init__(self, shape, weights: Dict, device="cuda", keep_rowmajor: bool = False, stream=None):
+        import torch
         self.shape = shape
         self.t = {k: _to_device(weights[k], shape.dtype, device) for k in ("embed", "lm_head", "final_norm")}
         self.layers = [{k: _to_device(L[k], shape.dtype, device) for k in self.KEYS} for L in weights["layers"]]
+        self.packed = None
+        if shape.dtype == "bf16":
+            desc = make_desc(shape.with_layers(self.n_layers))
+            nbytes = lib().specdec_packed_bytes(ctypes.byref(desc), self.n_layers)
+            if nbytes == 0:
+                raise SpecdecError(-2, "specdec_packed_bytes")
+            self.packed = torch.empty(nbytes, dtype=torch.uint8, device=self.t["embed"].device)
+            w, keep = self.c_struct(self.n_layers)
+            _check(lib().specdec_pack_weights(ctypes.byref(desc), ctypes.byref(w), self.n_layers,
+                                              self.packed.data_ptr(), nbytes, _stream(stream)),
+                   "specdec_pack_weights")
+            torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+            if not keep_rowmajor:
+                self.t["lm_head"] = None
+                for L in self.layers:
+                    for k in self.MATS:
+                        L[k] = None
 
     @property
     def n_layers(self):
@@ -197,9 +226,9 @@ class DeviceWeights:
     def c_struct(self, n_layers: int):
         arrays = {}
         for k in self.KEYS:
-            arr = (ctypes.c_void_p * n_layers)(*[self.layers[l][k].data_ptr() for l in range(n_layers)])
+            arr = (ctypes.c_void_p * n_layers)(*[_ptr(self.layers[l][k]) for l in range(n_layers)])
             arrays[k] = arr
-        w = Weights(self.t["embed"].data_ptr(), self.t["lm_head"].data_ptr(), self.t["final_norm"].data_ptr(),
+        w = Weights(self.t["embed"].data_ptr(), _ptr(self.t["lm_head"]), self.t["final_norm"].data_ptr(),
                     *[ctypes.cast(arrays[k], _PP) for k in self.KEYS])
         return w, arrays
 
@@ -219,7 +248,9 @@ class Model:
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dw.t["embed"].device)
         w, self._arrays = dw.c_struct(n_layers)
         h = ctypes.c_void_p()
-        _check(lib().specdec_model_create(ctypes.byref(self.desc), ctypes.byref(w), n_layers, max_rows, max_ctx,
+        pk = dw.packed
+        _check(lib().specdec_model_create(ctypes.byref(self.desc), ctypes.byref(w), n_layers, _ptr(pk),
+                                          0 if pk is None else pk.numel(), max_rows, max_ctx,
                                           self.workspace.data_ptr(), nbytes, ctypes.byref(h)),
                "specdec_model_create")
         self.handle = h
@@ -383,6 +414,14 @@ def specdec_status_string(status: int) -> str:
 
 def specdec_timing_enable(enable: bool):
     _check(lib().specdec_timing_enable(1 if enable else 0), "specdec_timing_enable")
+
+
+def specdec_time_kernel(model: "Model", kind: str, reps: int = 20, stream=None) -> float:
+    """Average duration (us) of `kind` re-launched back to back (see the header)."""
+    out = ctypes.c_double(0.0)
+    _check(lib().specdec_time_kernel(model.handle, KERNEL_KINDS.index(kind), reps, _stream(stream),
+                                     ctypes.byref(out)), "specdec_time_kernel")
+    return out.value
 
 
 def specdec_timing_read():

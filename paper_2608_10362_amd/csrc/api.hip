@@ -34,6 +34,12 @@ struct specdec_model {
   float* u;
   float* logits;
   int chunk, n_split_max;
+  // layer-0 launches of the last forward pass, for specdec_time_kernel
+  mutable bool rec_valid[SPECDEC_KERNEL_KINDS] = {};
+  mutable GemmArgs rec_gemm[SPECDEC_KERNEL_KINDS];
+  mutable int rec_rows[SPECDEC_KERNEL_KINDS];
+  mutable AttnArgs rec_attn;
+  mutable RowsArgs rec_embed;
 };
 
 namespace {
@@ -127,6 +133,32 @@ specdec_status check_desc(const specdec_model_desc* d) {
 
 specdec_status hip_status(hipError_t e) { return e == hipSuccess ? SPECDEC_OK : SPECDEC_ERR_HIP; }
 
+// Packed image: LM head, then per layer Wq, Wk, Wv, Wo, W_gate, W_up, W_down,
+// each 256-byte aligned.  Returns the bytes and the (N, K, byte offset) list.
+struct PackedMat {
+  int N, K;
+  size_t off;
+};
+size_t image_layout(const specdec_model_desc* d, int n_layers, std::vector<PackedMat>* mats) {
+  const int q = d->n_heads * d->head_dim, kv = d->n_kv_heads * d->head_dim;
+  size_t off = 0;
+  auto add = [&](int N, int K) {
+    if (mats) mats->push_back(PackedMat{N, K, off});
+    off = align_up(off + packed_elems(N, K) * 2);
+  };
+  add(d->vocab, d->d_model);
+  for (int l = 0; l < n_layers; ++l) {
+    add(q, d->d_model);
+    add(kv, d->d_model);
+    add(kv, d->d_model);
+    add(d->d_model, q);
+    add(d->ffn_dim, d->d_model);
+    add(d->ffn_dim, d->d_model);
+    add(d->d_model, d->ffn_dim);
+  }
+  return off;
+}
+
 #define SD_TRY(expr)                                   \
   do {                                                 \
     hipError_t _e = (expr);                            \
@@ -198,6 +230,13 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     Timed t(SPECDEC_KERNEL_EMBED, s);
     SD_TRY(launch_rows_embed(dt, ra, s));
   }
+  m->rec_embed = ra;
+  m->rec_valid[SPECDEC_KERNEL_EMBED] = true;
+  auto rec = [&](int kind, const GemmArgs& g) {
+    m->rec_gemm[kind] = g;
+    m->rec_rows[kind] = M;
+    m->rec_valid[kind] = true;
+  };
 
   GemmArgs base{};
   base.eps = d.rms_eps;
@@ -236,6 +275,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_QKV, s);
       SD_TRY(gemm_rows(dt, q, M, s));
     }
+    if (l == 0) rec(SPECDEC_KERNEL_QKV, q);
 
     at.layer = l;
     {
@@ -246,6 +286,10 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_ATTENTION, s);
       SD_TRY(launch_attention(at, s));
     }
+    if (l == 0) {
+      m->rec_attn = at;
+      m->rec_valid[SPECDEC_KERNEL_ROPE_APPEND] = m->rec_valid[SPECDEC_KERNEL_ATTENTION] = true;
+    }
 
     GemmArgs o = base;  // O projection + residual
     o.x = m->o; o.ldx = H * hd; o.K = H * hd;
@@ -255,6 +299,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_O_PROJ, s);
       SD_TRY(gemm_rows(dt, o, M, s));
     }
+    if (l == 0) rec(SPECDEC_KERNEL_O_PROJ, o);
     n_ss = n_resid_blocks;
 
     GemmArgs gu = base;  // RMSNorm + gate|up + SwiGLU
@@ -266,6 +311,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_GATE_UP, s);
       SD_TRY(gemm_rows(dt, gu, M, s));
     }
+    if (l == 0) rec(SPECDEC_KERNEL_GATE_UP, gu);
 
     GemmArgs dn = base;  // down projection + residual
     dn.x = m->u; dn.ldx = d.ffn_dim; dn.K = d.ffn_dim;
@@ -276,6 +322,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_DOWN, s);
       SD_TRY(gemm_rows(dt, dn, M, s));
     }
+    if (l == 0) rec(SPECDEC_KERNEL_DOWN, dn);
   }
 
   GemmArgs hd_ = base;  // final RMSNorm + LM head
@@ -286,6 +333,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     Timed t(SPECDEC_KERNEL_LM_HEAD, s);
     SD_TRY(gemm_rows(dt, hd_, M, s));
   }
+  rec(SPECDEC_KERNEL_LM_HEAD, hd_);
   return SPECDEC_OK;
 }
 
@@ -308,9 +356,41 @@ size_t specdec_workspace_bytes(const specdec_model_desc* desc, int32_t max_rows,
   return ws_layout(desc, max_rows, max_ctx).total;
 }
 
+size_t specdec_packed_bytes(const specdec_model_desc* desc, int32_t n_layers_used) {
+  if (check_desc(desc) != SPECDEC_OK || n_layers_used <= 0 || n_layers_used > desc->n_layers) return 0;
+  if (desc->dtype != SPECDEC_BF16) return 0;
+  return image_layout(desc, n_layers_used, nullptr);
+}
+
+specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
+                                    void* packed, size_t packed_bytes, void* stream) {
+  specdec_status st = check_desc(desc);
+  if (st != SPECDEC_OK) return st;
+  if (desc->dtype != SPECDEC_BF16) return SPECDEC_ERR_UNSUPPORTED;
+  if (!w || !packed || n_layers_used <= 0 || n_layers_used > desc->n_layers) return SPECDEC_ERR_INVALID_ARG;
+  if ((uintptr_t)packed % kAlign) return SPECDEC_ERR_INVALID_ARG;
+  std::vector<PackedMat> mats;
+  if (packed_bytes < image_layout(desc, n_layers_used, &mats)) return SPECDEC_ERR_INVALID_ARG;
+  if (!w->lm_head || !w->wq || !w->wk || !w->wv || !w->wo || !w->w_gate || !w->w_up || !w->w_down)
+    return SPECDEC_ERR_INVALID_ARG;
+  std::vector<const void*> src;
+  src.push_back(w->lm_head);
+  for (int l = 0; l < n_layers_used; ++l) {
+    const void* m[7] = {w->wq[l], w->wk[l], w->wv[l], w->wo[l], w->w_gate[l], w->w_up[l], w->w_down[l]};
+    for (const void* p : m) {
+      if (!p) return SPECDEC_ERR_INVALID_ARG;
+      src.push_back(p);
+    }
+  }
+  hipStream_t s = (hipStream_t)stream;
+  for (size_t i = 0; i < mats.size(); ++i)
+    SD_TRY(launch_pack(src[i], (char*)packed + mats[i].off, mats[i].N, mats[i].K, s));
+  return SPECDEC_OK;
+}
+
 specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
-                                    int32_t max_rows, int32_t max_ctx, void* workspace, size_t workspace_bytes,
-                                    specdec_model** out) {
+                                    const void* packed, size_t packed_bytes, int32_t max_rows, int32_t max_ctx,
+                                    void* workspace, size_t workspace_bytes, specdec_model** out) {
   if (!out) return SPECDEC_ERR_INVALID_ARG;
   *out = nullptr;
   specdec_status st = check_desc(desc);
@@ -320,13 +400,23 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   if ((uintptr_t)workspace % kAlign) return SPECDEC_ERR_INVALID_ARG;
   const WsLayout L = ws_layout(desc, max_rows, max_ctx);
   if (workspace_bytes < L.total) return SPECDEC_ERR_INVALID_ARG;
-  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo ||
-      !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+  const bool bf16 = desc->dtype == SPECDEC_BF16;
+  std::vector<PackedMat> mats;
+  if (bf16) {
+    if (!packed || (uintptr_t)packed % kAlign) return SPECDEC_ERR_INVALID_ARG;
+    if (packed_bytes < image_layout(desc, n_layers_used, &mats)) return SPECDEC_ERR_INVALID_ARG;
+  } else if (packed) {
     return SPECDEC_ERR_INVALID_ARG;
-  for (int l = 0; l < n_layers_used; ++l)
-    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->ffn_norm[l] || !w->w_gate[l] ||
-        !w->w_up[l] || !w->w_down[l])
+  }
+  if (!w->embed || !w->final_norm || !w->attn_norm || !w->ffn_norm) return SPECDEC_ERR_INVALID_ARG;
+  if (!bf16 && (!w->lm_head || !w->wq || !w->wk || !w->wv || !w->wo || !w->w_gate || !w->w_up || !w->w_down))
+    return SPECDEC_ERR_INVALID_ARG;
+  for (int l = 0; l < n_layers_used; ++l) {
+    if (!w->attn_norm[l] || !w->ffn_norm[l]) return SPECDEC_ERR_INVALID_ARG;
+    if (!bf16 && (!w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->w_gate[l] || !w->w_up[l] ||
+                  !w->w_down[l]))
       return SPECDEC_ERR_INVALID_ARG;
+  }
 
   specdec_model* m = new specdec_model();
   m->desc = *desc;
@@ -334,17 +424,32 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   m->max_rows = max_rows;
   m->max_ctx = max_ctx;
   m->embed = w->embed;
-  m->lm_head = w->lm_head;
   m->final_norm = w->final_norm;
   m->attn_norm.assign(w->attn_norm, w->attn_norm + n_layers_used);
-  m->wq.assign(w->wq, w->wq + n_layers_used);
-  m->wk.assign(w->wk, w->wk + n_layers_used);
-  m->wv.assign(w->wv, w->wv + n_layers_used);
-  m->wo.assign(w->wo, w->wo + n_layers_used);
   m->ffn_norm.assign(w->ffn_norm, w->ffn_norm + n_layers_used);
-  m->w_gate.assign(w->w_gate, w->w_gate + n_layers_used);
-  m->w_up.assign(w->w_up, w->w_up + n_layers_used);
-  m->w_down.assign(w->w_down, w->w_down + n_layers_used);
+  if (bf16) {  // matrices from the packed image
+    const char* img = (const char*)packed;
+    m->lm_head = img + mats[0].off;
+    for (int l = 0; l < n_layers_used; ++l) {
+      const PackedMat* p = &mats[1 + 7 * l];
+      m->wq.push_back(img + p[0].off);
+      m->wk.push_back(img + p[1].off);
+      m->wv.push_back(img + p[2].off);
+      m->wo.push_back(img + p[3].off);
+      m->w_gate.push_back(img + p[4].off);
+      m->w_up.push_back(img + p[5].off);
+      m->w_down.push_back(img + p[6].off);
+    }
+  } else {
+    m->lm_head = w->lm_head;
+    m->wq.assign(w->wq, w->wq + n_layers_used);
+    m->wk.assign(w->wk, w->wk + n_layers_used);
+    m->wv.assign(w->wv, w->wv + n_layers_used);
+    m->wo.assign(w->wo, w->wo + n_layers_used);
+    m->w_gate.assign(w->w_gate, w->w_gate + n_layers_used);
+    m->w_up.assign(w->w_up, w->w_up + n_layers_used);
+    m->w_down.assign(w->w_down, w->w_down + n_layers_used);
+  }
   char* base = (char*)workspace;
   m->rows = (RowDesc*)(base + L.rows);
   m->rope_cs = (float*)(base + L.rope);
@@ -646,6 +751,40 @@ specdec_status specdec_timing_read(double* total_ms, int64_t* launches) {
     if (launches) launches[k] = n[k];
   }
   return st;
+}
+
+specdec_status specdec_time_kernel(const specdec_model* m, int32_t kind, int32_t reps, void* stream,
+                                   double* avg_us) {
+  if (!m || !avg_us || reps <= 0 || kind < 0 || kind >= SPECDEC_KERNEL_KINDS) return SPECDEC_ERR_INVALID_ARG;
+  if (!m->rec_valid[kind]) return SPECDEC_ERR_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  const int dt = m->desc.dtype;
+  auto launch = [&]() -> hipError_t {
+    switch (kind) {
+      case SPECDEC_KERNEL_EMBED: return launch_rows_embed(dt, m->rec_embed, s);
+      case SPECDEC_KERNEL_ROPE_APPEND: return launch_rope_append(m->rec_attn, s);
+      case SPECDEC_KERNEL_ATTENTION: return launch_attention(m->rec_attn, s);
+      default: return gemm_rows(dt, m->rec_gemm[kind], m->rec_rows[kind], s);
+    }
+  };
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  SD_TRY(hipEventCreate(&e0));
+  if (hipEventCreate(&e1) != hipSuccess) {
+    (void)hipEventDestroy(e0);
+    return SPECDEC_ERR_HIP;
+  }
+  hipError_t err = launch();  // warm-up
+  if (err == hipSuccess) err = hipEventRecord(e0, s);
+  for (int i = 0; i < reps && err == hipSuccess; ++i) err = launch();
+  if (err == hipSuccess) err = hipEventRecord(e1, s);
+  if (err == hipSuccess) err = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (err != hipSuccess) return SPECDEC_ERR_HIP;
+  *avg_us = 1e3 * (double)ms / reps;
+  return SPECDEC_OK;
 }
 
 const char* specdec_status_string(specdec_status s) {

@@ -334,7 +334,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------- combine
+// Block (head, row): weights w_c = exp(m_c - max_c m_c) of the row's chunks
+// in LDS (fixed-order reductions), then o = sum_c w_c o_c / sum_c w_c l_c with
+// the chunk loop unrolled so the partial loads overlap.
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
+  extern __shared__ float wsh[];  // [n_split]
+  __shared__ float red[16];
   const int head = blockIdx.x, r = blockIdx.y;
   const int hd = a.head_dim, H = a.n_heads;
   const RowDesc rd = a.rows[r];
@@ -350,14 +355,28 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   }
   const size_t base = ((size_t)r * H + head) * a.n_split;
   float mx = -INFINITY;
-  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, a.ml_part[2 * (base + c)]);
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) mx = fmaxf(mx, a.ml_part[2 * (base + c)]);
+  mx = block_max(mx, red);
   float L = 0.f;
-  for (int c = 0; c < nch; ++c) L += expf(a.ml_part[2 * (base + c)] - mx) * a.ml_part[2 * (base + c) + 1];
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+    const float w = expf(a.ml_part[2 * (base + c)] - mx);
+    wsh[c] = w;
+    L += w * a.ml_part[2 * (base + c) + 1];
+  }
+  L = block_sum(L, red);  // its barrier also publishes wsh
   const float inv = 1.0f / L;
+  const float* op = a.o_part + base * hd;
   for (int dd = threadIdx.x; dd < hd; dd += blockDim.x) {
-    float acc = 0.f;
-    for (int c = 0; c < nch; ++c) acc += expf(a.ml_part[2 * (base + c)] - mx) * a.o_part[(base + c) * hd + dd];
-    o[dd] = acc * inv;
+    float acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
+    int c = 0;
+    for (; c + 4 <= nch; c += 4) {
+      acc0 += wsh[c] * op[(size_t)c * hd + dd];
+      acc1 += wsh[c + 1] * op[(size_t)(c + 1) * hd + dd];
+      acc2 += wsh[c + 2] * op[(size_t)(c + 2) * hd + dd];
+      acc3 += wsh[c + 3] * op[(size_t)(c + 3) * hd + dd];
+    }
+    for (; c < nch; ++c) acc0 += wsh[c] * op[(size_t)c * hd + dd];
+    o[dd] = ((acc0 + acc1) + (acc2 + acc3)) * inv;
   }
 }
 
@@ -420,7 +439,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), 0, s, a);
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), sizeof(float) * a.n_split, s, a);
   return hipGetLastError();
 }
 

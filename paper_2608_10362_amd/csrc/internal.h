@@ -24,7 +24,7 @@ struct GemmArgs {
   int n_ss, ss_ld;
   float eps;
   int M, K;
-  const void* w[3];
+  const void* w[3];    // bf16: packed images of the segments; f32: row-major [n_seg, K]
   int n_seg[3];
   int n_rows;          // total rows over segments (STORE/RESID); F for SWIGLU
   int kind;
@@ -35,6 +35,9 @@ struct GemmArgs {
   const void* gain_out;
   int gain_bf16;
 };
+// Packed bf16 weight image (16-row x 32-column 1 KB fragments in MFMA operand order).
+size_t packed_elems(int N, int K);
+hipError_t launch_pack(const void* src, void* dst, int N, int K, hipStream_t s);
 // Number of row blocks the launcher uses for this GEMM (for ss partial counts).
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M);
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);

@@ -84,6 +84,63 @@ __device__ int block_draw(RF rf, int V, uint32_t x, SampShared& sh) {
   return sh.token;
 }
 
+// Online (max, sum exp) of z_j = row[j] / T over a row, block-wide, one pass.
+// Elements are read four at a time when the row is 16-byte aligned.  The
+// per-thread states are merged in a fixed order (deterministic).
+struct MaxSum {
+  float m, s;
+};
+__device__ __forceinline__ void ms_add(MaxSum& a, float z) {
+  if (z > a.m) {
+    a.s = a.s * expf(a.m - z) + 1.0f;
+    a.m = z;
+  } else {
+    a.s += expf(z - a.m);
+  }
+}
+__device__ __forceinline__ MaxSum ms_merge(MaxSum a, MaxSum b) {
+  if (b.m == -INFINITY) return a;
+  if (a.m == -INFINITY) return b;
+  const float m = fmaxf(a.m, b.m);
+  return MaxSum{m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
+}
+__device__ MaxSum block_max_sum(const float* row, int V, float T, float* red2) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nt / kWave;
+  MaxSum st{-INFINITY, 0.f};
+  if ((V & 3) == 0 && ((uintptr_t)row & 15) == 0) {
+    const f32x4* r4 = (const f32x4*)row;
+    const int V4 = V >> 2;
+    int j = tid;
+    for (; j + 3 * nt < V4; j += 4 * nt) {
+      f32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = r4[j + u * nt];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ms_add(st, v[u][e] / T);
+    }
+    for (; j < V4; j += nt) {
+      const f32x4 v = r4[j];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ms_add(st, v[e] / T);
+    }
+  } else {
+    for (int j = tid; j < V; j += nt) ms_add(st, row[j] / T);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    MaxSum other{__shfl_xor(st.m, o, kWave), __shfl_xor(st.s, o, kWave)};
+    st = ms_merge(st, other);
+  }
+  __syncthreads();
+  if (lane == 0) { red2[2 * wave] = st.m; red2[2 * wave + 1] = st.s; }
+  __syncthreads();
+  MaxSum tot{red2[0], red2[1]};
+  for (int w = 1; w < nw; ++w) tot = ms_merge(tot, MaxSum{red2[2 * w], red2[2 * w + 1]});
+  return tot;
+}
+
 // ---------------------------------------------------------------- rows + embedding
 template <typename ET>
 __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
@@ -151,6 +208,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
 // ---------------------------------------------------------------- draft finish
 __global__ __launch_bounds__(kSampThreads) void draft_finish_kernel(DraftFinishArgs a) {
   __shared__ float redf[16];
+  __shared__ float red2[32];
   __shared__ int redi[16];
   __shared__ SampShared sh;
   const int b = blockIdx.x, V = a.V, tid = threadIdx.x, nt = blockDim.x;
@@ -178,12 +236,8 @@ __global__ __launch_bounds__(kSampThreads) void draft_finish_kernel(DraftFinishA
     tok = bi;
   } else {
     const float T = a.temperature;
-    float mx = -INFINITY;
-    for (int j = tid; j < V; j += nt) mx = fmaxf(mx, lg[j] / T);
-    mx = block_max(mx, redf);
-    float s = 0.f;
-    for (int j = tid; j < V; j += nt) s += expf(lg[j] / T - mx);
-    s = block_sum(s, redf);
+    const MaxSum st = block_max_sum(lg, V, T, red2);
+    const float mx = st.m, s = st.s;
     auto qf = [&](int j) { return expf(lg[j] / T - mx) / s; };
     if (a.q_out) {
       float* qo = a.q_out + ((size_t)b * a.gamma + a.slot) * V;
@@ -198,6 +252,7 @@ __global__ __launch_bounds__(kSampThreads) void draft_finish_kernel(DraftFinishA
 // ---------------------------------------------------------------- accept / resample
 __global__ __launch_bounds__(kSampThreads) void accept_kernel(AcceptArgs a) {
   __shared__ float redf[16];
+  __shared__ float red2[32];
   __shared__ int redi[16];
   __shared__ float rmax[kMaxGamma + 1], rsum[kMaxGamma + 1];
   __shared__ SampShared sh;
@@ -232,16 +287,10 @@ __global__ __launch_bounds__(kSampThreads) void accept_kernel(AcceptArgs a) {
     for (int i = 0; i <= g; ++i) {
       const float* row = P + (size_t)i * V;
       if (logits) {
-        float mx = -INFINITY;
-        for (int j = tid; j < V; j += nt) {
-          bad |= !isfinite(row[j]);
-          mx = fmaxf(mx, row[j] / T);
-        }
-        mx = block_max(mx, redf);
-        float s = 0.f;
-        for (int j = tid; j < V; j += nt) s += expf(row[j] / T - mx);
-        s = block_sum(s, redf);
-        if (tid == 0) { rmax[i] = mx; rsum[i] = s; }
+        const MaxSum st = block_max_sum(row, V, T, red2);
+        // a NaN/Inf logit makes the row's max or sum non-finite
+        bad |= !isfinite(st.m) || !isfinite(st.s);
+        if (tid == 0) { rmax[i] = st.m; rsum[i] = st.s; }
       } else {
         for (int j = tid; j < V; j += nt) bad |= !isfinite(row[j]);
       }

@@ -36,7 +36,7 @@ def test_header_declares_the_four_hot_path_calls():
 
 def test_every_declared_symbol_is_exported(lib):
     names = _declared()
-    assert len(names) >= 19
+    assert len(names) >= 21
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(binding._SIGS), "binding signatures out of sync with the header"
@@ -67,20 +67,33 @@ def test_model_create_argument_errors(lib):
     w = binding.Weights()
     fake = ctypes.c_void_p(256)  # never dereferenced: creation fails before any use
     # null weights struct
-    assert lib.specdec_model_create(ctypes.byref(d), None, 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    assert lib.specdec_model_create(ctypes.byref(d), None, 1, None, 0, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
     # null per-layer arrays
-    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 1, None, 0, 8, 128, fake, 1 << 30,
+                                    ctypes.byref(h)) == -1
     # too many layers
-    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 3, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -1
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w), 3, None, 0, 8, 128, fake, 1 << 30,
+                                    ctypes.byref(h)) == -1
     # unsupported shape
     bad = binding.make_desc(synth.TINY)
     bad.d_model = 100
-    assert lib.specdec_model_create(ctypes.byref(bad), ctypes.byref(w), 1, 8, 128, fake, 1 << 30, ctypes.byref(h)) == -2
+    assert lib.specdec_model_create(ctypes.byref(bad), ctypes.byref(w), 1, None, 0, 8, 128, fake, 1 << 30,
+                                    ctypes.byref(h)) == -2
     # workspace too small
     arr = (ctypes.c_void_p * 2)(256, 256)
     pp = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
     w2 = binding.Weights(256, 256, 256, *([pp] * 9))
-    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w2), 1, 8, 128, fake, 16, ctypes.byref(h)) == -1
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w2), 1, None, 0, 8, 128, fake, 16,
+                                    ctypes.byref(h)) == -1
+    # a float32 model takes no packed image; a bf16 model needs one of the right size
+    assert lib.specdec_model_create(ctypes.byref(d), ctypes.byref(w2), 1, fake, 1 << 30, 8, 128, fake, 1 << 30,
+                                    ctypes.byref(h)) == -1
+    d16 = binding.make_desc(synth.LLAMA_1B)
+    need = lib.specdec_packed_bytes(ctypes.byref(d16), 2)
+    assert need > 0 and lib.specdec_packed_bytes(ctypes.byref(d), 1) == 0
+    assert lib.specdec_model_create(ctypes.byref(d16), ctypes.byref(w2), 2, fake, need - 1, 8, 128, fake, 1 << 40,
+                                    ctypes.byref(h)) == -1
+    assert lib.specdec_pack_weights(ctypes.byref(d), ctypes.byref(w2), 1, fake, 1 << 30, None) == -6
     assert not h.value
 
 
