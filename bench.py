@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one 1 GiB device-to-device copy (reference for the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -115,6 +117,25 @@ def verify_step_bytes(shape, ctx, gamma, batch):
     weights = L * per_layer + (V * d + d) * e + batch * (gamma + 1) * d * e
     kv_row = shape.n_kv_heads * shape.head_dim * 2 * e * L
     return weights + batch * ctx * kv_row + batch * (gamma + 1) * kv_row
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of the dominant GEMM from the committed rocprofv3 counter summary
+    (profiles/gemm_<kind>_7b_hbm_traffic.md), or None if absent or taken on other kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"gemm_{kernel}_7b_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(("|", "#", "`")):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2608_10362_amd", "csrc", "gemm.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get("kernel_source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
+        return None
+    return int(float(fields["traffic_bytes_per_launch"]))
 
 
 # ---------------------------------------------------------------- CPU oracle baseline
@@ -280,6 +301,14 @@ def main():
         acc.append(sd.n_acc.clone())
     mean_A = float(torch.stack(acc).float().mean().item())
 
+    if args.copy_calibration:  # a plain copy of known size for scaling FETCH_SIZE / WRITE_SIZE
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     # Whole-step profile: every launch bracketed by HIP events on the library's stream
     # (adds a few us per launch; used for the step breakdown only).
     binding.specdec_timing_enable(True)
@@ -331,7 +360,7 @@ def main():
                    "hip_graph": use_graph},
         "roofline": {"bound": "hbm", "kernel": f"gemm {dom}", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": None, "bytes_per_launch": dom_bytes},
+                     "traffic": measured_traffic(dom), "bytes_per_launch": dom_bytes},
         "verify_ms": round(verify_ms, 4),
         "verify_hbm_GBps": round(verify_GBps, 1),
         "verify_hbm_frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
