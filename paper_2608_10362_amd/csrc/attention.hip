@@ -1,19 +1,22 @@
 // RoPE + KV append and GQA attention of the verify / draft passes against the
 // resident KV cache.
 //
-// KV layout (per layer l, sequence b, kv head g), storage type KT:
-//   K block [capacity][head_dim]  (row = position)
-//   V block [head_dim][capacity]  (transposed: a row = one dimension over positions)
-// at element offset ((l*B + b)*h_kv + g) * 2*capacity*head_dim (V after K).
-// The transposed V makes both operands of softmax(QK^T)V read contiguous
-// position runs.
+// KV layout (per layer l, sequence b, kv head g): a K block then a V block of
+// capacity*head_dim elements each, at element offset
+// ((l*B + b)*h_kv + g) * 2*capacity*head_dim.
+//  * bf16 caches store both in MFMA operand order, in 1 KB fragments, so that
+//    every wavefront load of the attention kernel reads 1 KB contiguously:
+//    K fragment (16 positions x 32 dims): lane 16*(d%32/8) + p%16, element d%8;
+//    V fragment (32 positions x 16 dims): lane 16*(p%32/8) + d%16, element p%8.
+//  * float32 caches (the tiny configuration): K row-major [position][dim],
+//    V transposed [dim][position].
 //
-// Attention is split over key chunks (flash-decoding style): one block per
-// (chunk, kv head, sequence) computes, for every query row of the sequence
-// and every query head of the kv group, the chunk's max, exp-sum and
-// unnormalised P V; a combine kernel merges the chunks per (row, head).  Query
-// i of a sequence at position pos_i sees keys 0..pos_i (causal inside the
-// verify block).
+// Attention is split over key chunks (flash-decoding style): one wave per
+// (16-query tile, 64-key split, kv head, sequence) computes, for every query
+// row of the sequence and every query head of the kv group, the chunk's max,
+// exp-sum and unnormalised P V; a combine kernel merges the chunks per (row,
+// head).  Query i of a sequence at position pos_i sees keys 0..pos_i (causal
+// inside the verify block).
 #include "device_common.h"
 #include "internal.h"
 
@@ -27,6 +30,24 @@ __device__ __forceinline__ KT* k_block(const KvLayout& kv, int layer, int b, int
   return (KT*)kv.data + off;
 }
 
+// Element offsets of K[p][d] and V[p][d] inside a (layer, sequence, kv head) block.
+template <typename KT> struct KvIndex;
+template <> struct KvIndex<float> {
+  __device__ static size_t k(int p, int d, int hd, int cap) { return (size_t)p * hd + d; }
+  __device__ static size_t v(int p, int d, int hd, int cap) { return (size_t)cap * hd + (size_t)d * cap + p; }
+};
+template <> struct KvIndex<uint16_t> {
+  __device__ static size_t k(int p, int d, int hd, int cap) {
+    const int kst = hd / 32;
+    return ((size_t)((p >> 4) * kst + (d >> 5)) * 64 + ((d & 31) >> 3) * 16 + (p & 15)) * 8 + (d & 7);
+  }
+  __device__ static size_t v(int p, int d, int hd, int cap) {
+    const int dt = hd / 16;
+    return (size_t)cap * hd + ((size_t)((p >> 5) * dt + (d >> 4)) * 64 + ((p & 31) >> 3) * 16 + (d & 15)) * 8 +
+           (p & 7);
+  }
+};
+
 // ---------------------------------------------------------------- RoPE + append
 // Block (head slot, row): slots [0, H) rotate a query head into qr, [H, H+G)
 // rotate a key head and store it at the row's position, [H+G, H+2G) store a
@@ -39,11 +60,12 @@ __global__ __launch_bounds__(64) void rope_append_kernel(AttnArgs a) {
   const RowDesc rd = a.rows[r];
   const float* src = a.qkv + (size_t)r * (H + 2 * G) * hd + (size_t)hs * hd;
   const float x1 = src[j], x2 = src[j + half];
+  const int cap = a.kv.capacity;
   if (hs >= H + G) {  // value head
     if (!rd.valid) return;
-    KT* vb = k_block<KT>(a.kv, a.layer, rd.b, hs - H - G) + (size_t)a.kv.capacity * hd;
-    Storage<KT>::store(vb + (size_t)j * a.kv.capacity + rd.pos, x1);
-    Storage<KT>::store(vb + (size_t)(j + half) * a.kv.capacity + rd.pos, x2);
+    KT* blk = k_block<KT>(a.kv, a.layer, rd.b, hs - H - G);
+    Storage<KT>::store(blk + KvIndex<KT>::v(rd.pos, j, hd, cap), x1);
+    Storage<KT>::store(blk + KvIndex<KT>::v(rd.pos, j + half, hd, cap), x2);
     return;
   }
   const float* cs = a.rope_cs + (size_t)r * hd;
@@ -54,9 +76,9 @@ __global__ __launch_bounds__(64) void rope_append_kernel(AttnArgs a) {
     q[j] = y1;
     q[j + half] = y2;
   } else if (rd.valid) {
-    KT* kb = k_block<KT>(a.kv, a.layer, rd.b, hs - H) + (size_t)rd.pos * hd;
-    Storage<KT>::store(kb + j, y1);
-    Storage<KT>::store(kb + j + half, y2);
+    KT* blk = k_block<KT>(a.kv, a.layer, rd.b, hs - H);
+    Storage<KT>::store(blk + KvIndex<KT>::k(rd.pos, j, hd, cap), y1);
+    Storage<KT>::store(blk + KvIndex<KT>::k(rd.pos, j + half, hd, cap), y2);
   }
 }
 
@@ -195,51 +217,14 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   const int rps = a.rps, r0 = b * rps, nq = rps * group;
   const int split = blockIdx.x % a.n_split, mt = blockIdx.x / a.n_split;
   if (mt * 16 >= nq) return;
-  int nk = 0;
-  for (int i = 0; i < rps; ++i) {
-    const RowDesc rd = a.rows[r0 + i];
-    if (rd.valid) nk = max(nk, rd.pos + 1);
-  }
-  const int k0 = split * kSplitKeys;
-  if (k0 >= nk) return;
   const int c16 = lane & 15, grp = lane >> 4;
+  const int k0 = split * kSplitKeys;
+  if (k0 >= a.kv.capacity) return;
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
   const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;
 
-  // K and V fragments of the whole split, issued first (the bytes in flight).
-  u32x4 kf[NT][KST];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int key = k0 + 16 * t + c16;
-#pragma unroll
-    for (int c = 0; c < KST; ++c)
-      kf[t][c] = key < nk ? *(const u32x4*)(kb + (size_t)key * HD + 32 * c + 8 * grp) : u32x4{0u, 0u, 0u, 0u};
-  }
-  u32x4 vf[2][DT];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int key = k0 + 32 * s + 8 * grp;  // first of this lane's 8 keys
-    const int nvalid = min(8, nk - key);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (nvalid > 0) {
-        v = *(const u32x4*)(vb + (size_t)(dt * 16 + c16) * a.kv.capacity + key);
-        if (nvalid < 8) {  // keys past the context: zero (never multiply stale memory)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (2 * j >= nvalid) v[j] = 0u;
-            else if (2 * j + 1 >= nvalid) v[j] &= 0xffffu;
-          }
-        }
-      }
-      vf[s][dt] = v;
-    }
-  }
-
-  // Q fragments (A operand): query qa = mt*16 + l%16, pre-scaled by 1/sqrt(hd).
-  const float scale = 1.0f / sqrtf((float)HD);
-  bf16x8 qhi[KST], qlo[KST];
+  // Q fragments (A operand) first: query qa = mt*16 + l%16, pre-scaled by 1/sqrt(hd).
+  float qv[KST][8];
   {
     const int qa = mt * 16 + c16;
     const float* qp = nullptr;
@@ -249,22 +234,72 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int c = 0; c < KST; ++c) {
-      float v[8];
+      if (qp) {
+        const f32x4* q4 = (const f32x4*)(qp + 32 * c + 8 * grp);
+        const f32x4 lo4 = q4[0], hi4 = q4[1];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = qp ? qp[32 * c + 8 * grp + j] * scale : 0.f;
-      split_hilo(v, qhi[c], qlo[c]);
+        for (int j = 0; j < 4; ++j) { qv[c][j] = lo4[j]; qv[c][4 + j] = hi4[j]; }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qv[c][j] = 0.f;
+      }
     }
   }
+  // K and V fragments of the whole split: 2 x 16 contiguous 1 KB fragments,
+  // issued before anything waits (k0 + 64 <= capacity: always in bounds).
+  u32x4 kf[NT][KST];
+  const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
+  u32x4 vf[2][DT];
+  const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[s][dt] = *(const u32x4*)(vfrag + (size_t)(s * DT + dt) * 512);
+
+  // Row descriptors: lane i < rps reads row i; nk = max(pos) + 1 over valid rows.
+  int mypos = -1;
+  if (lane < rps) {
+    const RowDesc rd = a.rows[r0 + lane];
+    if (rd.valid) mypos = rd.pos;
+  }
+  int nk = mypos + 1;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
+  if (k0 >= nk) return;
   // positions of the 4 query rows this lane holds in the C layout (-1: none)
   int qpos[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int qc = mt * 16 + 4 * grp + r;
-    qpos[r] = -1;
-    if (qc < nq) {
-      const RowDesc rd = a.rows[r0 + qc / group];
-      if (rd.valid) qpos[r] = rd.pos;
+    const int p = __shfl(mypos, min(qc, nq - 1) / group, kWave);
+    qpos[r] = qc < nq ? p : -1;
+  }
+  // keys past the context: zero their V entries (never multiply stale memory)
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int nvalid = nk - (k0 + 32 * s + 8 * grp);
+    if (nvalid < 8) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (2 * j >= nvalid) vf[s][dt][j] = 0u;
+          else if (2 * j + 1 >= nvalid) vf[s][dt][j] &= 0xffffu;
+        }
     }
+  }
+  const float scale = 1.0f / sqrtf((float)HD);
+  bf16x8 qhi[KST], qlo[KST];
+#pragma unroll
+  for (int c = 0; c < KST; ++c) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = qv[c][j] * scale;
+    split_hilo(v, qhi[c], qlo[c]);
   }
 
   floatx4 sf[NT];
@@ -388,10 +423,9 @@ __global__ __launch_bounds__(256) void kv_copy_kernel(KvLayout kv, int layer, in
   const int hd = kv.head_dim, G = kv.n_kv_heads;
   for (int i = threadIdx.x; i < G * hd; i += blockDim.x) {
     const int g = i / hd, dd = i % hd;
-    KT* kb = k_block<KT>(kv, layer, b, g);
-    KT* vb = kb + (size_t)kv.capacity * hd;
-    KT* kc = kb + (size_t)(pos0 + p) * hd + dd;
-    KT* vc = vb + (size_t)dd * kv.capacity + pos0 + p;
+    KT* blk = k_block<KT>(kv, layer, b, g);
+    KT* kc = blk + KvIndex<KT>::k(pos0 + p, dd, hd, kv.capacity);
+    KT* vc = blk + KvIndex<KT>::v(pos0 + p, dd, hd, kv.capacity);
     const size_t src = ((size_t)p * G + g) * hd + dd;
     if (k) *kc = k[src];
     if (v) *vc = v[src];
