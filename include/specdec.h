@@ -234,12 +234,24 @@ SPECDEC_API specdec_status specdec_verify(const specdec_model* target, specdec_k
  * max(0, fl32(p_i - q_i)) (from p_i if that is all zero); if all accepted emit
  * a draw from p_{gamma+1}.  Greedy (temperature == 0): A = length of the
  * prefix where d_i equals argmax p_i; emit argmax p_{A+1}.
- * Outputs n_accepted[b] = A in [0, gamma], next_token[b].  NaN/Inf inputs set
- * *status = SPECDEC_ERR_NONFINITE (device int32, sticky) and write A = -1. */
+ * Outputs n_accepted[b] = A in [0, gamma], next_token[b].  A NaN or Inf
+ * anywhere in p (either kind) or, when sampling, in q, or a drafted token
+ * outside [0, V) when sampling, sets *status = SPECDEC_ERR_NONFINITE (device
+ * int32, sticky, may be NULL) and writes A = -1, next_token = -1.
+ * workspace: device scratch of at least specdec_accept_workspace_bytes(batch,
+ * gamma, vocab) bytes, 256-byte aligned, owned by the caller; its contents
+ * need no initialisation and are dead after the call.  Calls that share a
+ * workspace must be ordered on one stream.
+ * Errors: INVALID_ARG (also for a missing or short workspace), UNSUPPORTED
+ * (gamma > 31). */
 SPECDEC_API specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
                               const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
                               uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
-                              int32_t* status, void* stream);
+                              int32_t* status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the accept workspace for `batch` sequences of gamma+1 rows over a
+ * vocabulary of `vocab` (0 for arguments specdec_accept rejects). */
+SPECDEC_API size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab);
 
 /* KV commit / rollback after specdec_accept (device-side, graph friendly):
  *  TARGET: len += A+1; pending = [next]                       (n_pending = 1)

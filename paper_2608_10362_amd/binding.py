@@ -90,7 +90,9 @@ _SIGS = {
     "specdec_accept": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                       ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
-                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_void_p]),
+    "specdec_accept_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "specdec_kv_commit": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_sample": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
@@ -353,8 +355,23 @@ def specdec_verify(target: Model, kv: KVCache, gamma: int, d, ld_d: int, logits_
                                 _stream(stream)), "specdec_verify")
 
 
+def specdec_accept_workspace_bytes(batch: int, gamma: int, vocab: int) -> int:
+    return int(lib().specdec_accept_workspace_bytes(batch, gamma, vocab))
+
+
+def accept_workspace(batch: int, gamma: int, vocab: int, device="cuda"):
+    """A device buffer large enough for specdec_accept's workspace."""
+    import torch
+    n = specdec_accept_workspace_bytes(batch, gamma, vocab)
+    if n == 0:
+        raise ValueError("specdec_accept does not support these sizes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
 def specdec_accept(batch: int, gamma: int, vocab: int, input_kind: int, temperature: float, p, q, d, ld_d: int,
-                   rand, seed: int, step: int, n_accepted, next_token, status=None, stream=None):
+                   rand, seed: int, step: int, n_accepted, next_token, status=None, workspace=None, stream=None):
+    """Accept / resample.  `workspace` (uint8 device tensor) is allocated per
+    call when not given; pass one from accept_workspace() in loops."""
     import torch
     _dev(p, "p", torch.float32, batch * (gamma + 1) * vocab)
     _dev(q, "q", torch.float32, batch * gamma * vocab, optional=temperature == 0 or gamma == 0)
@@ -366,9 +383,12 @@ def specdec_accept(batch: int, gamma: int, vocab: int, input_kind: int, temperat
     _dev(n_accepted, "n_accepted", torch.int32, batch)
     _dev(next_token, "next_token", torch.int32, batch)
     _dev(status, "status", torch.int32, 1, optional=True)
+    if workspace is None:
+        workspace = accept_workspace(batch, gamma, vocab, p.device)
+    _dev(workspace, "workspace", torch.uint8, 1)
     _check(lib().specdec_accept(batch, gamma, vocab, input_kind, temperature, p.data_ptr(), _ptr(q), _ptr(d), ld_d,
                                 _ptr(rand), seed, step, n_accepted.data_ptr(), next_token.data_ptr(), _ptr(status),
-                                _stream(stream)), "specdec_accept")
+                                workspace.data_ptr(), workspace.numel(), _stream(stream)), "specdec_accept")
 
 
 def specdec_kv_commit(kv: KVCache, gamma: int, role: int, n_accepted, d, ld_d: int, next_token, stream=None):
@@ -456,6 +476,7 @@ class SpecDecoder:
         self.n_acc = torch.zeros(B, dtype=torch.int32, device=dev)
         self.next = torch.zeros(B, dtype=torch.int32, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.accept_ws = accept_workspace(B, gamma, V, dev)
 
     def draft_phase(self, step: int, stream=None):
         for s in range(self.gamma):
@@ -465,7 +486,7 @@ class SpecDecoder:
     def verify_phase(self, step: int, stream=None):
         specdec_verify(self.target, self.kv_t, self.gamma, self.d, self.gamma, self.logits, stream)
         specdec_accept(self.B, self.gamma, self.V, INPUT_LOGITS, self.temperature, self.logits, self.q, self.d,
-                       self.gamma, None, self.seed, step, self.n_acc, self.next, self.status, stream)
+                       self.gamma, None, self.seed, step, self.n_acc, self.next, self.status, self.accept_ws, stream)
 
     def commit_phase(self, stream=None):
         specdec_kv_commit(self.kv_t, self.gamma, ROLE_TARGET, self.n_acc, self.d, self.gamma, self.next, stream)

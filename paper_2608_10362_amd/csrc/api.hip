@@ -33,6 +33,7 @@ struct specdec_model {
   float* o;
   float* u;
   float* logits;
+  void* samp;  // scratch of the draft's softmax / draw kernels
   int chunk, n_split_max;
   // layer-0 launches of the last forward pass, for specdec_time_kernel
   mutable bool rec_valid[SPECDEC_KERNEL_KINDS] = {};
@@ -90,7 +91,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -115,6 +116,7 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.o = take(R * H * hd * 4);
   w.u = take(R * d->ffn_dim * 4);
   w.logits = take(R * d->vocab * 4);
+  w.samp = take(sampling_scratch_bytes(max_rows, 1, d->vocab));
   w.total = off;
   return w;
 }
@@ -465,6 +467,7 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   m->o = (float*)(base + L.o);
   m->u = (float*)(base + L.u);
   m->logits = (float*)(base + L.logits);
+  m->samp = base + L.samp;
   m->chunk = L.chunk;
   m->n_split_max = L.n_split;
   *out = m;
@@ -628,6 +631,7 @@ specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, in
   f.ld_d = ld_d;
   f.logits_out = logits_out;
   f.status = kv_status(kv);
+  f.scratch = draft->samp;
   Timed t(SPECDEC_KERNEL_DRAFT_FINISH, s);
   return hip_status(launch_draft_finish(f, s));
 }
@@ -649,16 +653,22 @@ specdec_status specdec_verify(const specdec_model* target, specdec_kv* kv, int32
   return forward(target, kv, ra, (int)(kv->len_upper + gamma + 1), logits_out, (hipStream_t)stream);
 }
 
+size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab) {
+  if (batch <= 0 || gamma < 0 || gamma > 31 || vocab <= 0) return 0;
+  return sampling_scratch_bytes(batch, gamma + 1, vocab);
+}
+
 specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
                               const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
                               uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
-                              int32_t* status, void* stream) {
+                              int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
   if (batch <= 0 || gamma < 0 || vocab <= 0 || !p || !n_accepted || !next_token || !(temperature >= 0.f))
     return SPECDEC_ERR_INVALID_ARG;
+  if (gamma > 31) return SPECDEC_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < sampling_scratch_bytes(batch, gamma + 1, vocab)) return SPECDEC_ERR_INVALID_ARG;
   if (input_kind != SPECDEC_INPUT_PROBS && input_kind != SPECDEC_INPUT_LOGITS) return SPECDEC_ERR_INVALID_ARG;
   if (gamma > 0 && (!d || ld_d < gamma)) return SPECDEC_ERR_INVALID_ARG;
   if (temperature > 0.f && gamma > 0 && !q) return SPECDEC_ERR_INVALID_ARG;
-  if (gamma > 31) return SPECDEC_ERR_UNSUPPORTED;
   AcceptArgs a{};
   a.B = batch;
   a.gamma = gamma;
@@ -675,6 +685,7 @@ specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32
   a.n_accepted = n_accepted;
   a.next_token = next_token;
   a.status = status;
+  a.scratch = workspace;
   Timed t(SPECDEC_KERNEL_ACCEPT, (hipStream_t)stream);
   return hip_status(launch_accept(a, (hipStream_t)stream));
 }

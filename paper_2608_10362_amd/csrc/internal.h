@@ -105,8 +105,13 @@ struct DraftFinishArgs {
   int ld_d;
   float* logits_out;     // [B, V] or null
   int32_t* status;
+  void* scratch;         // sampling_scratch_bytes(B, 1, V) bytes
 };
 hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s);
+
+// Scratch of the multi-block softmax / accept / draw kernels for B sequences
+// with `rows` distribution rows each over a vocabulary of V.
+size_t sampling_scratch_bytes(int B, int rows, int V);
 
 struct AcceptArgs {
   int B, gamma, V, input_kind;
@@ -120,6 +125,7 @@ struct AcceptArgs {
   int32_t* n_accepted;
   int32_t* next_token;
   int32_t* status;
+  void* scratch;         // sampling_scratch_bytes(B, gamma + 1, V) bytes
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 

@@ -205,137 +205,372 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
   if (threadIdx.x == 0) a.ss[r] = ss;
 }
 
-// ---------------------------------------------------------------- draft finish
-__global__ __launch_bounds__(kSampThreads) void draft_finish_kernel(DraftFinishArgs a) {
-  __shared__ float redf[16];
-  __shared__ float red2[32];
-  __shared__ int redi[16];
-  __shared__ SampShared sh;
-  const int b = blockIdx.x, V = a.V, tid = threadIdx.x, nt = blockDim.x;
-  const float* lg = a.logits + ((size_t)b * a.rps + a.rps - 1) * V;
-  bool bad = false;
-  for (int j = tid; j < V; j += nt) {
-    const float v = lg[j];
-    bad |= !isfinite(v);
-    if (a.logits_out) a.logits_out[(size_t)b * V + j] = v;
-  }
-  if (__syncthreads_or(bad)) {
-    if (tid == 0) {
-      set_status(a.status, kStatusNonFinite);
-      a.d_out[(size_t)b * a.ld_d + a.slot] = 0;
-    }
-    return;
-  }
-  int tok;
-  if (a.temperature == 0.f) {
-    float bv = -INFINITY;
-    int bi = 0x7fffffff;
-    for (int j = tid; j < V; j += nt)
-      if (lg[j] > bv) { bv = lg[j]; bi = j; }
-    block_argmax(bv, bi, redf, redi);
-    tok = bi;
-  } else {
-    const float T = a.temperature;
-    const MaxSum st = block_max_sum(lg, V, T, red2);
-    const float mx = st.m, s = st.s;
-    auto qf = [&](int j) { return expf(lg[j] / T - mx) / s; };
-    if (a.q_out) {
-      float* qo = a.q_out + ((size_t)b * a.gamma + a.slot) * V;
-      for (int j = tid; j < V; j += nt) qo[j] = qf(j);
-    }
-    const uint32_t x = a.rand ? a.rand[b] : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_DRAFT, a.slot);
-    tok = block_draw(qf, V, x, sh);
-  }
-  if (tid == 0) a.d_out[(size_t)b * a.ld_d + a.slot] = tok;
+// ---------------------------------------------------------------- multi-block softmax / accept / draw
+// A vocabulary row is cut into NC chunks; one block per (chunk, row) so that
+// a single decision uses many CUs:
+//   stats     per (chunk, row): online (max, sum exp) of z = x / T, argmax, finiteness
+//   decide    per sequence: merge the chunk statistics (fixed order), accept scan
+//   partials  per (chunk, sequence): integer weight sums of the row to draw from
+//             (the draft's q is also written here)
+//   final     per sequence: find the chunk holding t, scan it, emit the token
+constexpr int kChunkThreads = 256;
+
+__host__ __device__ __forceinline__ int n_chunks(int V) {
+  int nc = (V + 1023) / 1024;
+  return nc < 1 ? 1 : (nc > 64 ? 64 : nc);
+}
+__host__ __device__ __forceinline__ int chunk_size(int V) { return (V + n_chunks(V) - 1) / n_chunks(V); }
+
+struct StatPart {
+  float m, s, amax_v;
+  int amax_i, bad, pad0, pad1, pad2;
+};
+struct DrawPart {
+  unsigned long long res, prob;
+};
+struct SeqState {
+  int A;            // accepted count (-1 error, -2 no draw needed)
+  int pad;
+  float2 ms[kMaxGamma + 1];  // merged (max, sum) per row
+};
+
+struct Scratch {
+  StatPart* stats;  // [rows_total][NC]
+  SeqState* seq;    // [B]
+  DrawPart* draw;   // [B][NC]
+};
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+__host__ __device__ inline Scratch carve(void* base, int B, int rows, int V) {
+  const int NC = n_chunks(V);
+  char* p = (char*)base;
+  Scratch s;
+  s.stats = (StatPart*)p;
+  p += align256(sizeof(StatPart) * (size_t)B * rows * NC);
+  s.seq = (SeqState*)p;
+  p += align256(sizeof(SeqState) * (size_t)B);
+  s.draw = (DrawPart*)p;
+  return s;
 }
 
-// ---------------------------------------------------------------- accept / resample
-__global__ __launch_bounds__(kSampThreads) void accept_kernel(AcceptArgs a) {
-  __shared__ float redf[16];
-  __shared__ float red2[32];
-  __shared__ int redi[16];
-  __shared__ float rmax[kMaxGamma + 1], rsum[kMaxGamma + 1];
-  __shared__ SampShared sh;
-  const int b = blockIdx.x, g = a.gamma, V = a.V, tid = threadIdx.x, nt = blockDim.x;
+// p_i(j) of row i: softmax(l/T) from merged statistics, or the probability itself.
+__device__ __forceinline__ float prob_of(const float* row, int j, bool logits, float T, float2 ms) {
+  const float v = row[j];
+  return logits ? expf(v / T - ms.x) / ms.y : v;
+}
+
+// stats: grid (NC, B * rows_per_seq), block 256.  Row i of sequence b is
+// x + (b * row_stride + row_off + i) * V.
+// Every value of the row, and of the row `chk` pairs with it (the draft's q
+// row i of an accept, rows i < chk_rows), must be finite.
+__global__ __launch_bounds__(kChunkThreads) void stats_kernel(const float* x, int V, int rows_per_seq, int row_stride,
+                                                              int row_off, float T, const float* chk, int chk_rows,
+                                                              StatPart* out) {
+  __shared__ float sm_m[4], sm_s[4], sm_v[4];
+  __shared__ int sm_i[4], sm_b[4];
+  const int c = blockIdx.x, r = blockIdx.y, NC = gridDim.x;
+  const int b = r / rows_per_seq, i = r % rows_per_seq;
+  const float* row = x + ((size_t)b * row_stride + row_off + i) * V;
+  const int cs = chunk_size(V), j0 = c * cs, j1 = min(V, j0 + cs);
+  MaxSum st{-INFINITY, 0.f};
+  float bv = -INFINITY;
+  int bi = 0x7fffffff, bad = 0;
+  for (int j = j0 + threadIdx.x; j < j1; j += kChunkThreads) {
+    const float v = row[j];
+    bad |= !isfinite(v);
+    if (v > bv) { bv = v; bi = j; }
+    if (T > 0.f) ms_add(st, v / T);
+  }
+  if (chk && i < chk_rows) {
+    const float* crow = chk + ((size_t)b * chk_rows + i) * V;
+    for (int j = j0 + threadIdx.x; j < j1; j += kChunkThreads) bad |= !isfinite(crow[j]);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    st = ms_merge(st, MaxSum{__shfl_xor(st.m, o, kWave), __shfl_xor(st.s, o, kWave)});
+    const float ov = __shfl_xor(bv, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    bad |= __shfl_xor(bad, o, kWave);
+  }
+  if (lane == 0) { sm_m[w] = st.m; sm_s[w] = st.s; sm_v[w] = bv; sm_i[w] = bi; sm_b[w] = bad; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    MaxSum t{sm_m[0], sm_s[0]};
+    float tv = sm_v[0];
+    int ti = sm_i[0], tb = sm_b[0];
+    for (int k = 1; k < kChunkThreads / kWave; ++k) {
+      t = ms_merge(t, MaxSum{sm_m[k], sm_s[k]});
+      if (sm_v[k] > tv || (sm_v[k] == tv && sm_i[k] < ti)) { tv = sm_v[k]; ti = sm_i[k]; }
+      tb |= sm_b[k];
+    }
+    out[(size_t)r * NC + c] = StatPart{t.m, t.s, tv, ti, tb, 0, 0, 0};
+  }
+}
+
+// Merge the chunk statistics of one row (fixed order).
+__device__ void merge_stats(const StatPart* parts, int NC, float& m, float& s, float& av, int& ai, int& bad) {
+  MaxSum t{parts[0].m, parts[0].s};
+  av = parts[0].amax_v;
+  ai = parts[0].amax_i;
+  bad = parts[0].bad;
+  for (int k = 1; k < NC; ++k) {
+    t = ms_merge(t, MaxSum{parts[k].m, parts[k].s});
+    if (parts[k].amax_v > av || (parts[k].amax_v == av && parts[k].amax_i < ai)) { av = parts[k].amax_v; ai = parts[k].amax_i; }
+    bad |= parts[k].bad;
+  }
+  m = t.m;
+  s = t.s;
+}
+
+// decide: grid B, block 64.
+__global__ __launch_bounds__(64) void accept_decide_kernel(AcceptArgs a) {
+  const int b = blockIdx.x, g = a.gamma, V = a.V, NC = n_chunks(V), lane = threadIdx.x;
+  Scratch sc = carve(a.scratch, a.B, g + 1, V);
+  const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
+  const float T = a.temperature;
+  __shared__ int amax[kMaxGamma + 1];
+  __shared__ float2 ms[kMaxGamma + 1];
+  int bad = 0;
+  if (lane <= g) {
+    float m, s, av;
+    int ai, bd;
+    merge_stats(sc.stats + ((size_t)b * (g + 1) + lane) * NC, NC, m, s, av, ai, bd);
+    if (logits && T > 0.f) bad |= !isfinite(m) || !isfinite(s);
+    bad |= bd;
+    amax[lane] = ai;
+    ms[lane] = make_float2(m, s);
+    sc.seq[b].ms[lane] = make_float2(m, s);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o, kWave);
+  __syncthreads();
+  if (lane != 0) return;
   const float* P = a.p + (size_t)b * (g + 1) * V;
   const float* Q = a.q ? a.q + (size_t)b * g * V : nullptr;
   const int32_t* d = a.d + (size_t)b * a.ld_d;
-  auto word = [&](int i) -> uint32_t {
-    if (a.rand) return a.rand[(size_t)b * (g + 1) + i];
-    return i < g ? draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, i)
-                 : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_RESAMPLE, 0);
-  };
-  bool bad = false;
-  int A = g, next = -1;
-  if (a.temperature == 0.f) {
-    for (int i = 0; i <= g; ++i) {
-      float bv = -INFINITY;
-      int bi = 0x7fffffff;
-      for (int j = tid; j < V; j += nt) {
-        const float v = P[(size_t)i * V + j];
-        bad |= !isfinite(v);
-        if (v > bv) { bv = v; bi = j; }
-      }
-      block_argmax(bv, bi, redf, redi);
-      if (i < g && bi != d[i]) { A = i; next = bi; break; }
-      if (i == g) next = bi;
-    }
-    bad = __syncthreads_or(bad);
-  } else {
-    const float T = a.temperature;
-    const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
-    for (int i = 0; i <= g; ++i) {
-      const float* row = P + (size_t)i * V;
-      if (logits) {
-        const MaxSum st = block_max_sum(row, V, T, red2);
-        // a NaN/Inf logit makes the row's max or sum non-finite
-        bad |= !isfinite(st.m) || !isfinite(st.s);
-        if (tid == 0) { rmax[i] = st.m; rsum[i] = st.s; }
-      } else {
-        for (int j = tid; j < V; j += nt) bad |= !isfinite(row[j]);
-      }
-    }
-    bad = __syncthreads_or(bad);
-    auto pf = [&](int i, int j) -> float {
-      const float v = P[(size_t)i * V + j];
-      return logits ? expf(v / T - rmax[i]) / rsum[i] : v;
-    };
-    if (!bad) {
+  int A = g;
+  if (!bad) {
+    if (T == 0.f) {
+      for (int i = 0; i < g; ++i)
+        if (amax[i] != d[i]) { A = i; break; }
+    } else {
       for (int i = 0; i < g; ++i) {
         const int di = d[i];
-        if (di < 0 || di >= V) { bad = true; break; }
-        const float pd = pf(i, di), qd = Q[(size_t)i * V + di];
-        if (!isfinite(qd)) { bad = true; break; }
-        const float u = word_to_uniform(word(i));
-        if (!(__fmul_rn(u, qd) < pd)) { A = i; break; }
+        if (di < 0 || di >= V) { bad = 1; break; }
+        const float pd = prob_of(P + (size_t)i * V, di, logits, T, ms[i]);
+        const float qd = Q[(size_t)i * V + di];
+        if (!isfinite(qd)) { bad = 1; break; }
+        const uint32_t w = a.rand ? a.rand[(size_t)b * (g + 1) + i]
+                                  : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, i);
+        if (!(__fmul_rn(word_to_uniform(w), qd) < pd)) { A = i; break; }
       }
     }
-    if (!bad && A < g) {
-      bool badq = false;
-      for (int j = tid; j < V; j += nt) badq |= !isfinite(Q[(size_t)A * V + j]);
-      bad = __syncthreads_or(badq);
-    }
-    if (!bad) {
-      const uint32_t x = word(g);
-      if (A < g) {
-        const float* qr = Q + (size_t)A * V;
-        next = block_draw([&](int j) { return fmaxf(0.f, __fsub_rn(pf(A, j), qr[j])); }, V, x, sh);
-        if (next < 0) next = block_draw([&](int j) { return pf(A, j); }, V, x, sh);
+  }
+  if (bad) {
+    set_status(a.status, kStatusNonFinite);
+    a.n_accepted[b] = -1;
+    a.next_token[b] = -1;
+    sc.seq[b].A = -1;
+  } else if (T == 0.f) {
+    a.n_accepted[b] = A;
+    a.next_token[b] = amax[A];
+    sc.seq[b].A = -2;
+  } else {
+    a.n_accepted[b] = A;
+    sc.seq[b].A = A;
+  }
+}
+
+// Weight sources of a draw.
+enum { W_ACCEPT = 0, W_DRAFT = 1 };
+
+struct DrawArgs {
+  int mode, B, V, gamma;
+  float T;
+  // accept
+  const float* p;
+  const float* q;
+  int logits;
+  // draft: logits of the proposing rows, q output
+  const float* lg;
+  int rps, slot;
+  float* q_out;
+  void* scratch;
+  int rows;  // rows per sequence in the scratch statistics
+};
+
+// R_j weights of sequence b at column j, for the residual (res) and the plain row (prob).
+__device__ __forceinline__ void weights_at(const DrawArgs& a, const SeqState& st, int b, int j, float& res, float& prob) {
+  if (a.mode == W_ACCEPT) {
+    const int A = st.A, g = a.gamma;
+    const float* P = a.p + ((size_t)b * (g + 1) + A) * a.V;
+    const float pj = prob_of(P, j, a.logits, a.T, st.ms[A]);
+    prob = pj;
+    res = A < g ? fmaxf(0.f, __fsub_rn(pj, a.q[((size_t)b * g + A) * a.V + j])) : 0.f;
+  } else {
+    const float* lg = a.lg + ((size_t)b * a.rps + a.rps - 1) * a.V;
+    prob = expf(lg[j] / a.T - st.ms[0].x) / st.ms[0].y;
+    res = 0.f;
+  }
+}
+
+// partials: grid (NC, B), block 256.
+__global__ __launch_bounds__(kChunkThreads) void draw_partials_kernel(DrawArgs a) {
+  __shared__ unsigned long long sr[4], sp[4];
+  const int c = blockIdx.x, b = blockIdx.y, V = a.V;
+  Scratch sc = carve(a.scratch, a.B, a.rows, V);
+  const SeqState& st = sc.seq[b];
+  if (st.A < 0) return;
+  const int cs = chunk_size(V), j0 = c * cs, j1 = min(V, j0 + cs);
+  unsigned long long r_sum = 0, p_sum = 0;
+  float* qo = a.mode == W_DRAFT && a.q_out ? a.q_out + ((size_t)b * a.gamma + a.slot) * V : nullptr;
+  for (int j = j0 + threadIdx.x; j < j1; j += kChunkThreads) {
+    float res, prob;
+    weights_at(a, st, b, j, res, prob);
+    if (qo) qo[j] = prob;
+    r_sum += fp_weight(res);
+    p_sum += fp_weight(prob);
+  }
+  r_sum = wave_sum_u64(r_sum);
+  p_sum = wave_sum_u64(p_sum);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) { sr[w] = r_sum; sp[w] = p_sum; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    DrawPart d{0ull, 0ull};
+    for (int k = 0; k < kChunkThreads / kWave; ++k) { d.res += sr[k]; d.prob += sp[k]; }
+    sc.draw[(size_t)b * gridDim.x + c] = d;
+  }
+}
+
+struct FinalArgs {
+  DrawArgs d;
+  const uint32_t* rand;   // accept: [B, gamma+1] (word gamma); draft: [B]
+  uint64_t seed, step;
+  int32_t* out;           // accept: next_token[B]; draft: d_out + slot
+  int ld_out;
+};
+
+// final: grid B, block 256.
+__global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) {
+  __shared__ unsigned long long wtot[4];
+  __shared__ int chunk_sel, use_res, done;
+  __shared__ unsigned long long t_in_chunk;
+  const DrawArgs& a = f.d;
+  const int b = blockIdx.x, V = a.V, NC = n_chunks(V), cs = chunk_size(V);
+  Scratch sc = carve(a.scratch, a.B, a.rows, V);
+  const SeqState& st = sc.seq[b];
+  if (st.A < 0) return;
+  const DrawPart* parts = sc.draw + (size_t)b * NC;
+  if (threadIdx.x == 0) {
+    unsigned long long tr = 0, tp = 0;
+    for (int k = 0; k < NC; ++k) { tr += parts[k].res; tp += parts[k].prob; }
+    done = 0;
+    {
+      const bool res = a.mode == W_ACCEPT && st.A < a.gamma && tr != 0;
+      const unsigned long long S = res ? tr : tp;
+      uint32_t x;
+      if (a.mode == W_ACCEPT)
+        x = f.rand ? f.rand[(size_t)b * (a.gamma + 1) + a.gamma] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_RESAMPLE, 0);
+      else
+        x = f.rand ? f.rand[b] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_DRAFT, a.slot);
+      if (S == 0) {
+        f.out[(size_t)b * f.ld_out] = -1;
+        done = 1;
       } else {
-        next = block_draw([&](int j) { return pf(g, j); }, V, x, sh);
+        const unsigned long long t = scale_word(x, S);
+        unsigned long long before = 0;
+        int c = 0;
+        for (; c < NC; ++c) {
+          const unsigned long long w = res ? parts[c].res : parts[c].prob;
+          if (t < before + w) break;
+          before += w;
+        }
+        chunk_sel = c;
+        use_res = res;
+        t_in_chunk = t - before;
       }
     }
   }
-  if (tid == 0) {
-    if (bad) {
-      set_status(a.status, kStatusNonFinite);
-      a.n_accepted[b] = -1;
-      a.next_token[b] = -1;
-    } else {
-      a.n_accepted[b] = A;
-      a.next_token[b] = next;
+  __syncthreads();
+  if (done) return;
+  // scan the selected chunk: thread k owns 4 consecutive columns
+  const int j0 = chunk_sel * cs, j1 = min(V, j0 + cs);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  unsigned long long mine[4], tot = 0;
+  for (int base = j0; base < j1; base += 4 * kChunkThreads) {
+    const int jj = base + 4 * threadIdx.x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float res = 0.f, prob = 0.f;
+      if (jj + e < j1) weights_at(a, st, b, jj + e, res, prob);
+      mine[e] = jj + e < j1 ? fp_weight(use_res ? res : prob) : 0ull;
     }
+    const unsigned long long sum4 = mine[0] + mine[1] + mine[2] + mine[3];
+    unsigned long long incl = sum4;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const unsigned long long n = shfl_up_u64(incl, o);
+      if (lane >= o) incl += n;
+    }
+    __syncthreads();
+    if (lane == kWave - 1) wtot[w] = incl;
+    __syncthreads();
+    unsigned long long wbefore = 0, round_tot = 0;
+    for (int k = 0; k < kChunkThreads / kWave; ++k) {
+      if (k < w) wbefore += wtot[k];
+      round_tot += wtot[k];
+    }
+    const unsigned long long t = t_in_chunk - tot;  // position inside this round
+    unsigned long long cum = wbefore + incl - sum4;
+    if (t < round_tot && cum <= t && t < cum + sum4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cum += mine[e];
+        if (cum > t) { f.out[(size_t)b * f.ld_out] = jj + e; break; }
+      }
+    }
+    if (t < round_tot) break;  // uniform: every thread sees the same totals
+    tot += round_tot;
   }
+}
+
+// draft greedy: grid B, block 64: merge the chunk argmax of the proposing row.
+__global__ __launch_bounds__(64) void draft_greedy_kernel(DraftFinishArgs a) {
+  const int b = blockIdx.x, NC = n_chunks(a.V);
+  Scratch sc = carve(a.scratch, a.B, 1, a.V);
+  if (threadIdx.x != 0) return;
+  float m, s, av;
+  int ai, bad;
+  merge_stats(sc.stats + (size_t)b * NC, NC, m, s, av, ai, bad);
+  if (bad) set_status(a.status, kStatusNonFinite);
+  a.d_out[(size_t)b * a.ld_d + a.slot] = bad ? 0 : ai;
+}
+
+// draft sampling: merge statistics into the sequence state (grid B, block 64).
+__global__ __launch_bounds__(64) void draft_merge_kernel(DraftFinishArgs a) {
+  const int b = blockIdx.x, NC = n_chunks(a.V);
+  Scratch sc = carve(a.scratch, a.B, 1, a.V);
+  if (threadIdx.x != 0) return;
+  float m, s, av;
+  int ai, bad;
+  merge_stats(sc.stats + (size_t)b * NC, NC, m, s, av, ai, bad);
+  bad |= !isfinite(m) || !isfinite(s);
+  if (bad) {
+    set_status(a.status, kStatusNonFinite);
+    sc.seq[b].A = -1;
+    a.d_out[(size_t)b * a.ld_d + a.slot] = 0;
+  } else {
+    sc.seq[b].A = 0;
+  }
+  sc.seq[b].ms[0] = make_float2(m, s);
+}
+
+__global__ void copy_logits_kernel(const float* lg, int rps, int V, float* out) {
+  const int b = blockIdx.y;
+  const float* src = lg + ((size_t)b * rps + rps - 1) * V;
+  for (int j = blockIdx.x * blockDim.x + threadIdx.x; j < V; j += gridDim.x * blockDim.x) out[(size_t)b * V + j] = src[j];
 }
 
 // ---------------------------------------------------------------- sampler / philox
@@ -391,14 +626,80 @@ hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+size_t sampling_scratch_bytes(int B, int rows, int V) {
+  const int NC = n_chunks(V);
+  return align256(sizeof(StatPart) * (size_t)B * rows * NC) + align256(sizeof(SeqState) * (size_t)B) +
+         align256(sizeof(DrawPart) * (size_t)B * NC);
+}
+
 hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(draft_finish_kernel, dim3(a.B), dim3(kSampThreads), 0, s, a);
+  const int NC = n_chunks(a.V);
+  if (a.logits_out) {
+    hipLaunchKernelGGL(copy_logits_kernel, dim3((a.V + 255) / 256, a.B), dim3(256), 0, s, a.logits, a.rps, a.V,
+                       a.logits_out);
+  }
+  Scratch sc = carve(a.scratch, a.B, 1, a.V);
+  hipLaunchKernelGGL(stats_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, a.logits, a.V, 1, a.rps, a.rps - 1,
+                     a.temperature, nullptr, 0, sc.stats);
+  if (a.temperature == 0.f) {
+    hipLaunchKernelGGL(draft_greedy_kernel, dim3(a.B), dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(draft_merge_kernel, dim3(a.B), dim3(64), 0, s, a);
+  DrawArgs d{};
+  d.mode = W_DRAFT;
+  d.B = a.B;
+  d.V = a.V;
+  d.gamma = a.gamma;
+  d.T = a.temperature;
+  d.lg = a.logits;
+  d.rps = a.rps;
+  d.slot = a.slot;
+  d.q_out = a.q_out;
+  d.scratch = a.scratch;
+  d.rows = 1;
+  hipLaunchKernelGGL(draw_partials_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
+  FinalArgs f{};
+  f.d = d;
+  f.rand = a.rand;
+  f.seed = a.seed;
+  f.step = a.step;
+  f.out = a.d_out + a.slot;
+  f.ld_out = a.ld_d;
+  hipLaunchKernelGGL(draw_final_kernel, dim3(a.B), dim3(kChunkThreads), 0, s, f);
   return hipGetLastError();
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   if (a.gamma > kMaxGamma) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(accept_kernel, dim3(a.B), dim3(kSampThreads), 0, s, a);
+  const int NC = n_chunks(a.V);
+  Scratch sc = carve(a.scratch, a.B, a.gamma + 1, a.V);
+  const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
+  hipLaunchKernelGGL(stats_kernel, dim3(NC, a.B * (a.gamma + 1)), dim3(kChunkThreads), 0, s, a.p, a.V, a.gamma + 1,
+                     a.gamma + 1, 0, logits ? a.temperature : 0.f, a.temperature > 0.f ? a.q : nullptr, a.gamma,
+                     sc.stats);
+  hipLaunchKernelGGL(accept_decide_kernel, dim3(a.B), dim3(64), 0, s, a);
+  if (a.temperature == 0.f) return hipGetLastError();
+  DrawArgs d{};
+  d.mode = W_ACCEPT;
+  d.B = a.B;
+  d.V = a.V;
+  d.gamma = a.gamma;
+  d.T = a.temperature;
+  d.p = a.p;
+  d.q = a.q;
+  d.logits = logits;
+  d.scratch = a.scratch;
+  d.rows = a.gamma + 1;
+  hipLaunchKernelGGL(draw_partials_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
+  FinalArgs f{};
+  f.d = d;
+  f.rand = a.rand;
+  f.seed = a.seed;
+  f.step = a.step;
+  f.out = a.next_token;
+  f.ld_out = 1;
+  hipLaunchKernelGGL(draw_final_kernel, dim3(a.B), dim3(kChunkThreads), 0, s, f);
   return hipGetLastError();
 }
 

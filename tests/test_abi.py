@@ -102,11 +102,20 @@ def test_call_argument_errors_before_any_launch(lib):
     # null handles / buffers are rejected synchronously
     assert lib.specdec_verify(None, ctypes.byref(kv), 4, None, 4, None, None) == -1
     assert lib.specdec_draft_step(None, ctypes.byref(kv), 4, 0, 1.0, 0, 0, None, None, None, 4, None, None) == -1
-    assert lib.specdec_accept(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, None) == -1
-    assert lib.specdec_accept(1, 4, 100, 7, 1.0, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
-                              4, None, 0, 0, ctypes.c_void_p(256), ctypes.c_void_p(256), None, None) == -1
-    assert lib.specdec_accept(1, 40, 100, 0, 1.0, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256),
-                              40, None, 0, 0, ctypes.c_void_p(256), ctypes.c_void_p(256), None, None) == -6
+    fake = ctypes.c_void_p(256)
+    ws = lib.specdec_accept_workspace_bytes(1, 4, 100)
+    assert ws > 0 and lib.specdec_accept_workspace_bytes(1, 40, 100) == 0
+    assert lib.specdec_accept(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, fake, ws,
+                              None) == -1
+    assert lib.specdec_accept(1, 4, 100, 7, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, fake, ws,
+                              None) == -1
+    assert lib.specdec_accept(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, fake, fake, None, fake, ws,
+                              None) == -6
+    # the workspace is required and must be large enough
+    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, None, ws,
+                              None) == -1
+    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, fake, ws - 1,
+                              None) == -1
     assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1
     assert lib.specdec_sample(1, 10, None, 10, None, 0, 0, 0, 0, None, None) == -1
     assert lib.specdec_draw_u32(1, 0, 0, 0x10000, 0, ctypes.c_void_p(256), None) == -1

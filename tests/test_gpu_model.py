@@ -4,6 +4,8 @@ Logits must agree within max-abs 1e-4 (float32 model) / 2e-2 (bf16 model),
 under teacher forcing: both sides get the same weights, resident context and
 drafted tokens.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -60,9 +62,24 @@ def test_tiny_prefill_and_verify(tiny):
     assert worst < TOL_F32
 
 
-def test_tiny_draft_steps(tiny):
+@pytest.fixture(scope="module")
+def tiny_wide():
+    """The tiny float32 model with a 50000-token vocabulary: the softmax and
+    draw run over 49 chunks of 1021 (last one ragged)."""
+    torch_cuda()
+    shape = dataclasses.replace(synth.TINY, vocab=50000)
+    W = synth.make_weights(shape)
+    dw = binding.DeviceWeights(shape, W)
+    return shape, W, binding.Model(dw, 1, max_rows=16, max_ctx=256)
+
+
+@pytest.mark.parametrize("wide", [False, True])
+def test_tiny_draft_steps(tiny, tiny_wide, wide):
     torch = torch_cuda()
-    shape, W, _, draft = tiny
+    if wide:
+        shape, W, draft = tiny_wide
+    else:
+        shape, W, _, draft = tiny
     g, T, seed, step = 4, 1.0, 2, 9
     prompt = synth.make_prompt(40, shape.vocab)
     kv = binding.KVCache(draft, 1, 256)

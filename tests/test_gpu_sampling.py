@@ -55,7 +55,7 @@ def _accept_inputs(B, g, V, seed, agree=0.7):
     return p, q, d, words
 
 
-@pytest.mark.parametrize("g,V", [(1, 512), (4, 32000), (8, 2048), (6, 32000)])
+@pytest.mark.parametrize("g,V", [(1, 512), (4, 32000), (8, 2048), (6, 32000), (4, 50000), (2, 128256), (3, 65)])
 def test_accept_sampling_bit_exact(g, V):
     torch = torch_cuda()
     B = 16
@@ -135,6 +135,25 @@ def test_accept_nonfinite_sets_status():
     assert nacc[1].item() == -1 and nacc[0].item() >= 0
     with pytest.raises(sampling.NonFiniteError):
         sampling.accept_sampling(p[1], q[1], d[1], [int(w) for w in words[1, :g]], int(words[1, g]))
+    # an Inf in a draft row the decision never reaches is still an error (every
+    # input row is checked, as the oracle does)
+    p, q, d, words = _accept_inputs(B, g, V, seed=4)
+    q[0, g - 1, 7] = np.inf
+    status.zero_()
+    binding.specdec_accept(B, g, V, binding.INPUT_PROBS, 1.0, f32(p), f32(q), i32(d), g, u32_tensor(words), 0, 0,
+                           nacc, nxt, status)
+    assert status.item() == -4 and nacc[0].item() == -1 and nxt[0].item() == -1 and nacc[1].item() >= 0
+    with pytest.raises(sampling.NonFiniteError):
+        sampling.accept_sampling(p[0], q[0], d[0], [int(w) for w in words[0, :g]], int(words[0, g]))
+    # greedy: a NaN in the bonus row
+    scores = np.random.default_rng(5).standard_normal((B, g + 1, V)).astype(np.float32)
+    scores[1, g, 3] = np.nan
+    status.zero_()
+    binding.specdec_accept(B, g, V, binding.INPUT_LOGITS, 0.0, f32(scores), None, i32(d), g, None, 0, 0,
+                           nacc, nxt, status)
+    assert status.item() == -4 and nacc[1].item() == -1 and nacc[0].item() >= 0
+    with pytest.raises(sampling.NonFiniteError):
+        sampling.accept_greedy(scores[1], d[1])
 
 
 def test_accept_logits_mode_matches_oracle():
