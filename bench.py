@@ -325,7 +325,8 @@ def main():
     draft_part(0); verify_part(0)
     torch.cuda.synchronize()
     kb_verify = kernel_bytes(shape, ctx + g + 1)
-    per_layer = {"embed": 1, "qkv": shape.n_layers, "rope_append": shape.n_layers, "attention": shape.n_layers,
+    # (bf16: RoPE and the KV append run in the QKV GEMM's epilogue, no rope_append launch)
+    per_layer = {"embed": 1, "qkv": shape.n_layers, "attention": shape.n_layers,
                  "o_proj": shape.n_layers, "gate_up": shape.n_layers, "down": shape.n_layers, "lm_head": 1}
     kernels = {}
     for k, n in per_layer.items():

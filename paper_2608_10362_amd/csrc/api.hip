@@ -190,7 +190,10 @@ hipError_t gemm_rows(int dtype, GemmArgs g, int M, hipStream_t s) {
     GemmArgs c = g;
     c.M = std::min(kMaxGemmRows, M - m0);
     c.x = g.x + (size_t)m0 * g.ldx;
-    c.out = g.out + (size_t)m0 * g.ldo;
+    if (g.out) c.out = g.out + (size_t)m0 * g.ldo;
+    if (g.rows) c.rows = g.rows + m0;
+    if (g.rope_cs) c.rope_cs = g.rope_cs + (size_t)m0 * g.head_dim;
+    if (g.qr) c.qr = g.qr + (size_t)m0 * g.n_heads * g.head_dim;
     if (g.ss_in) c.ss_in = g.ss_in + m0;
     if (g.ss_out) c.ss_out = g.ss_out + m0;
     if (g.xg_out) c.xg_out = g.xg_out + (size_t)m0 * g.ldo;
@@ -273,6 +276,11 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     q.w[0] = m->wq[l]; q.w[1] = m->wk[l]; q.w[2] = m->wv[l];
     q.n_seg[0] = H * hd; q.n_seg[1] = G * hd; q.n_seg[2] = G * hd;
     q.n_rows = (H + 2 * G) * hd; q.kind = EPI_STORE; q.out = m->qkv; q.ldo = (H + 2 * G) * hd;
+    if (dt == SPECDEC_BF16) {  // RoPE, the query store and the KV append run in the GEMM epilogue
+      q.kind = EPI_QKV; q.out = nullptr;
+      q.rows = m->rows; q.rope_cs = m->rope_cs; q.qr = m->qr; q.kv = kv_layout(kv); q.layer = l;
+      q.n_heads = H; q.n_kv_heads = G; q.head_dim = hd;
+    }
     {
       Timed t(SPECDEC_KERNEL_QKV, s);
       SD_TRY(gemm_rows(dt, q, M, s));
@@ -280,7 +288,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     if (l == 0) rec(SPECDEC_KERNEL_QKV, q);
 
     at.layer = l;
-    {
+    if (dt != SPECDEC_BF16) {
       Timed t(SPECDEC_KERNEL_ROPE_APPEND, s);
       SD_TRY(launch_rope_append(at, s));
     }
@@ -290,7 +298,8 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     }
     if (l == 0) {
       m->rec_attn = at;
-      m->rec_valid[SPECDEC_KERNEL_ROPE_APPEND] = m->rec_valid[SPECDEC_KERNEL_ATTENTION] = true;
+      m->rec_valid[SPECDEC_KERNEL_ATTENTION] = true;
+      m->rec_valid[SPECDEC_KERNEL_ROPE_APPEND] = dt != SPECDEC_BF16;
     }
 
     GemmArgs o = base;  // O projection + residual
@@ -385,8 +394,12 @@ specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specde
     }
   }
   hipStream_t s = (hipStream_t)stream;
-  for (size_t i = 0; i < mats.size(); ++i)
-    SD_TRY(launch_pack(src[i], (char*)packed + mats[i].off, mats[i].N, mats[i].K, s));
+  for (size_t i = 0; i < mats.size(); ++i) {
+    // Wq and Wk (matrices 1 and 2 of each layer's seven) carry the RoPE pair order
+    const int in_layer = i == 0 ? -1 : (int)((i - 1) % 7);
+    const int rope_hd = in_layer == 0 || in_layer == 1 ? desc->head_dim : 0;
+    SD_TRY(launch_pack(src[i], (char*)packed + mats[i].off, mats[i].N, mats[i].K, rope_hd, s));
+  }
   return SPECDEC_OK;
 }
 

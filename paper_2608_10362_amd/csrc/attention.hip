@@ -1,15 +1,8 @@
 // RoPE + KV append and GQA attention of the verify / draft passes against the
 // resident KV cache.
 //
-// KV layout (per layer l, sequence b, kv head g): a K block then a V block of
-// capacity*head_dim elements each, at element offset
-// ((l*B + b)*h_kv + g) * 2*capacity*head_dim.
-//  * bf16 caches store both in MFMA operand order, in 1 KB fragments, so that
-//    every wavefront load of the attention kernel reads 1 KB contiguously:
-//    K fragment (16 positions x 32 dims): lane 16*(d%32/8) + p%16, element d%8;
-//    V fragment (32 positions x 16 dims): lane 16*(p%32/8) + d%16, element p%8.
-//  * float32 caches (the tiny configuration): K row-major [position][dim],
-//    V transposed [dim][position].
+// The KV layout (internal.h) stores bf16 caches in MFMA operand order, so
+// that every wavefront load of the attention kernel reads 1 KB contiguously.
 //
 // Attention is split over key chunks (flash-decoding style): one wave per
 // (16-query tile, 64-key split, kv head, sequence) computes, for every query
@@ -23,30 +16,6 @@
 namespace specdec {
 
 namespace {
-
-template <typename KT>
-__device__ __forceinline__ KT* k_block(const KvLayout& kv, int layer, int b, int g) {
-  size_t off = (((size_t)layer * kv.batch + b) * kv.n_kv_heads + g) * 2 * (size_t)kv.capacity * kv.head_dim;
-  return (KT*)kv.data + off;
-}
-
-// Element offsets of K[p][d] and V[p][d] inside a (layer, sequence, kv head) block.
-template <typename KT> struct KvIndex;
-template <> struct KvIndex<float> {
-  __device__ static size_t k(int p, int d, int hd, int cap) { return (size_t)p * hd + d; }
-  __device__ static size_t v(int p, int d, int hd, int cap) { return (size_t)cap * hd + (size_t)d * cap + p; }
-};
-template <> struct KvIndex<uint16_t> {
-  __device__ static size_t k(int p, int d, int hd, int cap) {
-    const int kst = hd / 32;
-    return ((size_t)((p >> 4) * kst + (d >> 5)) * 64 + ((d & 31) >> 3) * 16 + (p & 15)) * 8 + (d & 7);
-  }
-  __device__ static size_t v(int p, int d, int hd, int cap) {
-    const int dt = hd / 16;
-    return (size_t)cap * hd + ((size_t)((p >> 5) * dt + (d >> 4)) * 64 + ((p & 31) >> 3) * 16 + (d & 15)) * 8 +
-           (p & 7);
-  }
-};
 
 // ---------------------------------------------------------------- RoPE + append
 // Block (head slot, row): slots [0, H) rotate a query head into qr, [H, H+G)

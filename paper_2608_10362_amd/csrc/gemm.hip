@@ -23,6 +23,14 @@ constexpr int kMfmaWaves = kMfmaThreads / kWave;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + expf(-z)); }
 
+// Raw buffer descriptor over `bytes` bytes at `base` (dword 3: the gfx9 raw
+// buffer format); loads past `bytes` return zeros.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kNonTemporal = 2;  // cache-policy bit of a streamed (read-once) load
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 __device__ __forceinline__ float load_gain(const void* g, int bf16, int n) {
   return bf16 ? bf16_bits_to_f32(((const uint16_t*)g)[n]) : ((const float*)g)[n];
 }
@@ -42,18 +50,20 @@ __device__ __forceinline__ void row_scale(const GemmArgs& a, float* scale) {
   }
 }
 
-// Epilogue over this block's final sums yfin[m][c], c < NC columns.
-template <int NC, int KIND>
+// Epilogue over this block's final sums yfin[m][c], c < NC columns (store,
+// residual, SwiGLU; the MFMA kernel has its own residual and QKV epilogues
+// that take their inputs from registers and LDS).
+template <int NC, int KIND, int NTH>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfin)[NC + 1], const float* scale) {
-  const int M = a.M;
+  const int M = a.M;  // (NTH = threads of the block: a constant, not a read of the dispatch packet)
   if (KIND == EPI_STORE) {
-    for (int i = threadIdx.x; i < M * NC; i += blockDim.x) {
+    for (int i = threadIdx.x; i < M * NC; i += NTH) {
       int m = i / NC, c = i % NC;
       int n = blk * NC + c;
       if (n < a.n_rows) a.out[(size_t)m * a.ldo + n] = yfin[m][c] * scale[m];
     }
   } else if (KIND == EPI_RESID) {
-    for (int i = threadIdx.x; i < M * NC; i += blockDim.x) {
+    for (int i = threadIdx.x; i < M * NC; i += NTH) {
       int m = i / NC, c = i % NC;
       int n = blk * NC + c;
       float hv = 0.f;
@@ -66,14 +76,14 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfi
       yfin[m][c] = hv;
     }
     __syncthreads();
-    for (int m = threadIdx.x; m < M; m += blockDim.x) {
+    for (int m = threadIdx.x; m < M; m += NTH) {
       float t = 0.f;
       for (int c = 0; c < NC; ++c) t += yfin[m][c] * yfin[m][c];
       a.ss_out[(size_t)blk * a.ss_ld + m] = t;
     }
   } else {  // EPI_SWIGLU: columns [0, NC/2) gate, [NC/2, NC) up
     constexpr int H = NC / 2;
-    for (int i = threadIdx.x; i < M * H; i += blockDim.x) {
+    for (int i = threadIdx.x; i < M * H; i += NTH) {
       int m = i / H, c = i % H;
       int n = blk * H + c;
       if (n < a.n_rows) {
@@ -143,11 +153,18 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   constexpr int MP = 16 * MT;
   constexpr int NF = T * MT;              // accumulator fragments per wave
   constexpr int RR = NF <= 2 ? NF : 2;    // fragments reduced per LDS round
+  constexpr bool QKV = KIND == EPI_QKV;
+  constexpr int E = (MP * NC + kMfmaThreads - 1) / kMfmaThreads;  // epilogue elements per thread
   __shared__ float red[RR][kMfmaWaves][kWave][4];
   __shared__ float yfin[MP][NC + 1];
   __shared__ float scale[MP];
+  __shared__ RowDesc s_rows[QKV ? MP : 1];
+  __shared__ float s_cs[QKV ? MP : 1][QKV ? 128 : 1];  // RoPE cos | sin of each row (head_dim <= 128)
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The wave index is uniform across the wave; saying so keeps every per-wave
+  // quantity derived from it (k-step list, tile, weight segment, buffer
+  // descriptors) in scalar registers.
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = lane >> 4, mrow = lane & 15;
   const int K = a.K;
   const int KS = (K + 31) / 32;
@@ -173,35 +190,64 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
 
   u32x4 wA[UB][T], wB[UB][T];
   f32x4 xA[UB][MT][2], xB[UB][MT][2];
+  // Residual epilogue inputs (old h and the next RMSNorm gain) of the tile whose
+  // last batch sits in the matching register buffer, fetched with that batch.
+  // (Only when every thread has at most one epilogue element; larger row
+  // counts read them in the epilogue, keeping the registers for the loads.)
+  constexpr bool PRE = KIND == EPI_RESID && E == 1;
+  struct Pre {
+    float h[E];
+    uint32_t g[E];  // bf16 bits of the gain (bf16 models only run this kernel)
+  } pA, pB;
+  auto epi_fetch = [&](int q, Pre& p) {
+    if constexpr (PRE) {
+      // (every batch fetches its tile's inputs: no branch; the copy fetched with
+      // the tile's last batch is the one its epilogue uses)
+      const int tile = blockIdx.x + (q / nbat) * gridDim.x;
+      const __amdgpu_buffer_rsrc_t hr = make_rsrc(a.out, (uint32_t)a.M * a.ldo * 4u);
+      const __amdgpu_buffer_rsrc_t gr = make_rsrc(a.gain_out, (uint32_t)a.n_rows * 2u);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int i = tid + e * kMfmaThreads, m = i / NC, n = tile * NC + i % NC;
+        const uint32_t bad = (uint32_t)(n >= a.n_rows) << 31;  // (rows m >= M fall outside hr)
+        p.h[e] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(hr, (((uint32_t)m * a.ldo + n) * 4u) | bad, 0, 0));
+        p.g[e] = __builtin_amdgcn_raw_buffer_load_b16(gr, ((uint32_t)n * 2u) | bad, 0, 0);
+      }
+    }
+  };
+  // Loads go through buffer descriptors: an offset past the descriptor's range
+  // reads zeros without touching memory, so rows beyond M, tiles beyond N and
+  // k-steps beyond the wave's list need no branches (a branch around a load
+  // makes the compiler wait for the data where the paths join).
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
   // load the q-th batch of this wave's work list (tile q / nbat, k-steps from (q % nbat) * UB)
   auto load = [&](int q, u32x4 (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
     const int kb = (q % nbat) * UB;  // index into this wave's k-step list
-    const uint16_t* wtile[T];
-    bool rok[T];
+    __amdgpu_buffer_rsrc_t wr[T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) wtile[t] = weight_tile(a, KIND, tile, NC, t, KS, rok[t]) + lane * 8;
+    for (int t = 0; t < T; ++t) {
+      bool rok;
+      const uint16_t* base = weight_tile(a, KIND, tile, NC, t, KS, rok);
+      wr[t] = make_rsrc(base, rok ? (uint32_t)KS * 1024u : 0u);
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int ks = ks0 + (kb + u) * kstride;
       const int k = ks * 32 + kg * 8;
-      const bool kok = (kb + u) < my_ks && ks < KS;
+      // (out-of-range flags are OR-ed into the offsets: a select on a wave-uniform
+      // flag would become a branch)
+      const uint32_t wbad = (uint32_t)((kb + u) >= my_ks || ks >= KS) << 31;
+      const uint32_t woff = ((uint32_t)ks * 1024u + lane * 16u) | wbad;
 #pragma unroll
-      for (int t = 0; t < T; ++t) {
-        if (kok && rok[t]) wv[u][t] = __builtin_nontemporal_load((const u32x4*)(wtile[t] + (size_t)ks * 512));
-        else wv[u][t] = u32x4{0u, 0u, 0u, 0u};
-      }
+      for (int t = 0; t < T; ++t) wv[u][t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], woff, 0, kNonTemporal);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = mt * 16 + mrow;
-        if (kok && k < K && m < a.M) {
-          const f32x4* xp = (const f32x4*)(a.x + (size_t)m * a.ldx + k);
-          xv[u][mt][0] = xp[0];
-          xv[u][mt][1] = xp[1];
-        } else {
-          xv[u][mt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-          xv[u][mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        const uint32_t xoff = (((uint32_t)m * a.ldx + k) * 4u) | wbad | ((uint32_t)(k >= K) << 31);
+        xv[u][mt][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff, 0, 0));
+        xv[u][mt][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16u, 0, 0));
       }
     }
   };
@@ -227,8 +273,64 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       }
     }
   };
+  auto mfma_epilogue = [&](int blk, const Pre& p) {
+    const int M = a.M;
+    if constexpr (PRE) {
+      const int m = tid / NC, c = tid % NC, n = blk * NC + c;
+      if (m < M) {
+        float hv = 0.f;
+        if (n < a.n_rows) {
+          hv = p.h[0] + yfin[m][c];
+          a.out[(size_t)m * a.ldo + n] = hv;
+          a.xg_out[(size_t)m * a.ldo + n] = hv * bf16_bits_to_f32((uint16_t)p.g[0]);
+        }
+        yfin[m][c] = hv;
+      }
+      __syncthreads();
+      for (int m = tid; m < M; m += kMfmaThreads) {
+        float t = 0.f;
+        for (int c = 0; c < NC; ++c) t += yfin[m][c] * yfin[m][c];
+        a.ss_out[(size_t)blk * a.ss_ld + m] = t;
+      }
+    } else if constexpr (KIND == EPI_QKV) {
+      // Columns of the Q and K segments come in RoPE pairs: column c (c % 16 < 8)
+      // is dim j = 8 * (tile within the head) + c % 8 of its head, column c ^ 8
+      // is dim j + hd/2.  x1' = x1 cos - x2 sin, x2' = x2 cos + x1 sin.
+      const int hd = a.head_dim, half = hd >> 1, H = a.n_heads;
+      const int nq = a.n_seg[0], nqk = nq + a.n_seg[1], cap = a.kv.capacity;
+#pragma unroll 1
+      for (int i = tid; i < M * NC; i += kMfmaThreads) {
+        const int m = i / NC, c = i % NC, n = blk * NC + c;
+        if (n >= a.n_rows) continue;
+        const float x = yfin[m][c] * scale[m];
+        const RowDesc rd = s_rows[m];
+        if (n < nqk) {
+          const bool is_k = n >= nq;
+          const int r = is_k ? n - nq : n;
+          const int head = r / hd, w = r % hd, ec = w & 15;
+          const int j = 8 * (w >> 4) + (ec & 7);
+          const float y = yfin[m][c ^ 8] * scale[m];
+          const float cs = s_cs[m][j], sn = s_cs[m][half + j];
+          const float out = ec < 8 ? x * cs - y * sn : x * cs + y * sn;
+          const int d = ec < 8 ? j : half + j;
+          if (!is_k) {
+            a.qr[((size_t)m * H + head) * hd + d] = out;
+          } else if (rd.valid) {
+            uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+            Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::k(rd.pos, d, hd, cap), out);
+          }
+        } else if (rd.valid) {
+          const int r = n - nqk, head = r / hd, d = r % hd;
+          uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+          Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::v(rd.pos, d, hd, cap), x);
+        }
+      }
+    } else {
+      epilogue<NC, KIND, kMfmaThreads>(a, blk, yfin, scale);
+    }
+  };
   // After the last batch of a tile: cross-wave reduction (fixed wave order) and epilogue.
-  auto finish = [&](int q) {
+  auto finish = [&](int q, const Pre& p) {
     if (q % nbat != nbat - 1) return;
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
 #pragma unroll
@@ -256,30 +358,109 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
     for (int t = 0; t < T; ++t)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    epilogue<NC, KIND>(a, tile, yfin, scale);
+    mfma_epilogue(tile, p);
     __syncthreads();  // yfin is reused by the next tile
   };
 
+  // Prologue.  The small operands only the epilogue needs (row-scale partial
+  // sums, the QKV tables) are requested first, then both register buffers'
+  // weight batches; storing the small ones then waits for them alone (loads
+  // complete in order), so no wave waits for a weight batch before its first
+  // multiply.
+  constexpr int RS_ROWS = (MP + kMfmaWaves - 1) / kMfmaWaves;  // scale rows per wave
+  constexpr int RS_P = 4;                                      // partial sums per lane held
+  float rs_v[RS_ROWS][RS_P];
+  {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(a.ss_in, a.ss_in ? (uint32_t)a.n_ss * a.ss_ld * 4u : 0u);
+#pragma unroll
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kMfmaWaves;
+#pragma unroll
+      for (int i = 0; i < RS_P; ++i) {
+        const int p = lane + i * kWave;
+        const uint32_t off = (m < a.M && p < a.n_ss) ? ((uint32_t)p * a.ss_ld + m) * 4u : kOutOfRange;
+        rs_v[r][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off, 0, 0));
+      }
+    }
+  }
+  constexpr bool HOIST = QKV && MT <= 2;  // (the 64-row tables would cost spills)
+  constexpr int CS_E = HOIST ? MP * 128 / kMfmaThreads : 1;  // table entries per thread
+  float cs_v[CS_E];
+  RowDesc rd_v{0, 0, 0, 0};
+  if constexpr (HOIST) {
+    const __amdgpu_buffer_rsrc_t cr = make_rsrc(a.rope_cs, (uint32_t)a.M * a.head_dim * 4u);
+#pragma unroll
+    for (int e = 0; e < CS_E; ++e) {
+      const int i = tid + e * kMfmaThreads, m = i / 128, j = i % 128;
+      const uint32_t off = j < a.head_dim ? ((uint32_t)m * a.head_dim + j) * 4u : kOutOfRange;
+      cs_v[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(cr, off, 0, 0));
+    }
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.rows, (uint32_t)a.M * (uint32_t)sizeof(RowDesc));
+    rd_v = __builtin_bit_cast(RowDesc, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rr, tid < MP ? (uint32_t)tid * (uint32_t)sizeof(RowDesc) : kOutOfRange, 0, 0));
+  }
   int q = 0;
-  if (total > 0) load(0, wA, xA);
-  // The row scale is only needed by the epilogue: computed while the first loads fly.
-  row_scale<MP>(a, scale);
+  if (total > 0) {
+    load(0, wA, xA);
+    epi_fetch(0, pA);
+  }
+  if (PIPE && total > 1) {
+    load(1, wB, xB);
+    epi_fetch(1, pB);
+  }
+  // s_m = 1/sqrt(sum_p ss[p][m] / K + eps): lanes sum their partials in p order
+  // (held ones first, then any beyond 64*RS_P), fixed shuffle tree.
+#pragma unroll
+  for (int r = 0; r < RS_ROWS; ++r) {
+    const int m = wave + r * kMfmaWaves;
+    if (m >= MP) break;
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < RS_P; ++i) t += rs_v[r][i];
+    if (a.ss_in && m < a.M)
+      for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t += a.ss_in[(size_t)p * a.ss_ld + m];
+    t = wave_sum(t);
+    if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+  }
+  if constexpr (HOIST) {
+#pragma unroll
+    for (int e = 0; e < CS_E; ++e) {
+      const int i = tid + e * kMfmaThreads;
+      s_cs[i / 128][i % 128] = cs_v[e];
+    }
+    if (tid < MP) s_rows[tid] = rd_v;
+  } else if constexpr (QKV) {
+    for (int i = tid; i < MP; i += kMfmaThreads) s_rows[i] = i < a.M ? a.rows[i] : RowDesc{0, 0, 0, 0};
+    for (int i = tid; i < MP * 128; i += kMfmaThreads) {
+      const int m = i / 128, j = i % 128;
+      s_cs[m][j] = (m < a.M && j < a.head_dim) ? a.rope_cs[(size_t)m * a.head_dim + j] : 0.f;
+    }
+  }
   if (PIPE) {
     while (q < total) {
-      if (q + 1 < total) load(q + 1, wB, xB);
       compute(wA, xA);
-      finish(q);
+      finish(q, pA);
+      if (q + 2 < total) {
+        load(q + 2, wA, xA);
+        epi_fetch(q + 2, pA);
+      }
       if (++q >= total) break;
-      if (q + 1 < total) load(q + 1, wA, xA);
       compute(wB, xB);
-      finish(q);
+      finish(q, pB);
+      if (q + 2 < total) {
+        load(q + 2, wB, xB);
+        epi_fetch(q + 2, pB);
+      }
       ++q;
     }
   } else {
     for (; q < total; ++q) {
-      if (q > 0) load(q, wA, xA);
+      if (q > 0) {
+        load(q, wA, xA);
+        epi_fetch(q, pA);
+      }
       compute(wA, xA);
-      finish(q);
+      finish(q, pA);
     }
   }
 }
@@ -318,7 +499,7 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
     }
   }
   __syncthreads();
-  epilogue<NC, KIND>(a, blk, yfin, scale);
+  epilogue<NC, KIND, 256>(a, blk, yfin, scale);
 }
 
 // k-steps per register buffer and whether two buffers are kept (the next
@@ -346,10 +527,18 @@ int compute_units() {
   return cus;
 }
 
+// The residual and QKV epilogues keep more live registers: one k-step per
+// buffer for single-tile units over more than 16 rows.
+template <int T, int MT, int KIND> struct BatchK {
+  static constexpr bool tight = (KIND == EPI_RESID || KIND == EPI_QKV) && T == 1 && MT >= 2;
+  static constexpr int UB = tight ? 1 : Batch<T, MT>::UB;
+  static constexpr bool PIPE = Batch<T, MT>::PIPE;
+};
+
 template <int T, int MT, int KIND>
 void launch_mfma_mt(const GemmArgs& a, int tiles, hipStream_t s) {
   const int grid = tiles < compute_units() ? tiles : compute_units();
-  hipLaunchKernelGGL((gemm_bf16_mfma<T, MT, Batch<T, MT>::UB, Batch<T, MT>::PIPE, KIND>), dim3(grid),
+  hipLaunchKernelGGL((gemm_bf16_mfma<T, MT, BatchK<T, MT, KIND>::UB, BatchK<T, MT, KIND>::PIPE, KIND>), dim3(grid),
                      dim3(kMfmaThreads), 0, s, a, tiles);
 }
 
@@ -385,14 +574,20 @@ int mfma_tiles(int kind, int n_rows) {
 }
 
 // One thread per 16-byte piece of the packed image of W [N, K] (row-major).
-__global__ void pack_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst, int N, int K, int KS) {
+__global__ void pack_kernel(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst, int N, int K, int KS,
+                            int rope_hd) {
   const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
   const size_t pieces = (size_t)(N / 16) * KS * 64;
   if (i >= pieces) return;
   const int lane = (int)(i % 64);
   const size_t frag = i / 64;
   const int ks = (int)(frag % KS), t = (int)(frag / KS);
-  const int row = 16 * t + (lane & 15), k = 32 * ks + 8 * (lane >> 4);
+  int row = 16 * t + (lane & 15);
+  if (rope_hd > 0) {  // tile t of its head: rows 8t' + e and hd/2 + 8t' + e, e < 8
+    const int head = (16 * t) / rope_hd, tq = (16 * t) % rope_hd / 16, e = lane & 15;
+    row = head * rope_hd + (e < 8 ? 8 * tq + e : rope_hd / 2 + 8 * tq + (e - 8));
+  }
+  const int k = 32 * ks + 8 * (lane >> 4);
   u32x4 v = u32x4{0u, 0u, 0u, 0u};
   if (k + 8 <= K) {
     v = *(const u32x4*)(src + (size_t)row * K + k);
@@ -410,12 +605,13 @@ __global__ void pack_kernel(const uint16_t* __restrict__ src, uint16_t* __restri
 
 size_t packed_elems(int N, int K) { return (size_t)(N / 16) * ((K + 31) / 32) * 512; }
 
-hipError_t launch_pack(const void* src, void* dst, int N, int K, hipStream_t s) {
+hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s) {
   if (N % 16 || K % 8) return hipErrorInvalidValue;
+  if (rope_hd < 0 || (rope_hd > 0 && (rope_hd % 16 || N % rope_hd))) return hipErrorInvalidValue;
   const int KS = (K + 31) / 32;
   const size_t pieces = (size_t)(N / 16) * KS * 64;
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, (const uint16_t*)src,
-                     (uint16_t*)dst, N, K, KS);
+                     (uint16_t*)dst, N, K, KS, rope_hd);
   return hipGetLastError();
 }
 
@@ -434,6 +630,7 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.M > kMaxGemmRows || (a.K % 8) != 0 || (a.ldx % 4) != 0) return hipErrorInvalidValue;
   const int blocks = gemm_row_blocks(dtype, a.kind, a.n_rows, a.M);
   if (dtype == SPECDEC_BF16) {
+    if (a.kind == EPI_RESID && !a.gain_bf16) return hipErrorInvalidValue;
     const int T = mfma_tiles(a.kind, a.n_rows);
     switch (a.kind) {
       case EPI_STORE:
@@ -443,6 +640,11 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
         return T == 1 ? launch_mfma_t<1, EPI_RESID>(a, blocks, s)
                       : (T == 2 ? launch_mfma_t<2, EPI_RESID>(a, blocks, s) : launch_mfma_t<3, EPI_RESID>(a, blocks, s));
       case EPI_SWIGLU: return launch_mfma_t<2, EPI_SWIGLU>(a, blocks, s);
+      case EPI_QKV:
+        if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
+          return hipErrorInvalidValue;
+        return T == 1 ? launch_mfma_t<1, EPI_QKV>(a, blocks, s)
+                      : (T == 2 ? launch_mfma_t<2, EPI_QKV>(a, blocks, s) : launch_mfma_t<3, EPI_QKV>(a, blocks, s));
     }
     return hipErrorInvalidValue;
   }

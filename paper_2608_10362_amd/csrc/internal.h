@@ -10,11 +10,53 @@
 
 namespace specdec {
 
+// ------------------------------------------------------------------ KV cache layout
+// Per layer l, sequence b, kv head g: a K block then a V block of
+// capacity*head_dim elements each, at element offset
+// ((l*B + b)*h_kv + g) * 2*capacity*head_dim.
+//  * bf16 caches store both in MFMA operand order, in 1 KB fragments:
+//    K fragment (16 positions x 32 dims): lane 16*(d%32/8) + p%16, element d%8;
+//    V fragment (32 positions x 16 dims): lane 16*(p%32/8) + d%16, element p%8.
+//  * float32 caches: K row-major [position][dim], V transposed [dim][position].
+struct KvLayout {
+  void* data;
+  int batch, capacity, n_kv_heads, head_dim, dtype;
+  size_t layer_elems() const { return (size_t)batch * n_kv_heads * 2 * (size_t)capacity * head_dim; }
+};
+
+template <typename KT>
+__device__ __forceinline__ KT* k_block(const KvLayout& kv, int layer, int b, int g) {
+  size_t off = (((size_t)layer * kv.batch + b) * kv.n_kv_heads + g) * 2 * (size_t)kv.capacity * kv.head_dim;
+  return (KT*)kv.data + off;
+}
+
+// Element offsets of K[p][d] and V[p][d] inside a (layer, sequence, kv head) block.
+template <typename KT> struct KvIndex;
+template <> struct KvIndex<float> {
+  __device__ static size_t k(int p, int d, int hd, int cap) { return (size_t)p * hd + d; }
+  __device__ static size_t v(int p, int d, int hd, int cap) { return (size_t)cap * hd + (size_t)d * cap + p; }
+};
+template <> struct KvIndex<uint16_t> {
+  __device__ static size_t k(int p, int d, int hd, int cap) {
+    const int kst = hd / 32;
+    return ((size_t)((p >> 4) * kst + (d >> 5)) * 64 + ((d & 31) >> 3) * 16 + (p & 15)) * 8 + (d & 7);
+  }
+  __device__ static size_t v(int p, int d, int hd, int cap) {
+    const int dt = hd / 16;
+    return (size_t)cap * hd + ((size_t)((p >> 5) * dt + (d >> 4)) * 64 + ((p & 31) >> 3) * 16 + (d & 15)) * 8 +
+           (p & 7);
+  }
+};
+
 // ------------------------------------------------------------------ GEMM
 // y = (x (.) gain) W^T, optional per-row scale s_m = 1/sqrt(mean_k h_mk^2 + eps)
 // taken from partial sums of squares, W bf16 or f32 row-major [N, K] split in
 // up to three row segments (Wq|Wk|Wv, or gate|up for SwiGLU).
-enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// EPI_QKV (bf16 only): Q|K|V projections whose epilogue applies RoPE to the
+// query and key rows, writes the rotated queries to qr and appends K and V
+// to the cache.  It needs the rotation pairs (j, j + hd/2) of a head in the
+// same 16-row tile, which the packed image provides (see launch_pack).
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 constexpr int kMaxGemmRows = 64;  // rows of x per GEMM launch (callers split larger M)
 
 struct GemmArgs {
@@ -34,10 +76,19 @@ struct GemmArgs {
   float* xg_out;       // RESID: [M, ldo] new residual times gain_out (input of the next RMSNorm'd GEMM)
   const void* gain_out;
   int gain_bf16;
+  // EPI_QKV
+  const RowDesc* rows;    // [M]
+  const float* rope_cs;   // [M, hd]: cos (j < hd/2) then sin
+  float* qr;              // [M, H, hd] rotated queries
+  KvLayout kv;
+  int layer, n_heads, n_kv_heads, head_dim;
 };
-// Packed bf16 weight image (16-row x 32-column 1 KB fragments in MFMA operand order).
+// Packed bf16 weight image (16-row x 32-column 1 KB fragments in MFMA operand
+// order).  rope_hd > 0 reorders the rows of each head of rope_hd rows so that
+// tile t of the head holds rows 8t..8t+7 then rope_hd/2 + 8t .. +7 (the
+// rotation pairs of RoPE side by side, 8 columns apart); 0 keeps the order.
 size_t packed_elems(int N, int K);
-hipError_t launch_pack(const void* src, void* dst, int N, int K, hipStream_t s);
+hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s);
 // Number of row blocks the launcher uses for this GEMM (for ss partial counts).
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M);
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
@@ -67,11 +118,6 @@ struct RowsArgs {
 hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------------ attention
-struct KvLayout {
-  void* data;
-  int batch, capacity, n_kv_heads, head_dim, dtype;
-  size_t layer_elems() const { return (size_t)batch * n_kv_heads * 2 * (size_t)capacity * head_dim; }
-};
 struct AttnArgs {
   const RowDesc* rows;
   int M, rps, n_heads, n_kv_heads, head_dim;
