@@ -192,36 +192,41 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
   const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;
 
-  // Q fragments (A operand) first: query qa = mt*16 + l%16, pre-scaled by 1/sqrt(hd).
-  float qv[KST][8];
-  {
-    const int qa = mt * 16 + c16;
-    const float* qp = nullptr;
-    if (qa < nq) {
-      const int row = r0 + qa / group, head = g * group + qa % group;
-      qp = a.qr + ((size_t)row * H + head) * HD;
-    }
-#pragma unroll
-    for (int c = 0; c < KST; ++c) {
-      if (qp) {
-        const f32x4* q4 = (const f32x4*)(qp + 32 * c + 8 * grp);
-        const f32x4 lo4 = q4[0], hi4 = q4[1];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) { qv[c][j] = lo4[j]; qv[c][4 + j] = hi4[j]; }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) qv[c][j] = 0.f;
-      }
-    }
-  }
-  // K and V fragments of the whole split: 2 x 16 contiguous 1 KB fragments,
-  // issued before anything waits (k0 + 64 <= capacity: always in bounds).
+  // Every load is issued before anything waits, smallest first (loads complete
+  // in order, so waiting for an early one never waits for a later one): the
+  // row descriptors, the K fragments, Q, then the V fragments.  Row
+  // descriptors and Q go through range-checked buffer loads (zeros past the
+  // range, no branch around a load).
+  // Row descriptors: lane i < rps reads row r0 + i.
+  const __amdgpu_buffer_rsrc_t rr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0, a.M * (int)sizeof(RowDesc), 0x00020000);
+  // (only the two fields used: a wider load leaves dead destination registers
+  // the allocator reuses, which forces a wait for the load)
+  const uint32_t roff = ((uint32_t)(r0 + lane) * (uint32_t)sizeof(RowDesc)) | ((uint32_t)(lane >= rps) << 31);
+  const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
+  const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
+  // K fragments of the split: 16 contiguous 1 KB fragments (k0 + 64 <= capacity: in bounds).
   u32x4 kf[NT][KST];
   const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
+  // Q fragments (A operand): query qa = mt*16 + l%16 (zeros past nq).
+  f32x4 qv4[KST][2];
+  {
+    const int qa = mt * 16 + c16;
+    const int row = r0 + qa / group, head = g * group + qa % group;
+    const __amdgpu_buffer_rsrc_t qrs =
+        __builtin_amdgcn_make_buffer_rsrc(a.qr, (short)0, a.M * H * HD * 4, 0x00020000);
+    const uint32_t qoff = ((((uint32_t)row * H + head) * HD + 8 * grp) * 4u) | ((uint32_t)(qa >= nq) << 31);
+#pragma unroll
+    for (int c = 0; c < KST; ++c) {
+      qv4[c][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c, 0, 0));
+      qv4[c][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c + 16u, 0, 0));
+    }
+  }
+  // V fragments: 2 x DT contiguous 1 KB fragments.
   u32x4 vf[2][DT];
   const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
 #pragma unroll
@@ -229,12 +234,11 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) vf[s][dt] = *(const u32x4*)(vfrag + (size_t)(s * DT + dt) * 512);
 
-  // Row descriptors: lane i < rps reads row i; nk = max(pos) + 1 over valid rows.
-  int mypos = -1;
-  if (lane < rps) {
-    const RowDesc rd = a.rows[r0 + lane];
-    if (rd.valid) mypos = rd.pos;
-  }
+  // (compiler barrier: keeps the early exit below from being hoisted above the
+  // loads, which would wait for the row descriptors before issuing them)
+  asm volatile("" ::: "memory");
+  // nk = max(pos) + 1 over the sequence's valid rows.
+  const int mypos = (lane < rps && rd_valid) ? rd_pos : -1;
   int nk = mypos + 1;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
@@ -267,7 +271,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
   for (int c = 0; c < KST; ++c) {
     float v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = qv[c][j] * scale;
+    for (int j = 0; j < 4; ++j) {
+      v[j] = qv4[c][0][j] * scale;
+      v[4 + j] = qv4[c][1][j] * scale;
+    }
     split_hilo(v, qhi[c], qlo[c]);
   }
 
@@ -384,6 +391,102 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- combine (bf16 path)
+// One wave per (row, head).  Every load is issued before the first wait: the
+// row's (max, sum) pairs (lane c holds splits c, c+64, ...) and the first 16
+// splits' partial outputs (lane holds dims lane, lane+64); each later chunk is
+// requested before the current one is accumulated.  o = sum_c w_c o_c /
+// sum_c w_c l_c with w_c = exp(m_c - max_c m_c), summed over c in order in four
+// interleaved accumulators.
+constexpr int kCombineMaxSplits = 256;  // 4 per lane
+
+template <int HD>
+__global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
+  constexpr int DPL = HD >= 64 ? HD / 64 : 1;  // dims per lane
+  constexpr int CH = 16;                        // splits per chunk of partial outputs
+  const int head = blockIdx.x, r = blockIdx.y, lane = threadIdx.x, H = a.n_heads, ns = a.n_split;
+  const size_t base = ((size_t)r * H + head) * ns;
+  const __amdgpu_buffer_rsrc_t mlr =
+      __builtin_amdgcn_make_buffer_rsrc(a.ml_part + 2 * base, (short)0, ns * 8, 0x00020000);
+  const __amdgpu_buffer_rsrc_t opr =
+      __builtin_amdgcn_make_buffer_rsrc(a.o_part + base * HD, (short)0, ns * HD * 4, 0x00020000);
+  // (two 4-byte loads per pair: this toolchain's 8-byte raw buffer load returns
+  // the low word in both elements)
+  float mv[4], lv[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t c = lane + 64 * j;
+    mv[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mlr, c * 8u, 0, 0));
+    lv[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mlr, c * 8u + 4u, 0, 0));
+  }
+  auto load_chunk = [&](int c0, float (&ov)[CH][DPL]) {
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc)
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) {
+        const uint32_t dim = lane + 64 * d;
+        const uint32_t off = (((uint32_t)(c0 + cc) * HD + dim) * 4u) | ((uint32_t)(dim >= (uint32_t)HD) << 31);
+        ov[cc][d] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(opr, off, 0, 0));
+      }
+  };
+  float ovA[CH][DPL], ovB[CH][DPL];
+  load_chunk(0, ovA);
+  asm volatile("" ::: "memory");  // (keep the loads above the exits below)
+
+  const RowDesc rd = a.rows[r];
+  float* o = a.o + ((size_t)r * H + head) * HD;
+  if (!rd.valid) {
+#pragma unroll
+    for (int d = 0; d < DPL; ++d)
+      if (lane + 64 * d < HD) o[lane + 64 * d] = 0.f;
+    return;
+  }
+  int nch = (rd.pos + 1 + kSplitKeys - 1) / kSplitKeys;
+  if (nch > ns) {  // the host's bound on the context was wrong: report, stay in bounds
+    if (lane == 0) set_status(a.status, kStatusKvCapacity);
+    nch = ns;
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (lane + 64 * j < nch) mx = fmaxf(mx, mv[j]);
+  mx = wave_max(mx);
+  float wv[4], L = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    wv[j] = lane + 64 * j < nch ? expf(mv[j] - mx) : 0.f;
+    L += wv[j] * lv[j];
+  }
+  L = wave_sum(L);
+  float acc[4][DPL];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) acc[i][d] = 0.f;
+  auto accumulate = [&](int c0, const float (&ov)[CH][DPL]) {
+#pragma unroll
+    for (int cc = 0; cc < CH; ++cc) {
+      const int c = c0 + cc;
+      if (c >= nch) break;
+      const float wj = c < 64 ? wv[0] : (c < 128 ? wv[1] : (c < 192 ? wv[2] : wv[3]));
+      const float w = __shfl(wj, c & 63, kWave);
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) acc[cc & 3][d] += w * ov[cc][d];
+    }
+  };
+  for (int c0 = 0; c0 < nch; c0 += 2 * CH) {
+    if (c0 + CH < nch) load_chunk(c0 + CH, ovB);
+    accumulate(c0, ovA);
+    if (c0 + CH >= nch) break;
+    if (c0 + 2 * CH < nch) load_chunk(c0 + 2 * CH, ovA);
+    accumulate(c0 + CH, ovB);
+  }
+  const float inv = 1.0f / L;
+#pragma unroll
+  for (int d = 0; d < DPL; ++d)
+    if (lane + 64 * d < HD) o[lane + 64 * d] = ((acc[0][d] + acc[1][d]) + (acc[2][d] + acc[3][d])) * inv;
+}
+
 // ---------------------------------------------------------------- KV context copy
 template <typename KT>
 __global__ __launch_bounds__(256) void kv_copy_kernel(KvLayout kv, int layer, int b, int pos0, const KT* k,
@@ -442,7 +545,15 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), sizeof(float) * a.n_split, s, a);
+  if (a.kv.dtype == SPECDEC_BF16 && a.n_split <= kCombineMaxSplits) {
+    switch (a.head_dim) {
+      case 32: hipLaunchKernelGGL((attn_combine_wave_kernel<32>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((attn_combine_wave_kernel<64>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
+      default: hipLaunchKernelGGL((attn_combine_wave_kernel<128>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
+    }
+  } else {
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), sizeof(float) * a.n_split, s, a);
+  }
   return hipGetLastError();
 }
 
