@@ -214,6 +214,7 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
 //             (the draft's q is also written here)
 //   final     per sequence: find the chunk holding t, scan it, emit the token
 constexpr int kChunkThreads = 256;
+constexpr int kMfmaWavesSamp = 16;  // waves of the decide kernel
 
 __host__ __device__ __forceinline__ int n_chunks(int V) {
   int nc = (V + 1023) / 1024;
@@ -308,65 +309,82 @@ __global__ __launch_bounds__(kChunkThreads) void stats_kernel(const float* x, in
   }
 }
 
-// Merge the chunk statistics of one row (fixed order).
-__device__ void merge_stats(const StatPart* parts, int NC, float& m, float& s, float& av, int& ai, int& bad) {
-  MaxSum t{parts[0].m, parts[0].s};
-  av = parts[0].amax_v;
-  ai = parts[0].amax_i;
-  bad = parts[0].bad;
-  for (int k = 1; k < NC; ++k) {
-    t = ms_merge(t, MaxSum{parts[k].m, parts[k].s});
-    if (parts[k].amax_v > av || (parts[k].amax_v == av && parts[k].amax_i < ai)) { av = parts[k].amax_v; ai = parts[k].amax_i; }
-    bad |= parts[k].bad;
+// Merge the chunk statistics of one row across a wave: lane k holds chunk k
+// (NC <= 64), xor butterfly (every lane ends with the same, deterministic
+// result: each merge is symmetric in its operands).
+__device__ StatPart wave_merge_stats(const StatPart* parts, int NC) {
+  const int lane = threadIdx.x & 63;
+  StatPart p{-INFINITY, 0.f, -INFINITY, 0x7fffffff, 0, 0, 0, 0};
+  if (lane < NC) p = parts[lane];
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const MaxSum t = ms_merge(MaxSum{p.m, p.s}, MaxSum{__shfl_xor(p.m, o, kWave), __shfl_xor(p.s, o, kWave)});
+    const float ov = __shfl_xor(p.amax_v, o, kWave);
+    const int oi = __shfl_xor(p.amax_i, o, kWave);
+    if (ov > p.amax_v || (ov == p.amax_v && oi < p.amax_i)) {
+      p.amax_v = ov;
+      p.amax_i = oi;
+    }
+    p.bad |= __shfl_xor(p.bad, o, kWave);
+    p.m = t.m;
+    p.s = t.s;
   }
-  m = t.m;
-  s = t.s;
+  return p;
 }
 
-// decide: grid B, block 64.
-__global__ __launch_bounds__(64) void accept_decide_kernel(AcceptArgs a) {
-  const int b = blockIdx.x, g = a.gamma, V = a.V, NC = n_chunks(V), lane = threadIdx.x;
+// decide: grid B, block 1024.  Wave w merges the statistics of rows w, w+16;
+// then wave 0 evaluates the gamma accept tests in parallel lanes and takes
+// the first event (rejection or error) in draft order.
+__global__ __launch_bounds__(1024) void accept_decide_kernel(AcceptArgs a) {
+  const int b = blockIdx.x, g = a.gamma, V = a.V, NC = n_chunks(V);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   Scratch sc = carve(a.scratch, a.B, g + 1, V);
   const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
   const float T = a.temperature;
   __shared__ int amax[kMaxGamma + 1];
   __shared__ float2 ms[kMaxGamma + 1];
-  int bad = 0;
-  if (lane <= g) {
-    float m, s, av;
-    int ai, bd;
-    merge_stats(sc.stats + ((size_t)b * (g + 1) + lane) * NC, NC, m, s, av, ai, bd);
-    if (logits && T > 0.f) bad |= !isfinite(m) || !isfinite(s);
-    bad |= bd;
-    amax[lane] = ai;
-    ms[lane] = make_float2(m, s);
-    sc.seq[b].ms[lane] = make_float2(m, s);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o, kWave);
+  __shared__ int bad_rows;
+  if (threadIdx.x == 0) bad_rows = 0;
   __syncthreads();
-  if (lane != 0) return;
-  const float* P = a.p + (size_t)b * (g + 1) * V;
-  const float* Q = a.q ? a.q + (size_t)b * g * V : nullptr;
-  const int32_t* d = a.d + (size_t)b * a.ld_d;
-  int A = g;
-  if (!bad) {
-    if (T == 0.f) {
-      for (int i = 0; i < g; ++i)
-        if (amax[i] != d[i]) { A = i; break; }
-    } else {
-      for (int i = 0; i < g; ++i) {
-        const int di = d[i];
-        if (di < 0 || di >= V) { bad = 1; break; }
-        const float pd = prob_of(P + (size_t)i * V, di, logits, T, ms[i]);
-        const float qd = Q[(size_t)i * V + di];
-        if (!isfinite(qd)) { bad = 1; break; }
-        const uint32_t w = a.rand ? a.rand[(size_t)b * (g + 1) + i]
-                                  : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, i);
-        if (!(__fmul_rn(word_to_uniform(w), qd) < pd)) { A = i; break; }
-      }
+  for (int r = w; r <= g; r += kMfmaWavesSamp) {
+    const StatPart p = wave_merge_stats(sc.stats + ((size_t)b * (g + 1) + r) * NC, NC);
+    if (lane == 0) {
+      amax[r] = p.amax_i;
+      ms[r] = make_float2(p.m, p.s);
+      sc.seq[b].ms[r] = make_float2(p.m, p.s);
+      if (p.bad || (logits && T > 0.f && (!isfinite(p.m) || !isfinite(p.s)))) atomicOr(&bad_rows, 1);
     }
   }
+  __syncthreads();
+  if (w != 0) return;
+  const int32_t* d = a.d + (size_t)b * a.ld_d;
+  int bad = bad_rows;
+  int A = g;
+  if (!bad) {
+    // lane i < g: event of draft position i (1 = rejection, 2 = error)
+    int ev = 0;
+    if (lane < g) {
+      const int di = d[lane];
+      if (T == 0.f) {
+        ev = amax[lane] != di ? 1 : 0;
+      } else if (di < 0 || di >= V) {
+        ev = 2;
+      } else {
+        const float pd = prob_of(a.p + ((size_t)b * (g + 1) + lane) * V, di, logits, T, ms[lane]);
+        const float qd = a.q[((size_t)b * g + lane) * V + di];
+        const uint32_t wd = a.rand ? a.rand[(size_t)b * (g + 1) + lane]
+                                   : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, lane);
+        ev = !isfinite(qd) ? 2 : (!(__fmul_rn(word_to_uniform(wd), qd) < pd) ? 1 : 0);
+      }
+    }
+    const unsigned long long hit = __ballot(ev != 0);
+    if (hit) {
+      const int first = __ffsll(hit) - 1;
+      if (__shfl(ev, first, kWave) == 2) bad = 1;
+      else A = first;
+    }
+  }
+  if (lane != 0) return;
   if (bad) {
     set_status(a.status, kStatusNonFinite);
     a.n_accepted[b] = -1;
@@ -463,33 +481,44 @@ __global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) 
   const SeqState& st = sc.seq[b];
   if (st.A < 0) return;
   const DrawPart* parts = sc.draw + (size_t)b * NC;
-  if (threadIdx.x == 0) {
-    unsigned long long tr = 0, tp = 0;
-    for (int k = 0; k < NC; ++k) { tr += parts[k].res; tp += parts[k].prob; }
-    done = 0;
-    {
-      const bool res = a.mode == W_ACCEPT && st.A < a.gamma && tr != 0;
-      const unsigned long long S = res ? tr : tp;
-      uint32_t x;
-      if (a.mode == W_ACCEPT)
-        x = f.rand ? f.rand[(size_t)b * (a.gamma + 1) + a.gamma] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_RESAMPLE, 0);
-      else
-        x = f.rand ? f.rand[b] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_DRAFT, a.slot);
-      if (S == 0) {
+  if (threadIdx.x < kWave) {  // wave 0: lane k holds chunk k; integer sums, exact in any order
+    const int lane = threadIdx.x;
+    DrawPart pk{0ull, 0ull};
+    if (lane < NC) pk = parts[lane];
+    const unsigned long long tr = wave_sum_u64(pk.res), tp = wave_sum_u64(pk.prob);
+    const bool res = a.mode == W_ACCEPT && st.A < a.gamma && tr != 0;
+    const unsigned long long S = res ? tr : tp;
+    uint32_t x;
+    if (a.mode == W_ACCEPT)
+      x = f.rand ? f.rand[(size_t)b * (a.gamma + 1) + a.gamma] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_RESAMPLE, 0);
+    else
+      x = f.rand ? f.rand[b] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_DRAFT, a.slot);
+    if (S == 0) {
+      if (lane == 0) {
         f.out[(size_t)b * f.ld_out] = -1;
         done = 1;
-      } else {
-        const unsigned long long t = scale_word(x, S);
-        unsigned long long before = 0;
-        int c = 0;
-        for (; c < NC; ++c) {
-          const unsigned long long w = res ? parts[c].res : parts[c].prob;
-          if (t < before + w) break;
-          before += w;
-        }
+      }
+    } else {
+      const unsigned long long t = scale_word(x, S);
+      const unsigned long long wk = res ? pk.res : pk.prob;
+      unsigned long long incl = wk;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const unsigned long long n = shfl_up_u64(incl, o);
+        if (lane >= o) incl += n;
+      }
+      // the chunk whose share [incl - wk, incl) of the running sum holds t
+      const unsigned long long hit = __ballot(t < incl && t >= incl - wk);
+      const int c = __ffsll(hit) - 1;
+      if (lane == c) {
         chunk_sel = c;
         use_res = res;
-        t_in_chunk = t - before;
+        t_in_chunk = t - (incl - wk);
+        done = 0;
+      }
+      if (hit == 0 && lane == 0) {  // (t < S: unreachable)
+        f.out[(size_t)b * f.ld_out] = -1;
+        done = 1;
       }
     }
   }
@@ -540,23 +569,19 @@ __global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) 
 __global__ __launch_bounds__(64) void draft_greedy_kernel(DraftFinishArgs a) {
   const int b = blockIdx.x, NC = n_chunks(a.V);
   Scratch sc = carve(a.scratch, a.B, 1, a.V);
+  const StatPart p = wave_merge_stats(sc.stats + (size_t)b * NC, NC);
   if (threadIdx.x != 0) return;
-  float m, s, av;
-  int ai, bad;
-  merge_stats(sc.stats + (size_t)b * NC, NC, m, s, av, ai, bad);
-  if (bad) set_status(a.status, kStatusNonFinite);
-  a.d_out[(size_t)b * a.ld_d + a.slot] = bad ? 0 : ai;
+  if (p.bad) set_status(a.status, kStatusNonFinite);
+  a.d_out[(size_t)b * a.ld_d + a.slot] = p.bad ? 0 : p.amax_i;
 }
 
 // draft sampling: merge statistics into the sequence state (grid B, block 64).
 __global__ __launch_bounds__(64) void draft_merge_kernel(DraftFinishArgs a) {
   const int b = blockIdx.x, NC = n_chunks(a.V);
   Scratch sc = carve(a.scratch, a.B, 1, a.V);
+  const StatPart p = wave_merge_stats(sc.stats + (size_t)b * NC, NC);
   if (threadIdx.x != 0) return;
-  float m, s, av;
-  int ai, bad;
-  merge_stats(sc.stats + (size_t)b * NC, NC, m, s, av, ai, bad);
-  bad |= !isfinite(m) || !isfinite(s);
+  const bool bad = p.bad || !isfinite(p.m) || !isfinite(p.s);
   if (bad) {
     set_status(a.status, kStatusNonFinite);
     sc.seq[b].A = -1;
@@ -564,7 +589,7 @@ __global__ __launch_bounds__(64) void draft_merge_kernel(DraftFinishArgs a) {
   } else {
     sc.seq[b].A = 0;
   }
-  sc.seq[b].ms[0] = make_float2(m, s);
+  sc.seq[b].ms[0] = make_float2(p.m, p.s);
 }
 
 __global__ void copy_logits_kernel(const float* lg, int rps, int V, float* out) {
@@ -678,7 +703,7 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(stats_kernel, dim3(NC, a.B * (a.gamma + 1)), dim3(kChunkThreads), 0, s, a.p, a.V, a.gamma + 1,
                      a.gamma + 1, 0, logits ? a.temperature : 0.f, a.temperature > 0.f ? a.q : nullptr, a.gamma,
                      sc.stats);
-  hipLaunchKernelGGL(accept_decide_kernel, dim3(a.B), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(accept_decide_kernel, dim3(a.B), dim3(64 * kMfmaWavesSamp), 0, s, a);
   if (a.temperature == 0.f) return hipGetLastError();
   DrawArgs d{};
   d.mode = W_ACCEPT;
