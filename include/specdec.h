@@ -262,6 +262,46 @@ SPECDEC_API size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, 
 SPECDEC_API specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, const int32_t* n_accepted,
                                  const int32_t* d, int32_t ld_d, const int32_t* next_token, void* stream);
 
+/* ---------------------------------------------------------------- draft reload
+ * Only K drafts stay resident; the others live in backing storage and are
+ * loaded asynchronously, overlapped with decoding, and the runtime never
+ * waits for a draft that is still loading (Sec. 3.3, Alg. 2 "asynchronously
+ * prefetch d"; Sec. 3.4, Alg. 3).  On one GPU: the backing storage is pinned
+ * host memory holding a packed image, a resident slot is a device buffer in
+ * the packed-image format, and a load is an H2D copy on a side stream whose
+ * completion an event records.  A draft model created over the slot may run
+ * on another stream once that stream waits for the event (or once
+ * specdec_event_query reports it done).  Keeping the shared LM head in the
+ * slot and reloading only a layer range avoids re-sending it. */
+
+/* Byte range [*offset, *offset + *bytes) of layers [first_layer, first_layer +
+ * n_layers) in the packed image of `desc` (the LM head occupies [0, offset of
+ * layer 0)).  Errors: INVALID_ARG (null pointers, range outside
+ * [0, desc->n_layers)), UNSUPPORTED (float32 desc: no packed image). */
+SPECDEC_API specdec_status specdec_packed_range(const specdec_model_desc* desc, int32_t first_layer, int32_t n_layers,
+                                                size_t* offset, size_t* bytes);
+
+/* Create / destroy a completion event (a HIP event without timing; host
+ * object, no device memory).  *event receives the handle. */
+SPECDEC_API specdec_status specdec_event_create(void** event);
+SPECDEC_API specdec_status specdec_event_destroy(void* event);
+
+/* Copy `bytes` bytes from host `host_src` to device `dst` on `copy_stream`
+ * (asynchronous: host_src must be pinned memory, e.g. from hipHostMalloc or a
+ * pinned torch tensor, and must stay valid until the event completes), then
+ * record `done_event` on `copy_stream`.  Returns at once.  Errors: INVALID_ARG
+ * (null pointers, bytes == 0), HIP. */
+SPECDEC_API specdec_status specdec_load_async(void* dst, const void* host_src, size_t bytes, void* copy_stream,
+                                              void* done_event);
+
+/* Make later work on `stream` wait for `event` (device-side; the host does
+ * not block). */
+SPECDEC_API specdec_status specdec_stream_wait_event(void* stream, void* event);
+
+/* Non-blocking completion test: *done = 1 when all work recorded before
+ * `event` has finished, else 0. */
+SPECDEC_API specdec_status specdec_event_query(void* event, int32_t* done);
+
 /* ---------------------------------------------------------------- building blocks */
 
 /* Fixed-point inverse-CDF draw for each row b of probs [batch, ld] (first

@@ -93,6 +93,14 @@ _SIGS = {
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                       ctypes.c_void_p]),
     "specdec_accept_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "specdec_packed_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]),
+    "specdec_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
+    "specdec_event_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "specdec_load_async": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                          ctypes.c_void_p]),
+    "specdec_stream_wait_event": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "specdec_event_query": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32)]),
     "specdec_kv_commit": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_sample": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
@@ -238,7 +246,9 @@ class DeviceWeights:
 class Model:
     """A model handle (target, or a draft = layer prefix) with its own workspace."""
 
-    def __init__(self, dw: DeviceWeights, n_layers: int, max_rows: int, max_ctx: int):
+    def __init__(self, dw: DeviceWeights, n_layers: int, max_rows: int, max_ctx: int, packed=None):
+        """``packed``: a device image to run from instead of ``dw.packed`` (a
+        draft slot, see DraftSlot); it must hold at least ``n_layers`` layers."""
         import torch
         self.dw = dw
         self.shape = dw.shape
@@ -250,7 +260,10 @@ class Model:
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dw.t["embed"].device)
         w, self._arrays = dw.c_struct(n_layers)
         h = ctypes.c_void_p()
-        pk = dw.packed
+        pk = dw.packed if packed is None else packed
+        if packed is not None:
+            _dev(packed, "packed", torch.uint8, 1)
+        self._packed = pk  # (kept alive with the handle)
         _check(lib().specdec_model_create(ctypes.byref(self.desc), ctypes.byref(w), n_layers, _ptr(pk),
                                           0 if pk is None else pk.numel(), max_rows, max_ctx,
                                           self.workspace.data_ptr(), nbytes, ctypes.byref(h)),
@@ -317,6 +330,76 @@ class KVCache:
         _check(lib().specdec_kv_read_state(ctypes.byref(self.kv), L.ctypes.data, P.ctypes.data, N.ctypes.data,
                                            S.ctypes.data, _stream(stream)), "specdec_kv_read_state")
         return {"len": L, "pending": P.reshape(B, 2), "n_pending": N, "status": int(S[0])}
+
+
+# ---------------------------------------------------------------- draft reload
+def packed_range(shape, first_layer: int, n_layers: int):
+    """(offset, bytes) of layers [first_layer, first_layer + n_layers) in the packed image."""
+    d = make_desc(shape)
+    off, nb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().specdec_packed_range(ctypes.byref(d), first_layer, n_layers, ctypes.byref(off), ctypes.byref(nb)),
+           "specdec_packed_range")
+    return off.value, nb.value
+
+
+class Event:
+    """A completion event owned by the library (see specdec_event_create)."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(lib().specdec_event_create(ctypes.byref(h)), "specdec_event_create")
+        self.handle = h
+
+    def query(self) -> bool:
+        done = ctypes.c_int32(0)
+        _check(lib().specdec_event_query(self.handle, ctypes.byref(done)), "specdec_event_query")
+        return bool(done.value)
+
+    def wait(self, stream=None):
+        """Make `stream` (default: the current one) wait for the event."""
+        _check(lib().specdec_stream_wait_event(_stream(stream), self.handle), "specdec_stream_wait_event")
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.specdec_event_destroy(self.handle)
+            self.handle = None
+
+
+class DraftSlot:
+    """One resident draft slot: a device buffer in the packed-image format for
+    drafts of up to ``max_layers`` layers (drafts are layer prefixes of the
+    target, so their images are prefixes of its image).  The backing storage
+    is a pinned host copy of that image prefix.  The shared LM head is copied
+    into the slot once; ``load_async`` then re-sends only the layers of the
+    draft being made resident, on ``copy_stream``, and ``event`` completes when
+    they have landed."""
+
+    def __init__(self, dw: DeviceWeights, max_layers: int):
+        import torch
+        if dw.packed is None:
+            raise ValueError("draft slots hold packed (bf16) images")
+        self.shape = dw.shape.with_layers(dw.n_layers)
+        self.max_layers = max_layers
+        off0, nb = packed_range(self.shape, 0, max_layers)
+        self.nbytes = off0 + nb
+        dev = dw.packed.device
+        self.slot = torch.empty(self.nbytes, dtype=torch.uint8, device=dev)
+        self.host = torch.empty(self.nbytes, dtype=torch.uint8, pin_memory=True)
+        self.host.copy_(dw.packed[:self.nbytes])
+        self.slot[:off0].copy_(dw.packed[:off0])  # the shared LM head, once
+        torch.cuda.current_stream().synchronize()
+        self.event = Event()
+        self.layers = 0  # layers whose load has been issued
+
+    def load_async(self, n_layers: int, copy_stream=None) -> int:
+        """Issue the H2D copy of layers [0, n_layers); returns the bytes sent."""
+        if not 0 < n_layers <= self.max_layers:
+            raise ValueError("n_layers outside the slot")
+        off, nb = packed_range(self.shape, 0, n_layers)
+        _check(lib().specdec_load_async(self.slot.data_ptr() + off, self.host.data_ptr() + off, nb,
+                                        _stream(copy_stream), self.event.handle), "specdec_load_async")
+        self.layers = n_layers
+        return nb
 
 
 # ---------------------------------------------------------------- entry points

@@ -666,6 +666,65 @@ specdec_status specdec_verify(const specdec_model* target, specdec_kv* kv, int32
   return forward(target, kv, ra, (int)(kv->len_upper + gamma + 1), logits_out, (hipStream_t)stream);
 }
 
+specdec_status specdec_packed_range(const specdec_model_desc* desc, int32_t first_layer, int32_t n_layers,
+                                    size_t* offset, size_t* bytes) {
+  specdec_status st = check_desc(desc);
+  if (st != SPECDEC_OK) return st;
+  if (desc->dtype != SPECDEC_BF16) return SPECDEC_ERR_UNSUPPORTED;
+  if (!offset || !bytes || first_layer < 0 || n_layers <= 0 || first_layer + n_layers > desc->n_layers)
+    return SPECDEC_ERR_INVALID_ARG;
+  std::vector<PackedMat> mats;
+  const size_t total = image_layout(desc, first_layer + n_layers, &mats);
+  // matrices: [0] LM head, then 7 per layer
+  *offset = mats[1 + 7 * (size_t)first_layer].off;
+  *bytes = total - *offset;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_event_create(void** event) {
+  if (!event) return SPECDEC_ERR_INVALID_ARG;
+  *event = nullptr;
+  hipEvent_t e = nullptr;
+  SD_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  *event = (void*)e;
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_event_destroy(void* event) {
+  if (!event) return SPECDEC_ERR_INVALID_ARG;
+  SD_TRY(hipEventDestroy((hipEvent_t)event));
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_load_async(void* dst, const void* host_src, size_t bytes, void* copy_stream, void* done_event) {
+  if (!dst || !host_src || !bytes || !done_event) return SPECDEC_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)copy_stream;
+  SD_TRY(hipMemcpyAsync(dst, host_src, bytes, hipMemcpyHostToDevice, s));
+  SD_TRY(hipEventRecord((hipEvent_t)done_event, s));
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_stream_wait_event(void* stream, void* event) {
+  if (!event) return SPECDEC_ERR_INVALID_ARG;
+  SD_TRY(hipStreamWaitEvent((hipStream_t)stream, (hipEvent_t)event, 0));
+  return SPECDEC_OK;
+}
+
+specdec_status specdec_event_query(void* event, int32_t* done) {
+  if (!event || !done) return SPECDEC_ERR_INVALID_ARG;
+  const hipError_t e = hipEventQuery((hipEvent_t)event);
+  if (e == hipSuccess) {
+    *done = 1;
+    return SPECDEC_OK;
+  }
+  if (e == hipErrorNotReady) {
+    (void)hipGetLastError();  // clear the not-ready code
+    *done = 0;
+    return SPECDEC_OK;
+  }
+  return SPECDEC_ERR_HIP;
+}
+
 size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab) {
   if (batch <= 0 || gamma < 0 || gamma > 31 || vocab <= 0) return 0;
   return sampling_scratch_bytes(batch, gamma + 1, vocab);

@@ -119,3 +119,37 @@ def test_call_argument_errors_before_any_launch(lib):
     assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1
     assert lib.specdec_sample(1, 10, None, 10, None, 0, 0, 0, 0, None, None) == -1
     assert lib.specdec_draw_u32(1, 0, 0, 0x10000, 0, ctypes.c_void_p(256), None) == -1
+
+
+def test_packed_range_tiles_the_image(lib):
+    shape = synth.LLAMA_1B.with_layers(3)
+    d = binding.make_desc(shape)
+    total = lib.specdec_packed_bytes(ctypes.byref(d), 3)
+    head_off, _ = binding.packed_range(shape, 0, 1)
+    prev_end = head_off
+    for layer in range(3):
+        off, nb = binding.packed_range(shape, layer, 1)
+        assert off == prev_end and nb > 0
+        prev_end = off + nb
+    assert prev_end == total
+    off, nb = binding.packed_range(shape, 0, 2)
+    assert off == head_off and off + nb == lib.specdec_packed_bytes(ctypes.byref(d), 2)
+    # the LM head region is its [V, d] bf16 image, 256-byte aligned
+    assert head_off == -(-shape.vocab * shape.d_model * 2 // 256) * 256
+    off_t, nb_t = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.specdec_packed_range(ctypes.byref(d), 2, 2, ctypes.byref(off_t), ctypes.byref(nb_t)) == -1
+    assert lib.specdec_packed_range(ctypes.byref(d), -1, 1, ctypes.byref(off_t), ctypes.byref(nb_t)) == -1
+    assert lib.specdec_packed_range(ctypes.byref(d), 0, 1, None, ctypes.byref(nb_t)) == -1
+    d32 = binding.make_desc(synth.TINY)
+    assert lib.specdec_packed_range(ctypes.byref(d32), 0, 1, ctypes.byref(off_t), ctypes.byref(nb_t)) == -6
+
+
+def test_reload_calls_reject_bad_arguments(lib):
+    fake = ctypes.c_void_p(256)
+    assert lib.specdec_event_create(None) == -1
+    assert lib.specdec_event_destroy(None) == -1
+    assert lib.specdec_load_async(None, fake, 16, None, fake) == -1
+    assert lib.specdec_load_async(fake, fake, 0, None, fake) == -1
+    assert lib.specdec_load_async(fake, fake, 16, None, None) == -1
+    assert lib.specdec_stream_wait_event(None, None) == -1
+    assert lib.specdec_event_query(None, None) == -1
