@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--reload", action="store_true",
+                    help="instead of the verify line, measure draft reloads (2/4/8-layer drafts) from pinned host "
+                         "memory into a resident slot on a side stream, alone and under concurrent verify steps")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one 1 GiB device-to-device copy (reference for the HBM byte counters)")
     return ap.parse_args()
@@ -176,6 +179,88 @@ def cpu_baseline(shape, ctx, gamma):
                        f"time x {shape.n_layers} layers -> {t_full:.1f} s per verify step")}
 
 
+# ---------------------------------------------------------------- draft reload
+def reload_bench(dw, graphs, verify_part, args):
+    """H2D reloads of 2/4/8-layer draft layers into one resident slot (the LM
+    head stays in the slot), each timed with events on the copy stream; then
+    the verify step replayed on the main stream while an 8-layer reload runs
+    on the side stream, against the verify step alone."""
+    import numpy as np
+    import torch
+
+    from paper_2608_10362_amd import binding
+    slot = binding.DraftSlot(dw, max_layers=8)
+    copy = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    log(f"draft slot {slot.nbytes / 1e9:.2f} GB, pinned host image {slot.host.numel() / 1e9:.2f} GB")
+
+    def timed_load(k):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(copy)
+        nb = slot.load_async(k, copy)
+        e1.record(copy)
+        return nb, e0, e1
+
+    loads = {}
+    for k in (2, 4, 8):
+        ms = []
+        for _ in range(3):
+            nb, e0, e1 = timed_load(k)
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        med = float(np.median(ms))
+        loads[str(k)] = {"bytes": nb, "ms": round(med, 3), "GBps": round(nb / (med * 1e-3) / 1e9, 2)}
+    nb, e0, e1 = timed_load(8)
+    issued_not_done = not slot.event.query()  # the load is asynchronous: the host was not blocked
+    e1.synchronize()
+
+    def replay_verify():
+        if graphs:
+            graphs[1].replay()
+        else:
+            verify_part(0)
+
+    for _ in range(5):
+        replay_verify()
+    torch.cuda.synchronize()
+    n = 10
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(n):
+        replay_verify()
+    a1.record()
+    a1.synchronize()
+    alone = a0.elapsed_time(a1) / n
+    # as many verify steps as fit inside one 8-layer reload
+    n_ov = max(1, int(loads["8"]["ms"] / alone) - 2)
+    torch.cuda.synchronize()
+    nb, e0, e1 = timed_load(8)
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record()
+    for _ in range(n_ov):
+        replay_verify()
+    b1.record()
+    torch.cuda.synchronize()
+    during = b0.elapsed_time(b1) / n_ov
+    copy_ms = e0.elapsed_time(e1)
+    return {
+        "metric": "draft reload into a resident slot (H2D, side stream)",
+        "unit": "ms",
+        "higher_is_better": False,
+        "data": "synthetic",
+        "dtype": "bf16",
+        "config": {"workload": "7B-shaped target; 2/4/8-layer draft layers copied from pinned host memory into one "
+                               "HBM slot that keeps the shared LM head", "slot_bytes": slot.nbytes},
+        "reload": loads,
+        "load_returned_before_completion": bool(issued_not_done),
+        "verify_ms_alone": round(alone, 4),
+        "verify_ms_during_8_layer_reload": round(during, 4),
+        "verify_steps_overlapped": n_ov,
+        "reload_ms_under_verify": round(copy_ms, 3),
+        "hip_graph": bool(graphs),
+    }
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -278,6 +363,10 @@ def main():
             verify_part(i)
             if ev: ev[1].record()
             commit_part()
+
+    if args.reload:
+        print(json.dumps(reload_bench(dw, graphs, verify_part, args)), flush=True)
+        return
 
     for i in range(args.warmup):
         run_step(i)
