@@ -147,13 +147,18 @@ __global__ __launch_bounds__(256) void attn_partial_kernel(AttnArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- MFMA split-KV partials (bf16 cache)
-// One wave per (16-query tile, 64-key split, kv head, sequence).  S = Q K^T
-// and O = P V run on v_mfma_f32_16x16x32_bf16 with the float32 operands (Q,
-// P) split into hi + lo bf16 parts; K fragments are 16-byte loads of K rows,
-// V fragments 16-byte loads of the transposed V rows.  Lane l holds rows
-// 4(l/16)+r of S and O, so the per-row max / sum live in the same lanes.
-constexpr int kSplitKeys = 64;
+// ---------------------------------------------------------------- MFMA attention partials (bf16 cache)
+// The keys [0, 32 n_sub) of each (kv head, sequence) are cut into n_part parts
+// of S sub-chunks of 32 keys; the last part also takes the remainder (fewer
+// than 2S sub-chunks).  One block per (part, 16-query tile, kv head,
+// sequence) and one wave per sub-chunk.  S is chosen on the host so that the
+// blocks about fill the CUs once: every CU then streams about the same number
+// of K/V bytes.  Per wave, S = Q K^T and O = P V run on
+// v_mfma_f32_16x16x32_bf16 with the float32 operands (Q, P) split into hi + lo
+// bf16 parts; lane l holds rows 4(l/16)+r of S and O, so the per-row max and
+// sum live in the same lanes.  The block merges its waves' (max, sum, O) in
+// LDS (fixed wave order) and writes one partial per part.
+constexpr int kSubKeys = 32;
 
 __device__ __forceinline__ void split_hilo(const float* v, bf16x8& hi, bf16x8& lo) {
 #pragma unroll
@@ -175,171 +180,203 @@ __device__ __forceinline__ float group16_sum(float v) {
   return v;
 }
 
+// Dynamic LDS: per wave a P tile [16][36] (the transposed read of P V), then,
+// reused once every wave is past P V, the merge buffers [NW][RS][HD] of O and
+// [NW][RS][2] of (max, sum), RS = query rows of the tile.
+__host__ __device__ inline size_t attn_block_lds(int NW, int RS, int HD) {
+  const size_t p = (size_t)NW * 16 * (kSubKeys + 4);
+  const size_t m = (size_t)NW * RS * (HD + 2);
+  return (p > m ? p : m) * sizeof(float);
+}
+
+constexpr int kMaxPartWaves = 12;  // 3 waves per SIMD: up to 170 VGPRs per lane
+
 template <int HD>
-__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs a, int S, int n_sub, int NW) {
   constexpr int KST = HD / 32;  // k-steps of Q K^T
   constexpr int DT = HD / 16;   // 16-wide dimension tiles of P V
-  constexpr int NT = kSplitKeys / 16;
-  __shared__ float pbuf[16][kSplitKeys + 4];
-  const int lane = threadIdx.x, g = blockIdx.y, b = blockIdx.z;
+  constexpr int NT = kSubKeys / 16;
+  extern __shared__ float smem[];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = blockIdx.y, b = blockIdx.z;
   const int H = a.n_heads, G = a.n_kv_heads, group = H / G;
   const int rps = a.rps, r0 = b * rps, nq = rps * group;
-  const int split = blockIdx.x % a.n_split, mt = blockIdx.x / a.n_split;
-  if (mt * 16 >= nq) return;
+  const int n_part = a.n_split;
+  const int part = blockIdx.x % n_part, mt = blockIdx.x / n_part;
+  const int RS = min(16, nq - mt * 16);  // query rows of this tile (> 0 by the grid)
   const int c16 = lane & 15, grp = lane >> 4;
-  const int k0 = split * kSplitKeys;
-  if (k0 >= a.kv.capacity) return;
+  const int sub_here = part == n_part - 1 ? n_sub - part * S : S;
+  const int k0 = (part * S + wave) * kSubKeys;
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
   const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;
-
-  // Every load is issued before anything waits, smallest first (loads complete
-  // in order, so waiting for an early one never waits for a later one): the
-  // row descriptors, the K fragments, Q, then the V fragments.  Row
-  // descriptors and Q go through range-checked buffer loads (zeros past the
-  // range, no branch around a load).
-  // Row descriptors: lane i < rps reads row r0 + i.
-  const __amdgpu_buffer_rsrc_t rr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0, a.M * (int)sizeof(RowDesc), 0x00020000);
-  // (only the two fields used: a wider load leaves dead destination registers
-  // the allocator reuses, which forces a wait for the load)
-  const uint32_t roff = ((uint32_t)(r0 + lane) * (uint32_t)sizeof(RowDesc)) | ((uint32_t)(lane >= rps) << 31);
-  const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
-  const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
-  // K fragments of the split: 16 contiguous 1 KB fragments (k0 + 64 <= capacity: in bounds).
-  u32x4 kf[NT][KST];
-  const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
-  // Q fragments (A operand): query qa = mt*16 + l%16 (zeros past nq).
-  f32x4 qv4[KST][2];
-  {
-    const int qa = mt * 16 + c16;
-    const int row = r0 + qa / group, head = g * group + qa % group;
-    const __amdgpu_buffer_rsrc_t qrs =
-        __builtin_amdgcn_make_buffer_rsrc(a.qr, (short)0, a.M * H * HD * 4, 0x00020000);
-    const uint32_t qoff = ((((uint32_t)row * H + head) * HD + 8 * grp) * 4u) | ((uint32_t)(qa >= nq) << 31);
-#pragma unroll
-    for (int c = 0; c < KST; ++c) {
-      qv4[c][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c, 0, 0));
-      qv4[c][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c + 16u, 0, 0));
-    }
-  }
-  // V fragments: 2 x DT contiguous 1 KB fragments.
-  u32x4 vf[2][DT];
-  const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[s][dt] = *(const u32x4*)(vfrag + (size_t)(s * DT + dt) * 512);
-
-  // (compiler barrier: keeps the early exit below from being hoisted above the
-  // loads, which would wait for the row descriptors before issuing them)
-  asm volatile("" ::: "memory");
-  // nk = max(pos) + 1 over the sequence's valid rows.
-  const int mypos = (lane < rps && rd_valid) ? rd_pos : -1;
-  int nk = mypos + 1;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
-  if (k0 >= nk) return;
-  // positions of the 4 query rows this lane holds in the C layout (-1: none)
-  int qpos[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qc = mt * 16 + 4 * grp + r;
-    const int p = __shfl(mypos, min(qc, nq - 1) / group, kWave);
-    qpos[r] = qc < nq ? p : -1;
-  }
-  // keys past the context: zero their V entries (never multiply stale memory)
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int nvalid = nk - (k0 + 32 * s + 8 * grp);
-    if (nvalid < 8) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (2 * j >= nvalid) vf[s][dt][j] = 0u;
-          else if (2 * j + 1 >= nvalid) vf[s][dt][j] &= 0xffffu;
-        }
-    }
-  }
-  const float scale = 1.0f / sqrtf((float)HD);
-  bf16x8 qhi[KST], qlo[KST];
-#pragma unroll
-  for (int c = 0; c < KST; ++c) {
-    float v[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[j] = qv4[c][0][j] * scale;
-      v[4 + j] = qv4[c][1][j] * scale;
-    }
-    split_hilo(v, qhi[c], qlo[c]);
-  }
-
-  floatx4 sf[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < KST; ++c) {
-      const bf16x8 kk = __builtin_bit_cast(bf16x8, kf[t][c]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qhi[c], kk, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qlo[c], kk, acc, 0, 0, 0);
-    }
-    const int key = k0 + 16 * t + c16;
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (key > qpos[r]) acc[r] = -INFINITY;
-    sf[t] = acc;
-  }
-  float mx[4], sm[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) m = fmaxf(m, sf[t][r]);
-    mx[r] = group16_max(m);
-    float s = 0.f;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const float p = mx[r] == -INFINITY || sf[t][r] == -INFINITY ? 0.f : expf(sf[t][r] - mx[r]);
-      pbuf[4 * grp + r][16 * t + c16] = p;
-      s += p;
-    }
-    sm[r] = group16_sum(s);
-  }
-  __syncthreads();  // one wave per block: P written by all lanes before the transposed reads
 
   floatx4 of[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) of[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, sm[4] = {0.f, 0.f, 0.f, 0.f};
+  int qpos[4] = {-1, -1, -1, -1};
+  float* pbuf = smem + (size_t)wave * 16 * (kSubKeys + 4);
+
+  if (wave < sub_here) {  // (wave-uniform) a wave past the part's sub-chunks only joins the merge
+    // Every load is issued before anything waits, smallest first (loads complete
+    // in order, so waiting for an early one never waits for a later one): the
+    // row descriptors, the K fragments, Q, then the V fragments.  Row
+    // descriptors and Q go through range-checked buffer loads.
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0,
+                                                                         a.M * (int)sizeof(RowDesc), 0x00020000);
+    // (only the two fields used: a wider load leaves dead destination registers
+    // the allocator reuses, which forces a wait for the load)
+    const uint32_t roff = ((uint32_t)(r0 + lane) * (uint32_t)sizeof(RowDesc)) | ((uint32_t)(lane >= rps) << 31);
+    const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
+    const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
+    // K fragments of the sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity).
+    u32x4 kf[NT][KST];
+    const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    float pv[8];
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) pv[j] = pbuf[c16][32 * s + 8 * grp + j];
-    bf16x8 phi, plo;
-    split_hilo(pv, phi, plo);
+      for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
+    // Q fragments (A operand): query qa = mt*16 + l%16 (zeros past nq).
+    f32x4 qv4[KST][2];
+    {
+      const int qa = mt * 16 + c16;
+      const int row = r0 + qa / group, head = g * group + qa % group;
+      const __amdgpu_buffer_rsrc_t qrs =
+          __builtin_amdgcn_make_buffer_rsrc(a.qr, (short)0, a.M * H * HD * 4, 0x00020000);
+      const uint32_t qoff = ((((uint32_t)row * H + head) * HD + 8 * grp) * 4u) | ((uint32_t)(qa >= nq) << 31);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16x8 vv = __builtin_bit_cast(bf16x8, vf[s][dt]);
-      of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vv, of[dt], 0, 0, 0);
-      of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vv, of[dt], 0, 0, 0);
+      for (int c = 0; c < KST; ++c) {
+        qv4[c][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c, 0, 0));
+        qv4[c][1] =
+            __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c + 16u, 0, 0));
+      }
+    }
+    // V fragments: DT contiguous 1 KB fragments (32 positions x 16 dims each).
+    u32x4 vf[DT];
+    const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = *(const u32x4*)(vfrag + (size_t)dt * 512);
+    // (compiler barrier: keeps what follows from being hoisted above the loads)
+    asm volatile("" ::: "memory");
+
+    // nk = max(pos) + 1 over the sequence's valid rows.
+    const int mypos = (lane < rps && rd_valid) ? rd_pos : -1;
+    int nk = mypos + 1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
+    // positions of the 4 query rows this lane holds in the C layout (-1: none)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qc = mt * 16 + 4 * grp + r;
+      const int p = __shfl(mypos, min(qc, nq - 1) / group, kWave);
+      qpos[r] = qc < nq ? p : -1;
+    }
+    if (k0 < nk) {
+      // keys past the context: zero their V entries (never multiply stale memory)
+      const int nvalid = nk - (k0 + 8 * grp);
+      if (nvalid < 8) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (2 * j >= nvalid) vf[dt][j] = 0u;
+            else if (2 * j + 1 >= nvalid) vf[dt][j] &= 0xffffu;
+          }
+      }
+      const float scale = 1.0f / sqrtf((float)HD);
+      bf16x8 qhi[KST], qlo[KST];
+#pragma unroll
+      for (int c = 0; c < KST; ++c) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[j] = qv4[c][0][j] * scale;
+          v[4 + j] = qv4[c][1][j] * scale;
+        }
+        split_hilo(v, qhi[c], qlo[c]);
+      }
+      floatx4 sf[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < KST; ++c) {
+          const bf16x8 kk = __builtin_bit_cast(bf16x8, kf[t][c]);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qhi[c], kk, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qlo[c], kk, acc, 0, 0, 0);
+        }
+        const int key = k0 + 16 * t + c16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (key > qpos[r]) acc[r] = -INFINITY;
+        sf[t] = acc;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) m = fmaxf(m, sf[t][r]);
+        mx[r] = group16_max(m);
+        float sum = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float p = mx[r] == -INFINITY || sf[t][r] == -INFINITY ? 0.f : expf(sf[t][r] - mx[r]);
+          pbuf[(4 * grp + r) * (kSubKeys + 4) + 16 * t + c16] = p;
+          sum += p;
+        }
+        sm[r] = group16_sum(sum);
+      }
+      __builtin_amdgcn_wave_barrier();  // P written by all lanes of the wave before the transposed reads
+      float pv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = pbuf[c16 * (kSubKeys + 4) + 8 * grp + j];
+      bf16x8 phi, plo;
+      split_hilo(pv, phi, plo);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const bf16x8 vv = __builtin_bit_cast(bf16x8, vf[dt]);
+        of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vv, of[dt], 0, 0, 0);
+        of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vv, of[dt], 0, 0, 0);
+      }
     }
   }
+
+  // Merge the waves' partials of this part (LDS reused: every wave is past P V).
+  __syncthreads();
+  float* so = smem;                            // [NW][RS][HD]
+  float* sml = smem + (size_t)NW * RS * HD;    // [NW][RS][2]
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int qc = mt * 16 + 4 * grp + r;
-    if (qpos[r] < 0 || mx[r] == -INFINITY) continue;
-    const int row = r0 + qc / group, head = g * group + qc % group;
-    const size_t slot = ((size_t)row * H + head) * a.n_split + split;
+    const int row = 4 * grp + r;
+    if (row >= RS) continue;
+    const bool live = qpos[r] >= 0 && mx[r] != -INFINITY;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) a.o_part[slot * HD + dt * 16 + c16] = of[dt][r];
+    for (int dt = 0; dt < DT; ++dt) so[((size_t)wave * RS + row) * HD + dt * 16 + c16] = live ? of[dt][r] : 0.f;
     if (c16 == 0) {
-      a.ml_part[2 * slot] = mx[r];
-      a.ml_part[2 * slot + 1] = sm[r];
+      sml[((size_t)wave * RS + row) * 2] = live ? mx[r] : -INFINITY;
+      sml[((size_t)wave * RS + row) * 2 + 1] = live ? sm[r] : 0.f;
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < RS * HD; i += NW * kWave) {
+    const int row = i / HD, d = i % HD, qc = mt * 16 + row;
+    float M = -INFINITY;
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sml[((size_t)w * RS + row) * 2]);
+    if (M == -INFINITY) continue;  // no key of this part is visible to the row
+    float L = 0.f, O = 0.f;
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sml[((size_t)w * RS + row) * 2];
+      if (mw == -INFINITY) continue;
+      const float e = expf(mw - M);
+      L += e * sml[((size_t)w * RS + row) * 2 + 1];
+      O += e * so[((size_t)w * RS + row) * HD + d];
+    }
+    const int qrow = r0 + qc / group, head = g * group + qc % group;
+    const size_t slot = ((size_t)qrow * H + head) * n_part + part;
+    a.o_part[slot * HD + d] = O;
+    if (d == 0) {
+      a.ml_part[2 * slot] = M;
+      a.ml_part[2 * slot + 1] = L;
     }
   }
 }
@@ -359,11 +396,9 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
     for (int dd = threadIdx.x; dd < hd; dd += blockDim.x) o[dd] = 0.f;
     return;
   }
-  int nch = (rd.pos + 1 + a.chunk - 1) / a.chunk;
-  if (nch > a.n_split) {  // the host's bound on the context was wrong: report, stay in bounds
-    if (threadIdx.x == 0) set_status(a.status, kStatusKvCapacity);
-    nch = a.n_split;
-  }
+  // splits holding keys <= pos (with parts, the last one also holds the remainder)
+  const int nch = min(rd.pos / a.chunk + 1, a.n_split);
+  if (rd.pos + 1 > a.max_ctx && threadIdx.x == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
   const size_t base = ((size_t)r * H + head) * a.n_split;
   float mx = -INFINITY;
   for (int c = threadIdx.x; c < nch; c += blockDim.x) mx = fmaxf(mx, a.ml_part[2 * (base + c)]);
@@ -429,8 +464,12 @@ __global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
         ov[cc][d] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(opr, off, 0, 0));
       }
   };
-  float ovA[CH][DPL], ovB[CH][DPL];
-  load_chunk(0, ovA);
+  // Partial outputs of NG chunks (64 splits) are requested at once: one memory
+  // round trip for contexts up to 64 splits, one more per further 64.
+  constexpr int NG = 4;
+  float ov[NG][CH][DPL];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) load_chunk(g * CH, ov[g]);
   asm volatile("" ::: "memory");  // (keep the loads above the exits below)
 
   const RowDesc rd = a.rows[r];
@@ -441,11 +480,9 @@ __global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
       if (lane + 64 * d < HD) o[lane + 64 * d] = 0.f;
     return;
   }
-  int nch = (rd.pos + 1 + kSplitKeys - 1) / kSplitKeys;
-  if (nch > ns) {  // the host's bound on the context was wrong: report, stay in bounds
-    if (lane == 0) set_status(a.status, kStatusKvCapacity);
-    nch = ns;
-  }
+  // parts holding keys <= pos (the last part also holds the remainder)
+  const int nch = min(rd.pos / a.chunk + 1, ns);
+  if (rd.pos + 1 > a.max_ctx && lane == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
   float mx = -INFINITY;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
@@ -463,23 +500,23 @@ __global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int d = 0; d < DPL; ++d) acc[i][d] = 0.f;
-  auto accumulate = [&](int c0, const float (&ov)[CH][DPL]) {
+  for (int g0 = 0; g0 < nch; g0 += NG * CH) {
+    if (g0 > 0) {
 #pragma unroll
-    for (int cc = 0; cc < CH; ++cc) {
-      const int c = c0 + cc;
-      if (c >= nch) break;
-      const float wj = c < 64 ? wv[0] : (c < 128 ? wv[1] : (c < 192 ? wv[2] : wv[3]));
-      const float w = __shfl(wj, c & 63, kWave);
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) acc[cc & 3][d] += w * ov[cc][d];
+      for (int g = 0; g < NG; ++g) load_chunk(g0 + g * CH, ov[g]);
     }
-  };
-  for (int c0 = 0; c0 < nch; c0 += 2 * CH) {
-    if (c0 + CH < nch) load_chunk(c0 + CH, ovB);
-    accumulate(c0, ovA);
-    if (c0 + CH >= nch) break;
-    if (c0 + 2 * CH < nch) load_chunk(c0 + 2 * CH, ovA);
-    accumulate(c0 + CH, ovB);
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+#pragma unroll
+      for (int cc = 0; cc < CH; ++cc) {
+        const int c = g0 + g * CH + cc;
+        if (c < nch) {
+          const float wj = c < 64 ? wv[0] : (c < 128 ? wv[1] : (c < 192 ? wv[2] : wv[3]));
+          const float w = __shfl(wj, c & 63, kWave);
+#pragma unroll
+          for (int d = 0; d < DPL; ++d) acc[cc & 3][d] += w * ov[g][cc][d];
+        }
+      }
   }
   const float inv = 1.0f / L;
 #pragma unroll
@@ -513,7 +550,7 @@ size_t attn_smem_bytes(int chunk, int hd) {
 }  // namespace
 
 int attention_chunk(int dtype, int head_dim) {
-  if (dtype == SPECDEC_BF16) return kSplitKeys;
+  if (dtype == SPECDEC_BF16) return kSubKeys;  // (parts are whole numbers of sub-chunks: at most one split each)
   return head_dim >= 128 ? 32 : (head_dim >= 64 ? 64 : 128);
 }
 
@@ -528,14 +565,30 @@ hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int B = a.M / a.rps;
+  AttnArgs ab = a;  // the bf16 path chooses its own parts
   if (a.kv.dtype == SPECDEC_BF16) {
-    if (a.chunk != kSplitKeys) return hipErrorInvalidValue;
-    const int nq = a.rps * (a.n_heads / a.n_kv_heads);
-    dim3 grid(a.n_split * ((nq + 15) / 16), a.n_kv_heads, B);
+    const int nq = a.rps * (a.n_heads / a.n_kv_heads), n_mt = (nq + 15) / 16, RS = nq < 16 ? nq : 16;
+    const int n_sub = (a.max_ctx + kSubKeys - 1) / kSubKeys;
+    if (n_sub * kSubKeys > a.kv.capacity || n_sub > a.n_split * (a.chunk / kSubKeys)) return hipErrorInvalidValue;
+    // sub-chunks per part: the blocks should about fill the CUs once
+    const long units = (long)a.n_kv_heads * B * n_mt;
+    int S = (int)((n_sub * units + device_compute_units() / 2) / device_compute_units());
+    S = S < 1 ? 1 : (S > kMaxPartWaves ? kMaxPartWaves : S);  // (reduced below while the last part is too big)
+    int n_part = 0, NW = 0;
+    for (;; --S) {
+      n_part = n_sub / S > 0 ? n_sub / S : 1;
+      NW = n_sub - (n_part - 1) * S;
+      if (S == 1 || (NW <= kMaxPartWaves && attn_block_lds(NW, RS, a.head_dim) <= 65536)) break;
+    }
+    if (NW > kMaxPartWaves || attn_block_lds(NW, RS, a.head_dim) > 65536) return hipErrorInvalidValue;
+    ab.n_split = n_part;
+    ab.chunk = S * kSubKeys;
+    dim3 grid(n_part * n_mt, a.n_kv_heads, B);
+    const size_t lds = attn_block_lds(NW, RS, a.head_dim);
     switch (a.head_dim) {
-      case 32: hipLaunchKernelGGL((attn_mfma_kernel<32>), grid, dim3(64), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((attn_mfma_kernel<64>), grid, dim3(64), 0, s, a); break;
-      case 128: hipLaunchKernelGGL((attn_mfma_kernel<128>), grid, dim3(64), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((attn_block_kernel<32>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
+      case 64: hipLaunchKernelGGL((attn_block_kernel<64>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
+      case 128: hipLaunchKernelGGL((attn_block_kernel<128>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
       default: return hipErrorInvalidValue;
     }
   } else {
@@ -545,14 +598,14 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.kv.dtype == SPECDEC_BF16 && a.n_split <= kCombineMaxSplits) {
-    switch (a.head_dim) {
-      case 32: hipLaunchKernelGGL((attn_combine_wave_kernel<32>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((attn_combine_wave_kernel<64>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
-      default: hipLaunchKernelGGL((attn_combine_wave_kernel<128>), dim3(a.n_heads, a.M), dim3(64), 0, s, a); break;
+  if (ab.kv.dtype == SPECDEC_BF16 && ab.n_split <= kCombineMaxSplits) {
+    switch (ab.head_dim) {
+      case 32: hipLaunchKernelGGL((attn_combine_wave_kernel<32>), dim3(ab.n_heads, ab.M), dim3(64), 0, s, ab); break;
+      case 64: hipLaunchKernelGGL((attn_combine_wave_kernel<64>), dim3(ab.n_heads, ab.M), dim3(64), 0, s, ab); break;
+      default: hipLaunchKernelGGL((attn_combine_wave_kernel<128>), dim3(ab.n_heads, ab.M), dim3(64), 0, s, ab); break;
     }
   } else {
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.n_heads, a.M), dim3(128), sizeof(float) * a.n_split, s, a);
+    hipLaunchKernelGGL(attn_combine_kernel, dim3(ab.n_heads, ab.M), dim3(128), sizeof(float) * ab.n_split, s, ab);
   }
   return hipGetLastError();
 }

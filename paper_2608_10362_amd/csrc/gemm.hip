@@ -603,6 +603,8 @@ __global__ void pack_kernel(const uint16_t* __restrict__ src, uint16_t* __restri
 
 }  // namespace
 
+int device_compute_units() { return compute_units(); }
+
 size_t packed_elems(int N, int K) { return (size_t)(N / 16) * ((K + 31) / 32) * 512; }
 
 hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s) {

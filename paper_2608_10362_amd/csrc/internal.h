@@ -135,6 +135,7 @@ struct AttnArgs {
   int32_t* status;
 };
 int attention_chunk(int dtype, int head_dim);  // keys per split of the attention kernel
+int device_compute_units();                    // CUs of the current device (cached)
 hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
