@@ -23,6 +23,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -43,6 +45,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, choices=(1, 2, 3, 5),
+                    help="3 (default): the 7B gamma=4 bs1 headline line; 1: tiny float32; 2: 1.1B-shaped bf16; "
+                         "5: 7B-shaped, 16 sequences with contexts U[1024, 8192], gamma 6, T 0.8")
     ap.add_argument("--reload", action="store_true",
                     help="instead of the verify line, measure draft reloads (2/4/8-layer drafts) from pinned host "
                          "memory into a resident slot on a side stream, alone and under concurrent verify steps")
@@ -261,6 +266,181 @@ def reload_bench(dw, graphs, verify_part, args):
     }
 
 
+# ---------------------------------------------------------------- shared step timing
+def capture_graphs(sd, draft_part, verify_part, commit_part, no_graph):
+    """Capture draft / verify+accept / commit as three HIP graphs; every replay is
+    checked bit for bit against an eager step (three replays, eager work in
+    between).  Returns None (eager launches) if capture is off or fails."""
+    import torch
+    draft_part(0); verify_part(0); commit_part()
+    torch.cuda.synchronize()
+    ref = (sd.d.clone(), sd.logits.clone(), sd.n_acc.clone(), sd.next.clone())
+    if no_graph:
+        return None
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            draft_part(0); verify_part(0); commit_part()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        gd, gv, gc = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gd):
+            draft_part(0)
+        with torch.cuda.graph(gv):
+            verify_part(0)
+        with torch.cuda.graph(gc):
+            commit_part()
+        for r in range(3):
+            gd.replay(); gv.replay(); gc.replay()
+            torch.cuda.synchronize()
+            same = (torch.equal(sd.d, ref[0]) and torch.equal(sd.logits, ref[1]) and
+                    torch.equal(sd.n_acc, ref[2]) and torch.equal(sd.next, ref[3]))
+            if not same:
+                raise RuntimeError(f"graph replay {r} differs from the eager step")
+            draft_part(0); verify_part(0); commit_part()
+            torch.cuda.synchronize()
+        return (gd, gv, gc)
+    except Exception as e:
+        log(f"graph capture disabled: {e}")
+        return None
+
+
+def time_steps(graphs, draft_part, verify_part, commit_part, steps, warmup):
+    """Time `steps` steps after `warmup`: the verify (+ accept) time from events
+    around the verify graph, the step time from events around the loop."""
+    import torch
+
+    def run_step(i, ev=None):
+        if graphs:
+            graphs[0].replay()
+            if ev: ev[0].record()
+            graphs[1].replay()
+            if ev: ev[1].record()
+            graphs[2].replay()
+        else:
+            draft_part(i)
+            if ev: ev[0].record()
+            verify_part(i)
+            if ev: ev[1].record()
+            commit_part()
+
+    for i in range(warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        run_step(warmup + i, evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    verify = [a.elapsed_time(b) for a, b in evs]
+    return {"verify_ms": sum(verify) / steps, "verify_ms_p10": float(np.percentile(verify, 10)),
+            "verify_ms_p50": float(np.percentile(verify, 50)), "verify_ms_p90": float(np.percentile(verify, 90)),
+            "step_ms": start.elapsed_time(end) / steps}
+
+
+def verify_bytes_ragged(shape, lengths, gamma):
+    """verify_step_bytes for per-sequence contexts."""
+    L, d, f, V = shape.n_layers, shape.d_model, shape.ffn_dim, shape.vocab
+    e = 2 if shape.dtype == "bf16" else 4
+    B = len(lengths)
+    per_layer = ((shape.q_dim + 2 * shape.kv_dim) * d + d * shape.q_dim + 3 * f * d + 2 * d) * e
+    weights = L * per_layer + (V * d + d) * e + B * (gamma + 1) * d * e
+    kv_row = shape.n_kv_heads * shape.head_dim * 2 * e * L
+    return weights + int(sum(lengths)) * kv_row + B * (gamma + 1) * kv_row
+
+
+CONFIGS = {
+    1: dict(desc="tiny float32 (L=2, d=128, 4x32 MHA, F=512, V=512), 1-layer draft, 64-token prompt",
+            shape="TINY", batch=1, gamma=4, prompt=64, temperature=1.0, draft_layers=1, generate=32),
+    2: dict(desc="1.1B-shaped bf16 (L=22, d=2048, 32q/4kv x 64, F=5632, V=32000), 4-layer draft, "
+                 "512-token prompt", shape="LLAMA_1B", batch=1, gamma=4, prompt=512, temperature=1.0,
+            draft_layers=4, generate=256),
+    5: dict(desc="7B-shaped bf16, 16 sequences with resident contexts U[1024, 8192] (seed 4), 4-layer draft",
+            shape="LLAMA_7B", batch=16, gamma=6, lengths=(1024, 8192), temperature=0.8, draft_layers=4),
+}
+
+
+def run_config(args):
+    """Configurations other than the headline one, measured the same way: every
+    step from the same state (restored on the device), graph replays, HIP events."""
+    import torch
+
+    from paper_2608_10362_amd import binding, synth
+    cfg = CONFIGS[args.config]
+    shape = getattr(synth, cfg["shape"])
+    B, g, T, k = cfg["batch"], cfg["gamma"], cfg["temperature"], cfg["draft_layers"]
+    t0 = time.time()
+    if shape.dtype == "f32":
+        dw = binding.DeviceWeights(shape, synth.make_weights(shape))
+    else:
+        dw = device_weights(shape)
+    if "prompt" in cfg:
+        n0 = cfg["prompt"]
+        lengths = np.full(B, n0 - 1, np.int64)
+        need = n0 + cfg["generate"] + 2 * g + 2
+    else:
+        lengths = synth.make_ragged_lengths(B, *cfg["lengths"]).astype(np.int64)
+        need = int(lengths.max()) + g + 2
+    cap = (need + 63) // 64 * 64
+    rows = max(B * (g + 1), 2 * B, 64)
+    target = binding.Model(dw, shape.n_layers, max_rows=rows, max_ctx=cap)
+    draft = binding.Model(dw, k, max_rows=rows, max_ctx=cap)
+    kv_t, kv_d = binding.KVCache(target, B, cap), binding.KVCache(draft, B, cap)
+    if "prompt" in cfg:
+        tok = torch.from_numpy(synth.make_prompt(cfg["prompt"], shape.vocab, batch=B).astype(np.int32)).cuda()
+        binding.specdec_prefill(target, kv_t, tok)
+        binding.specdec_prefill(draft, kv_d, tok)
+    else:
+        install_context(kv_t, shape.n_layers, shape, [int(x) for x in lengths])
+        install_context(kv_d, k, shape, [int(x) for x in lengths])
+        pend = synth.make_prompt(1, shape.vocab, batch=B)[:, 0]
+        st = (lengths.astype(np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
+        kv_t.set_state(*st)
+        kv_d.set_state(*st)
+    torch.cuda.synchronize()
+    saved = (kv_t.state.clone(), kv_d.state.clone(), kv_t.kv.len_upper, kv_d.kv.len_upper)
+    sd = binding.SpecDecoder(target, draft, kv_t, kv_d, g, T, seed=synth.SEED_SAMPLING)
+    log(f"config {args.config} set-up {time.time() - t0:.1f} s")
+
+    def restore():
+        kv_t.state.copy_(saved[0]); kv_d.state.copy_(saved[1])
+        kv_t.kv.len_upper, kv_d.kv.len_upper = saved[2], saved[3]
+
+    def draft_part(i):
+        restore()
+        sd.draft_phase(i)
+
+    verify_part = lambda i: sd.verify_phase(i)  # noqa: E731
+    graphs = capture_graphs(sd, draft_part, verify_part, sd.commit_phase, args.no_graph)
+    tm = time_steps(graphs, draft_part, verify_part, sd.commit_phase, args.steps, args.warmup)
+    status = min(int(sd.status.item()), kv_t.read_state()["status"], kv_d.read_state()["status"])
+    acc = []
+    for i in range(8):
+        draft_part(1000 + i); sd.verify_phase(1000 + i); sd.commit_phase()
+        acc.append(sd.n_acc.clone())
+    mean_A = float(torch.stack(acc).float().mean().item())
+    vbytes = verify_bytes_ragged(shape, lengths, g)
+    gbps = vbytes / (tm["verify_ms"] * 1e-3) / 1e9
+    result = {
+        "metric": f"verify-step tokens/s (config {args.config})", "value": round(B * (g + 1) / (tm["verify_ms"] * 1e-3), 2),
+        "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(tm["step_ms"], 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if shape.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": cfg["desc"], "gamma": g, "batch": B, "temperature": T, "draft_layers": k,
+                   "context_lengths": [int(x) for x in lengths][:16], "hip_graph": bool(graphs)},
+        "verify_ms": round(tm["verify_ms"], 4), "verify_ms_p10_p50_p90": [round(tm["verify_ms_p10"], 4),
+                                                                         round(tm["verify_ms_p50"], 4),
+                                                                         round(tm["verify_ms_p90"], 4)],
+        "verify_bytes": vbytes, "verify_hbm_GBps": round(gbps, 1), "verify_hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+        "generated_tokens_per_s": round(B * (mean_A + 1) / (tm["step_ms"] * 1e-3), 2),
+        "mean_accepted": round(mean_A, 3), "device_status": status,
+    }
+    print(json.dumps(result), flush=True)
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -274,6 +454,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     binding.lib()
+    if args.config != 3:
+        run_config(args)
+        return
     shape = synth.LLAMA_7B
     B, g, ctx, T = args.batch, args.gamma, args.ctx, args.temperature
     cap = ((ctx + g + 2 + 63) // 64) * 64
@@ -286,7 +469,6 @@ def main():
     install_context(kv_t, shape.n_layers, shape, [ctx] * B)
     install_context(kv_d, args.draft_layers, shape, [ctx] * B)
     pend = synth.make_prompt(1, shape.vocab, batch=B)[:, 0]
-    import numpy as np
     st = (np.full(B, ctx, np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
     kv_t.set_state(*st)
     kv_d.set_state(*st)
@@ -311,76 +493,13 @@ def main():
     def commit_part():
         sd.commit_phase()
 
-    # eager reference step (also the result the graphs must reproduce)
-    draft_part(0)
-    verify_part(0)
-    commit_part()
-    torch.cuda.synchronize()
-    ref = (sd.d.clone(), sd.logits.clone(), sd.n_acc.clone(), sd.next.clone())
-
-    use_graph = not args.no_graph
-    graphs = None
-    if use_graph:
-        try:
-            side = torch.cuda.Stream()
-            side.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(side):
-                draft_part(0); verify_part(0); commit_part()
-            torch.cuda.current_stream().wait_stream(side)
-            torch.cuda.synchronize()
-            gd, gv, gc = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-            with torch.cuda.graph(gd):
-                draft_part(0)
-            with torch.cuda.graph(gv):
-                verify_part(0)
-            with torch.cuda.graph(gc):
-                commit_part()
-            graphs = (gd, gv, gc)
-            # every replay must reproduce the eager step exactly
-            for r in range(3):
-                gd.replay(); gv.replay(); gc.replay()
-                torch.cuda.synchronize()
-                same = (torch.equal(sd.d, ref[0]) and torch.equal(sd.logits, ref[1]) and
-                        torch.equal(sd.n_acc, ref[2]) and torch.equal(sd.next, ref[3]))
-                if not same:
-                    raise RuntimeError(f"graph replay {r} differs from the eager step")
-                draft_part(0); verify_part(0); commit_part()  # eager work between replays
-                torch.cuda.synchronize()
-        except Exception as e:  # report and time eagerly
-            log(f"graph capture disabled: {e}")
-            graphs, use_graph = None, False
-
-    def run_step(i, ev=None):
-        if graphs:
-            graphs[0].replay()
-            if ev: ev[0].record()
-            graphs[1].replay()
-            if ev: ev[1].record()
-            graphs[2].replay()
-        else:
-            draft_part(i)
-            if ev: ev[0].record()
-            verify_part(i)
-            if ev: ev[1].record()
-            commit_part()
-
+    graphs = capture_graphs(sd, draft_part, verify_part, commit_part, args.no_graph)
+    use_graph = graphs is not None
     if args.reload:
         print(json.dumps(reload_bench(dw, graphs, verify_part, args)), flush=True)
         return
-
-    for i in range(args.warmup):
-        run_step(i)
-    torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for i in range(args.steps):
-        run_step(args.warmup + i, evs[i])
-    end.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    verify_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
-    step_ms = total_ms / args.steps
+    tm = time_steps(graphs, draft_part, verify_part, commit_part, args.steps, args.warmup)
+    verify_ms, step_ms = tm["verify_ms"], tm["step_ms"]
     status = min(int(sd.status.item()), kv_t.read_state()["status"], kv_d.read_state()["status"])
 
     # mean accepted length over eager steps with distinct random draws (outside the timed region)
@@ -452,6 +571,8 @@ def main():
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                      "traffic": measured_traffic(dom), "bytes_per_launch": dom_bytes},
         "verify_ms": round(verify_ms, 4),
+        "verify_ms_p10_p50_p90": [round(tm["verify_ms_p10"], 4), round(tm["verify_ms_p50"], 4),
+                                  round(tm["verify_ms_p90"], 4)],
         "verify_hbm_GBps": round(verify_GBps, 1),
         "verify_hbm_frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
         "verify_bytes": vbytes,
