@@ -268,6 +268,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   at.ml_part = m->ml_part;
   at.o = m->o;
   at.status = kv_status(kv);
+  at.seq_bound = M / ra.rps > 1;
 
   for (int l = 0; l < m->n_layers; ++l) {
     GemmArgs q = base;  // RMSNorm + Q|K|V projections

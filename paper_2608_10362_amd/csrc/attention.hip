@@ -205,7 +205,19 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
   const int part = blockIdx.x % n_part, mt = blockIdx.x / n_part;
   const int RS = min(16, nq - mt * 16);  // query rows of this tile (> 0 by the grid)
   const int c16 = lane & 15, grp = lane >> 4;
-  const int sub_here = part == n_part - 1 ? n_sub - part * S : S;
+  int sub_here = part == n_part - 1 ? n_sub - part * S : S;
+  if (a.seq_bound) {
+    // Keys past this sequence's own context are never loaded: within a sequence
+    // positions grow with the row index, so its last row (when valid) bounds
+    // them.  (Scalar loads; one wait before the K/V loads are issued.)
+    const RowDesc last = a.rows[r0 + rps - 1];
+    if (last.valid) {
+      const int first = part * S * kSubKeys;
+      if (first > last.pos) return;  // (block-uniform, before any barrier) no key of this part is visible
+      const int need = (last.pos + 1 - first + kSubKeys - 1) / kSubKeys;
+      sub_here = need < sub_here ? need : sub_here;
+    }
+  }
   const int k0 = (part * S + wave) * kSubKeys;
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
   const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;

@@ -133,6 +133,7 @@ struct AttnArgs {
   float* ml_part;        // [M, h, n_split, 2]
   float* o;              // [M, h hd]
   int32_t* status;
+  int seq_bound;         // 1: bound each sequence's keys by its own last row (batches of several sequences)
 };
 int attention_chunk(int dtype, int head_dim);  // keys per split of the attention kernel
 int device_compute_units();                    // CUs of the current device (cached)
