@@ -45,8 +45,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, choices=(1, 2, 3, 5),
+    ap.add_argument("--config", type=int, default=3, choices=(1, 2, 3, 4, 5),
                     help="3 (default): the 7B gamma=4 bs1 headline line; 1: tiny float32; 2: 1.1B-shaped bf16; "
+                         "4: draft switching (2/4/8-layer drafts, resident / reload / cache policy); "
                          "5: 7B-shaped, 16 sequences with contexts U[1024, 8192], gamma 6, T 0.8")
     ap.add_argument("--reload", action="store_true",
                     help="instead of the verify line, measure draft reloads (2/4/8-layer drafts) from pinned host "
@@ -441,6 +442,67 @@ def run_config(args):
     print(json.dumps(result), flush=True)
 
 
+# ---------------------------------------------------------------- config 4: draft switching
+def run_switching(args):
+    """Draft switching on the 7B-shaped target (Sec. 3.3-3.4 on one GPU): drafts
+    of 2, 4 and 8 layers, context 1024, gamma 4, greedy, scheduling every N = 4
+    iterations along a Markov schedule (stay 0.8, seed 3, starting at the
+    4-layer draft), 128 generated tokens.  Modes: static (the 4-layer draft
+    throughout), resident (every draft resident), reload (one slot, blocking
+    reload on a switch), memspec (K = 2 slots, Alg. 2 prefetches overlapped with
+    decoding, best resident draft, Alg. 3).  Wall time covers the whole run,
+    catch-up forwards and reloads included."""
+    import torch
+
+    from paper_2608_10362_amd import binding, synth
+    from paper_2608_10362_amd.runtime import HostImage, SwitchingRunner, score_stream
+    shape = synth.LLAMA_7B
+    layers, g, ctx, N, K, n_iter, n_tok = [2, 4, 8], 4, 1024, 4, 2, 400, 128
+    cap = (ctx + n_iter * (g + 1) + 2 * g + 63) // 64 * 64
+    dw = device_weights(shape)
+    image = HostImage(dw, max(layers))
+    points = (n_iter + N - 1) // N
+    schedule = synth.make_markov_schedule(points, 3, start=1, stay=0.8)
+    scores = score_stream(schedule, 3)
+    pend = int(synth.make_prompt(1, shape.vocab)[0, 0])
+    out = {}
+    ref_text = None
+    for mode in ("static", "resident", "reload", "memspec"):
+        target = binding.Model(dw, shape.n_layers, max_rows=g + 1, max_ctx=cap)
+        kv_t = binding.KVCache(target, 1, cap)
+        r = SwitchingRunner(dw, target, kv_t, layers, g, 0.0, synth.SEED_SAMPLING, cap,
+                            "resident" if mode == "static" else mode, slots=K if mode == "memspec" else 1, image=image)
+        install_context(kv_t, shape.n_layers, shape, [ctx])
+        for d, k in enumerate(layers):
+            install_context(r.kv[d], k, shape, [ctx])
+        r.start_from_context(ctx, pend)
+        sched = [1] * points if mode == "static" else list(schedule)
+        st = r.run(n_iter, sched, scores, N, max_tokens=n_tok)
+        text = r.text[ctx:]
+        if ref_text is None:
+            ref_text = text
+        n_common = min(len(text), len(ref_text))
+        same = text[:n_common] == ref_text[:n_common]
+        out[mode] = {"wall_ms": round(st.wall_ms, 2), "iterations": st.iterations, "tokens": st.tokens,
+                     "tokens_per_s": round(st.tokens / (st.wall_ms * 1e-3), 2), "switches": st.switches,
+                     "reloads": st.reloads, "reload_GB": round(st.reload_bytes / 1e9, 3),
+                     "blocked_ms": round(st.blocked_ms, 2), "catchup_tokens": st.catchup_tokens,
+                     "matches_desired": round(float(np.mean([a == d for a, d in zip(st.active, st.desired)])), 3),
+                     "text_agrees": bool(same)}
+        log(f"{mode}: {out[mode]}")
+        del r, target, kv_t
+        torch.cuda.empty_cache()
+    result = {
+        "metric": "generated tokens/s under draft switching (config 4)", "value": out["memspec"]["tokens_per_s"],
+        "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+        "config": {"workload": "7B-shaped bf16 target, drafts of 2/4/8 layers, context 1024, gamma 4, greedy, "
+                               "interval N=4, K=2, Markov schedule stay 0.8 (seed 3), 128 generated tokens",
+                   "draft_layers": layers},
+        "modes": out,
+    }
+    print(json.dumps(result), flush=True)
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -454,6 +516,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     binding.lib()
+    if args.config == 4:
+        run_switching(args)
+        return
     if args.config != 3:
         run_config(args)
         return

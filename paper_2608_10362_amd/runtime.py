@@ -209,6 +209,14 @@ class SwitchingRunner:
         self.text = [int(t) for t in prompt.reshape(-1)]
         torch.cuda.synchronize()
 
+    def start_from_context(self, length: int, pending: int):
+        """Start from a resident context of `length` positions already installed in
+        the target's and every draft's cache (tokens unknown: only tokens after it
+        are ever re-processed) with `pending` as the next input token."""
+        for kv in [self.kv_t] + [self.kv[d] for d in range(len(self.layers))]:
+            kv.set_state([length], [[0, pending]], [1])
+        self.text = [-1] * length + [int(pending)]
+
     def _catch_up(self, d: int, model, stats: RunStats):
         """Bring draft d's cache up to the committed text: a forward over the
         tokens it has not processed; its pending token becomes the target's."""
