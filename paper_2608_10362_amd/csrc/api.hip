@@ -34,6 +34,7 @@ struct specdec_model {
   float* u;
   float* logits;
   void* samp;  // scratch of the draft's softmax / draw kernels
+  float* ypart = nullptr;  // split-K partials of the wide residual GEMMs (passes of more than 64 rows)
   int chunk, n_split_max;
   // layer-0 launches of the last forward pass, for specdec_time_kernel
   mutable bool rec_valid[SPECDEC_KERNEL_KINDS] = {};
@@ -91,7 +92,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, ypart, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -99,7 +100,10 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   WsLayout w{};
   const size_t R = (size_t)max_rows;
   const int hd = d->head_dim, H = d->n_heads, G = d->n_kv_heads;
-  w.ss_parts = std::max(1, gemm_row_blocks(d->dtype, EPI_RESID, d->d_model, max_rows));
+  // (passes of up to max_rows rows: the skinny and, above kMaxGemmRows, the wide partial counts)
+  w.ss_parts = std::max(1, gemm_row_blocks(d->dtype, EPI_RESID, d->d_model, std::min(max_rows, kMaxGemmRows)));
+  const bool wide = gemm_wide(d->dtype, max_rows);
+  if (wide) w.ss_parts = std::max(w.ss_parts, gemm_row_blocks(d->dtype, EPI_RESID, d->d_model, max_rows));
   w.chunk = attention_chunk(d->dtype, hd);
   w.n_split = (max_ctx + w.chunk - 1) / w.chunk;
   size_t off = 0;
@@ -117,6 +121,7 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.u = take(R * d->ffn_dim * 4);
   w.logits = take(R * d->vocab * 4);
   w.samp = take(sampling_scratch_bytes(max_rows, 1, d->vocab));
+  w.ypart = take(wide ? wide_ypart_floats(d->d_model) * 4 : 0);
   w.total = off;
   return w;
 }
@@ -184,11 +189,15 @@ specdec_status check_kv(const specdec_model* m, const specdec_kv* kv) {
   return SPECDEC_OK;
 }
 
-// Runs GEMM `g` over the rows [0, M) in launches of at most kMaxGemmRows rows.
+// Runs GEMM `g` over the rows [0, M) in launches of at most gemm_launch_rows rows
+// (the kernel family is chosen by the whole pass's M, so every launch of a pass
+// writes the same number of ss partials).
 hipError_t gemm_rows(int dtype, GemmArgs g, int M, hipStream_t s) {
-  for (int m0 = 0; m0 < M; m0 += kMaxGemmRows) {
+  const int step = gemm_launch_rows(dtype, M);
+  g.wide = gemm_wide(dtype, M);
+  for (int m0 = 0; m0 < M; m0 += step) {
     GemmArgs c = g;
-    c.M = std::min(kMaxGemmRows, M - m0);
+    c.M = std::min(step, M - m0);
     c.x = g.x + (size_t)m0 * g.ldx;
     if (g.out) c.out = g.out + (size_t)m0 * g.ldo;
     if (g.rows) c.rows = g.rows + m0;
@@ -247,6 +256,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   base.eps = d.rms_eps;
   base.ss_ld = m->ss_ld;
   base.gain_bf16 = dt == SPECDEC_BF16;
+  base.ypart = m->ypart;
   int n_ss = 1;
   const int n_resid_blocks = gemm_row_blocks(dt, EPI_RESID, d.d_model, M);
 
@@ -414,6 +424,8 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   if (!w || !workspace || max_rows <= 0 || max_ctx <= 0) return SPECDEC_ERR_INVALID_ARG;
   if (n_layers_used <= 0 || n_layers_used > desc->n_layers) return SPECDEC_ERR_INVALID_ARG;
   if ((uintptr_t)workspace % kAlign) return SPECDEC_ERR_INVALID_ARG;
+  // passes of more than 64 rows sum one RMSNorm partial per 128 columns in a wave: d_model <= 8192
+  if (gemm_wide(desc->dtype, max_rows) && desc->d_model > 8192) return SPECDEC_ERR_SHAPE;
   const WsLayout L = ws_layout(desc, max_rows, max_ctx);
   if (workspace_bytes < L.total) return SPECDEC_ERR_INVALID_ARG;
   const bool bf16 = desc->dtype == SPECDEC_BF16;
@@ -482,6 +494,7 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   m->u = (float*)(base + L.u);
   m->logits = (float*)(base + L.logits);
   m->samp = base + L.samp;
+  m->ypart = gemm_wide(desc->dtype, max_rows) ? (float*)(base + L.ypart) : nullptr;
   m->chunk = L.chunk;
   m->n_split_max = L.n_split;
   *out = m;

@@ -11,6 +11,8 @@
 // the weight fragment is read from HBM once; the padding of M up to 16 is
 // free because the pass is bandwidth-bound (about M flops per weight byte).
 // float32 weights (the tiny configuration) run on a plain vector kernel.
+#include <algorithm>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -465,6 +467,341 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   }
 }
 
+// ---------------------------------------------------------------- wide-M MFMA kernel (bf16 weights)
+// Passes of more than 64 rows (the verify blocks of many sequences, prefill
+// and catch-up chunks) in launches of up to 128 rows.  A block covers NC =
+// 64*T weight rows and a range of k-steps with G k-groups of 4 waves: group g
+// takes every G-th k-step of the range and wave w of a group owns tiles
+// wT..wT+T-1.  Each k-step's x slab (MP rows x 32 columns) is converted once
+// by its group into hi + lo bf16 A fragments in LDS (two buffers per group)
+// and shared by the group's four waves, so activation traffic per weight
+// byte falls by the 4T tiles sharing it.  Grids are about one block per CU,
+// so the G groups are what keeps more than one wave per SIMD busy; each wave
+// also keeps x slabs XR = 4 k-steps ahead and weight fragments D k-steps ahead
+// in register rings.  The groups' sums are added in group order in LDS; the
+// epilogues (store, SwiGLU, QKV with RoPE) then read the accumulators in
+// place.  Residual GEMMs (O, down: few row tiles) split K over the grid and
+// write partial sums, which resid_reduce_kernel adds in a fixed order.
+constexpr int kWideGroups = 2;
+constexpr int kWideThreads = 256 * kWideGroups;
+constexpr int kWideRows = 128;  // rows per launch of the wide kernel
+constexpr int kWideCols = 128;  // columns per block of the split-K reduction (and per ss partial)
+constexpr int kWideMaxSs = 64;  // ss partials a wide launch sums (one per lane)
+
+template <int MT, int T, int KIND>
+__global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int ks_per_split, int n_split) {
+  constexpr int G = kWideGroups;
+  constexpr int MP = 16 * MT, NC = 64 * T;
+  constexpr int D = T == 1 ? 8 : 4;                  // weight k-steps in flight per wave
+  constexpr int XR = 4;                              // x slabs in flight per group
+  constexpr int PJ = (MP * 4 + 255) / 256;           // 32-byte x pieces per thread per slab
+  constexpr int MTP = PJ * 256 / 64;                 // m tiles the pieces cover (>= MT; extra rows read zeros)
+  constexpr bool QKV = KIND == EPI_QKV, SCALE = KIND != EPI_RESID;
+  constexpr int RSR = MP / (4 * G);                  // row-scale rows per wave
+  constexpr int CSL = QKV ? MP / 16 : 1;             // 16-byte cos/sin pieces per lane (8 columns x MP rows x 2)
+  static_assert(KIND != EPI_SWIGLU || T == 2, "SwiGLU pairs one gate and one up tile per wave");
+  static_assert(!QKV || T == 1, "the QKV epilogue tables cover one tile per wave");
+  static_assert(D % XR == 0, "the unrolled step loop indexes both rings statically");
+  static_assert(MP % (4 * G) == 0, "row-scale rows split evenly over the waves");
+  static_assert((G - 1) * 4 * T * MT <= G * 2 * MTP * 2, "group sums fit in the slab buffers");
+  __shared__ u32x4 s_a[G][2][MTP][2][kWave];  // [group][buffer][m tile][hi, lo][lane]
+  __shared__ float scale[MP];
+  __shared__ f32x4 s_cs[QKV ? 4 : 1][QKV ? MP : 1][4];  // per tile wave, per row: cos of its 8 dims, then sin
+  __shared__ RowDesc s_rows[QKV ? MP : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2, wl = wave & 3, gtid = tid & 255;  // k-group, wave in group, thread in group
+  const int K = a.K, KS = (K + 31) / 32;
+  const int split = (int)blockIdx.x % n_split, blk = (int)blockIdx.x / n_split;
+  const int ks_begin = split * ks_per_split;
+  const int ks_end = min(KS, ks_begin + ks_per_split);
+  const int n_k = ks_end - ks_begin;
+  const int n_steps = (n_k + G - 1) / G;  // steps of every group (a group's last ones may be past the range)
+
+  // Weight tiles of this wave (SwiGLU: gate tile w and the up tile of the same columns).
+  __amdgpu_buffer_rsrc_t wr[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int lt = KIND == EPI_SWIGLU ? (t == 0 ? wl : 4 + wl) : wl * T + t;
+    bool ok;
+    const uint16_t* base = weight_tile(a, KIND, blk, NC, lt, KS, ok);
+    wr[t] = make_rsrc(base, ok ? (uint32_t)KS * 1024u : 0u);
+  }
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
+
+  floatx4 acc[T][MT];
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  u32x4 wv[D][T];
+  f32x4 xv[XR][PJ][2];
+
+  // Step j of group g is k-step ks_begin + j*G + g.
+  auto load_w = [&](int j, u32x4 (&w)[T]) {
+    const int i = j * G + grp;
+    const uint32_t bad = (uint32_t)(i >= n_k) << 31;
+    const uint32_t off = ((uint32_t)(ks_begin + i) * 1024u + lane * 16u) | bad;
+#pragma unroll
+    for (int t = 0; t < T; ++t) w[t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], off, 0, kNonTemporal);
+  };
+  // Piece p = lane p%64 of the A fragment of m tile p/64: 8 consecutive floats
+  // of row 16*(p/64) + p%16 at column 8*(p%64/16) of the k-step (a wave moves
+  // whole fragments: contiguous LDS stores, 16 rows x 128 bytes per load).
+  auto load_x = [&](int j, f32x4 (&xs)[PJ][2]) {
+    const int i = j * G + grp;
+    const uint32_t bad = (uint32_t)(i >= n_k) << 31;
+#pragma unroll
+    for (int q = 0; q < PJ; ++q) {
+      const int p = gtid + q * 256, m = (p >> 6) * 16 + (p & 15), k = (ks_begin + i) * 32 + ((p >> 4) & 3) * 8;
+      const uint32_t off = (((uint32_t)m * a.ldx + k) * 4u) | bad | ((uint32_t)(k >= K) << 31);
+      xs[q][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      xs[q][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off + 16u, 0, 0));
+    }
+  };
+  // A fragment lane 16*(k/8) + m%16 holds row m, columns 8*(k/8)..+7
+  auto store_x = [&](int buf, const f32x4 (&xs)[PJ][2]) {
+#pragma unroll
+    for (int q = 0; q < PJ; ++q) {
+      const int p = gtid + q * 256;
+      const int mt = p >> 6, ln = p & 63;
+      bf16x8 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = xs[q][e >> 2][e & 3];
+        const __bf16 h = (__bf16)v;
+        hi[e] = h;
+        lo[e] = (__bf16)(v - (float)h);
+      }
+      s_a[grp][buf][mt][0][ln] = __builtin_bit_cast(u32x4, hi);
+      s_a[grp][buf][mt][1][ln] = __builtin_bit_cast(u32x4, lo);
+    }
+  };
+  // All fragment reads first, then the hi products of every tile, then the lo
+  // ones (a product's accumulator is not the previous product's).
+  auto compute = [&](int buf, const u32x4 (&w)[T]) {
+    bf16x8 av[MT][2];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      av[mt][0] = __builtin_bit_cast(bf16x8, s_a[grp][buf][mt][0][lane]);
+      av[mt][1] = __builtin_bit_cast(bf16x8, s_a[grp][buf][mt][1][lane]);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+          acc[t][mt] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[mt][h], __builtin_bit_cast(bf16x8, w[t]), acc[t][mt], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * MT, 0);     // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * MT * T, 0);  // then MFMAs
+  };
+
+  // QKV epilogue geometry of this wave's tile: rotation dims 8*tq + e (e < 8)
+  // of its head for Q and K columns.
+  const int hd = a.head_dim, half = hd >> 1;
+  const int nq = a.n_seg[0], nqk = nq + a.n_seg[1];
+  const int n0 = blk * NC + wl * 16;  // (QKV: T == 1)
+  const int r0 = n0 >= nqk ? n0 - nqk : (n0 >= nq ? n0 - nq : n0);
+  const int tq = (r0 % hd) >> 4;
+
+  // Prologue.  Loads in order: the epilogue's small operands (row-scale
+  // partial sums; QKV: cos/sin of the tile's 8 dims and the row descriptors,
+  // fetched by group 0), XR x slabs, D weight k-steps.  Loads complete in
+  // order, so storing the small operands waits for them alone.
+  float rsv[SCALE ? RSR : 1];
+  if constexpr (SCALE) {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(a.ss_in, a.ss_in ? (uint32_t)a.n_ss * a.ss_ld * 4u : 0u);
+#pragma unroll
+    for (int i = 0; i < RSR; ++i) {
+      const int m = wave + 4 * G * i;
+      const uint32_t off = ((uint32_t)lane * a.ss_ld + m) * 4u | ((uint32_t)(m >= a.M || lane >= a.n_ss) << 31);
+      rsv[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off, 0, 0));
+    }
+  }
+  f32x4 csv[CSL];
+  u32x4 rdv = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (QKV) {
+    const __amdgpu_buffer_rsrc_t cr = make_rsrc(a.rope_cs, (uint32_t)a.M * hd * 4u);
+#pragma unroll
+    for (int q = 0; q < CSL; ++q) {  // piece v = lane + 64q: row v/4, (cos, sin) = (v/2)%2, half (v%2)
+      const int v = lane + 64 * q, m = v >> 2, sn = (v >> 1) & 1, hf = v & 1;
+      const uint32_t off = ((uint32_t)m * hd + sn * half + 8 * tq + 4 * hf) * 4u |
+                           ((uint32_t)(n0 >= nqk || grp != 0) << 31);
+      csv[q] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(cr, off, 0, 0));
+    }
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.rows, (uint32_t)a.M * (uint32_t)sizeof(RowDesc));
+    rdv = __builtin_amdgcn_raw_buffer_load_b128(
+        rr, (uint32_t)tid * (uint32_t)sizeof(RowDesc) | ((uint32_t)(tid >= MP) << 31), 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < XR; ++r) load_x(r, xv[r]);
+#pragma unroll
+  for (int u = 0; u < D; ++u) load_w(u, wv[u]);
+  if constexpr (SCALE) {
+    // s_m = 1/sqrt(sum_p ss[p][m] / K + eps): partial p in lane p, fixed shuffle tree
+#pragma unroll
+    for (int i = 0; i < RSR; ++i) {
+      const int m = wave + 4 * G * i;
+      const float t = wave_sum(rsv[i]);  // (n_ss <= 64: checked by the launcher)
+      if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+    }
+  }
+  if constexpr (QKV) {
+    if (grp == 0) {
+#pragma unroll
+      for (int q = 0; q < CSL; ++q) {
+        const int v = lane + 64 * q;
+        s_cs[wl][v >> 2][v & 3] = csv[q];
+      }
+    }
+    if (tid < MP) s_rows[tid] = __builtin_bit_cast(RowDesc, rdv);
+  }
+  store_x(0, xv[0]);
+  load_x(XR, xv[0]);
+  __syncthreads();
+
+  // Step j: multiply the group's slab j (LDS buffer j%2) by weight slot j%D,
+  // refill the slot with step j+D, move slab j+1 (register slot (j+1)%XR) into
+  // the other buffer and fetch slab j+1+XR into its slot.  The step count is
+  // rounded up to a multiple of D: steps past the range multiply zeros (their
+  // loads are out of range), which keeps the loop free of early exits (an exit
+  // edge into the loop makes the compiler wait for every load in flight at the
+  // top of the loop).  (Scheduling barriers keep each step's conversions after
+  // its multiplies: hoisted above them, the conversions of a later slab would
+  // wait for the weight loads issued after it.)
+  for (int j0 = 0; j0 < n_steps; j0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int j = j0 + u;
+      __builtin_amdgcn_sched_barrier(0);
+      compute(u & 1, wv[u]);
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(j + D, wv[u]);
+      store_x((u + 1) & 1, xv[(u + 1) % XR]);
+      load_x(j + 1 + XR, xv[(u + 1) % XR]);
+      __syncthreads();
+    }
+  }
+
+  // Group sums: groups 1.. park theirs in the (now free) slab buffers, group 0
+  // adds them in group order and runs the epilogue.
+  if constexpr (G > 1) {
+    floatx4* park = reinterpret_cast<floatx4*>(&s_a[0][0][0][0][0]);
+    if (grp > 0) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) park[(((grp - 1) * 4 + wl) * T * MT + t * MT + mt) * kWave + lane] = acc[t][mt];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g = 1; g < G; ++g)
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] += park[(((g - 1) * 4 + wl) * T * MT + t * MT + mt) * kWave + lane];
+  }
+
+  // Epilogue (group 0).  acc[t][mt][r] is row mt*16 + 4*(lane/16) + r, column lane%16 of tile t.
+  const int M = a.M, cl = lane & 15, rg = lane >> 4;
+  if constexpr (KIND == EPI_RESID) {
+    float* yp = a.ypart + (size_t)split * M * a.n_rows;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int n = blk * NC + (wl * T + t) * 16 + cl;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mt * 16 + 4 * rg + r;
+          if (m < M && n < a.n_rows) yp[(size_t)m * a.n_rows + n] = acc[t][mt][r];
+        }
+    }
+  } else if constexpr (KIND == EPI_STORE) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int n = blk * NC + (wl * T + t) * 16 + cl;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mt * 16 + 4 * rg + r;
+          if (m < M && n < a.n_rows) a.out[(size_t)m * a.ldo + n] = acc[t][mt][r] * scale[m];
+        }
+    }
+  } else if constexpr (KIND == EPI_SWIGLU) {
+    const int f = blk * (NC / 2) + wl * 16 + cl;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mt * 16 + 4 * rg + r;
+        if (m < M && f < a.n_rows)
+          a.out[(size_t)m * a.ldo + f] = silu_f(acc[0][mt][r] * scale[m]) * (acc[1][mt][r] * scale[m]);
+      }
+  } else {  // EPI_QKV: the RoPE partner of column c is column c ^ 8 of the same tile, i.e. lane ^ 8
+    const int H = a.n_heads, cap = a.kv.capacity;
+    const int n = n0 + cl;
+    const bool is_q = n < nq, is_v = n >= nqk;
+    const int head = r0 / hd, w = r0 % hd + cl, ec = cl, e = cl & 7;
+    const int j = 8 * tq + e, d = ec < 8 ? j : half + j;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mt * 16 + 4 * rg + r;
+        const float x = acc[0][mt][r] * scale[m];
+        const float y = __shfl_xor(x, 8, kWave);
+        if (m >= M || n >= a.n_rows) continue;
+        const RowDesc rd = s_rows[m];
+        if (is_v) {
+          if (rd.valid) {
+            uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+            Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::v(rd.pos, w, hd, cap), x);
+          }
+          continue;
+        }
+        const f32x4 c4 = s_cs[wl][m][e >> 2], s4 = s_cs[wl][m][2 + (e >> 2)];
+        const float cs = c4[e & 3], sn = s4[e & 3];
+        const float out = ec < 8 ? x * cs - y * sn : x * cs + y * sn;
+        if (is_q) {
+          a.qr[((size_t)m * H + head) * hd + d] = out;
+        } else if (rd.valid) {
+          uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+          Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::k(rd.pos, d, hd, cap), out);
+        }
+      }
+  }
+}
+
+// Sum of the split-K partials of a residual GEMM in split order, residual
+// add, next RMSNorm input and its sums of squares.  Block = 128 columns x 8
+// rows; thread = 4 columns of one row; ss partial p = column block p.
+__global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_split) {
+  const int tid = threadIdx.x, m = (int)blockIdx.y * 8 + (tid >> 5);
+  const int n = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
+  const int M = a.M;
+  float t = 0.f;
+  if (m < M && n < a.n_rows) {
+    f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < n_split; ++s) y += *(const f32x4*)(a.ypart + ((size_t)s * M + m) * a.n_rows + n);
+    float* hp = a.out + (size_t)m * a.ldo + n;
+    const f32x4 h = *(const f32x4*)hp + y;
+    *(f32x4*)hp = h;
+    const uint16_t* g = (const uint16_t*)a.gain_out + n;
+    *(f32x4*)(a.xg_out + (size_t)m * a.ldo + n) =
+        f32x4{h[0] * bf16_bits_to_f32(g[0]), h[1] * bf16_bits_to_f32(g[1]), h[2] * bf16_bits_to_f32(g[2]),
+              h[3] * bf16_bits_to_f32(g[3])};
+    t = h[0] * h[0] + h[1] * h[1] + h[2] * h[2] + h[3] * h[3];
+  }
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) t += __shfl_xor(t, o, kWave);
+  if ((tid & 31) == 0 && m < M) a.ss_out[(size_t)blockIdx.x * a.ss_ld + m] = t;
+}
+
 // ---------------------------------------------------------------- vector kernel (float32 weights)
 // Block = 4 waves over NC weight rows; each wave takes NC/4 rows, lanes stride
 // over K; M processed 8 rows at a time.
@@ -617,8 +954,13 @@ hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hi
   return hipGetLastError();
 }
 
+bool gemm_wide(int dtype, int M) { return dtype == SPECDEC_BF16 && M > kMaxGemmRows; }
+int gemm_launch_rows(int dtype, int M) { return gemm_wide(dtype, M) ? kWideRows : kMaxGemmRows; }
+constexpr int kWideSplitMax = 4;
+size_t wide_ypart_floats(int n_rows) { return (size_t)kWideSplitMax * kWideRows * n_rows; }
+
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M) {
-  (void)M;
+  if (gemm_wide(dtype, M) && kind == EPI_RESID) return (n_rows + kWideCols - 1) / kWideCols;
   if (dtype == SPECDEC_BF16) {
     int nc = 16 * mfma_tiles(kind, n_rows);
     int per = kind == EPI_SWIGLU ? nc / 2 : nc;
@@ -628,8 +970,63 @@ int gemm_row_blocks(int dtype, int kind, int n_rows, int M) {
   return (n_rows + per - 1) / per;
 }
 
+namespace {
+template <int MT, int T, int KIND>
+void launch_wide_mt(const GemmArgs& a, int blocks, int ks_per_split, int n_split, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_bf16_wide<MT, T, KIND>), dim3(blocks * n_split), dim3(kWideThreads), 0, s, a,
+                     ks_per_split, n_split);
+}
+template <int T, int KIND>
+void launch_wide_t(const GemmArgs& a, int blocks, int ks_per_split, int n_split, hipStream_t s) {
+  const int MT = (a.M + 15) / 16;
+  if (MT <= 4) launch_wide_mt<4, T, KIND>(a, blocks, ks_per_split, n_split, s);
+  else if (MT <= 7) launch_wide_mt<7, T, KIND>(a, blocks, ks_per_split, n_split, s);
+  else launch_wide_mt<8, T, KIND>(a, blocks, ks_per_split, n_split, s);
+}
+
+hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
+  if (a.M > kWideRows || (a.ss_in && a.n_ss > kWideMaxSs)) return hipErrorInvalidValue;
+  const int KS = (a.K + 31) / 32, cus = compute_units();
+  switch (a.kind) {
+    case EPI_STORE: {
+      const int T = (a.n_rows + 127) / 128 * 10 >= cus * 9 ? 2 : 1;
+      const int blocks = (a.n_rows + 64 * T - 1) / (64 * T);
+      if (T == 2) launch_wide_t<2, EPI_STORE>(a, blocks, KS, 1, s);
+      else launch_wide_t<1, EPI_STORE>(a, blocks, KS, 1, s);
+      break;
+    }
+    case EPI_QKV:
+      if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
+        return hipErrorInvalidValue;
+      launch_wide_t<1, EPI_QKV>(a, (a.n_rows + 63) / 64, KS, 1, s);
+      break;
+    case EPI_SWIGLU: launch_wide_t<2, EPI_SWIGLU>(a, (a.n_rows + 63) / 64, KS, 1, s); break;
+    case EPI_RESID: {
+      if (!a.ypart) return hipErrorInvalidValue;
+      // split K until the grid covers the CUs (each split at least one k-step)
+      const int blocks = (a.n_rows + 63) / 64;
+      int n_split = std::min(kWideSplitMax, std::max(1, (cus + blocks - 1) / blocks));
+      n_split = std::min(n_split, KS);
+      const int ks_per_split = (KS + n_split - 1) / n_split;
+      n_split = (KS + ks_per_split - 1) / ks_per_split;
+      launch_wide_t<1, EPI_RESID>(a, blocks, ks_per_split, n_split, s);
+      hipLaunchKernelGGL(resid_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8),
+                         dim3(256), 0, s, a, n_split);
+      break;
+    }
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 0 || a.M > kMaxGemmRows || (a.K % 8) != 0 || (a.ldx % 4) != 0) return hipErrorInvalidValue;
+  if (a.M <= 0 || (a.K % 8) != 0 || (a.ldx % 4) != 0) return hipErrorInvalidValue;
+  if (a.wide) {
+    if (dtype != SPECDEC_BF16 || (a.kind == EPI_RESID && (!a.gain_bf16 || a.n_rows % 4))) return hipErrorInvalidValue;
+    return launch_wide(a, s);
+  }
+  if (a.M > kMaxGemmRows) return hipErrorInvalidValue;
   const int blocks = gemm_row_blocks(dtype, a.kind, a.n_rows, a.M);
   if (dtype == SPECDEC_BF16) {
     if (a.kind == EPI_RESID && !a.gain_bf16) return hipErrorInvalidValue;

@@ -57,7 +57,13 @@ template <> struct KvIndex<uint16_t> {
 // to the cache.  It needs the rotation pairs (j, j + hd/2) of a head in the
 // same 16-row tile, which the packed image provides (see launch_pack).
 enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
-constexpr int kMaxGemmRows = 64;  // rows of x per GEMM launch (callers split larger M)
+constexpr int kMaxGemmRows = 64;  // rows of x per launch of the skinny kernels (callers split larger M)
+// Passes of more than kMaxGemmRows bf16 rows run the wide kernel in launches of
+// up to gemm_launch_rows() rows; residual GEMMs there split K over the grid
+// and need ypart = wide_ypart_floats(n_rows) floats.
+bool gemm_wide(int dtype, int M);
+int gemm_launch_rows(int dtype, int M);
+size_t wide_ypart_floats(int n_rows);
 
 struct GemmArgs {
   const float* x;      // [M, ldx] (for normalised inputs: h * gain, the producer applies the gain)
@@ -82,6 +88,9 @@ struct GemmArgs {
   float* qr;              // [M, H, hd] rotated queries
   KvLayout kv;
   int layer, n_heads, n_kv_heads, head_dim;
+  // wide passes
+  int wide;               // 1: the whole pass has more than kMaxGemmRows rows (set by the caller for every launch)
+  float* ypart;           // RESID: split-K partial sums, wide_ypart_floats(n_rows) floats
 };
 // Packed bf16 weight image (16-row x 32-column 1 KB fragments in MFMA operand
 // order).  rope_hd > 0 reorders the rows of each head of rope_hd rows so that
@@ -89,7 +98,8 @@ struct GemmArgs {
 // rotation pairs of RoPE side by side, 8 columns apart); 0 keeps the order.
 size_t packed_elems(int N, int K);
 hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s);
-// Number of row blocks the launcher uses for this GEMM (for ss partial counts).
+// Number of row blocks the launcher uses for this GEMM (for ss partial counts)
+// in a pass of M rows.
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M);
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 

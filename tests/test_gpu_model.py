@@ -209,9 +209,17 @@ def test_bf16_7b_shape_verify(g):
 
 
 def test_bf16_7b_shape_multi_request_ragged():
-    # 16 sequences, ragged contexts, gamma 6: 112 rows (GEMMs run in two row launches)
+    # 16 sequences, ragged contexts, gamma 6: 112 rows (one launch of the wide GEMMs)
     lengths = synth.make_ragged_lengths(16, 40, 400)
     _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=2)
+
+
+@pytest.mark.parametrize("B,g", [(13, 4), (16, 7), (25, 7)])
+def test_bf16_1b_shape_wide_rows(B, g):
+    # 65, 128 and 200 rows (128 + 72 in two launches): the wide GEMM path with
+    # its 4-, 7- and 8-tile row variants, split-K residual GEMMs, head_dim 64 RoPE
+    lengths = synth.make_ragged_lengths(B, 1, 300, seed=5)
+    _bf16_case(synth.LLAMA_1B, 2, list(lengths), g=g, seed=3)
 
 
 # ---------------------------------------------------------------- context copy and errors
