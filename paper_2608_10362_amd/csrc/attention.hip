@@ -10,6 +10,8 @@
 // exp-sum and unnormalised P V; a combine kernel merges the chunks per (row,
 // head).  Query i of a sequence at position pos_i sees keys 0..pos_i (causal
 // inside the verify block).
+#include <algorithm>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -190,9 +192,15 @@ __host__ __device__ inline size_t attn_block_lds(int NW, int RS, int HD) {
 }
 
 constexpr int kMaxPartWaves = 12;  // 3 waves per SIMD: up to 170 VGPRs per lane
+constexpr int kLoopWaves = 4;      // waves per block when waves loop over several sub-chunks
 
-template <int HD>
-__global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs a, int S, int n_sub, int NW) {
+// LOOP: wave w takes sub-chunks w, w + NW, ... of its part (online softmax
+// across them), so long contexts keep every wave streaming K/V instead of
+// ending the block after one sub-chunk (4-wave blocks, up to 256 registers);
+// otherwise each wave takes one sub-chunk (up to 12-wave blocks).
+template <int HD, bool LOOP>
+__global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ? 2 : 1) void attn_block_kernel(
+    AttnArgs a, int S, int n_sub, int NW) {
   constexpr int KST = HD / 32;  // k-steps of Q K^T
   constexpr int DT = HD / 16;   // 16-wide dimension tiles of P V
   constexpr int NT = kSubKeys / 16;
@@ -218,7 +226,6 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
       sub_here = need < sub_here ? need : sub_here;
     }
   }
-  const int k0 = (part * S + wave) * kSubKeys;
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
   const uint16_t* vb = kb + (size_t)a.kv.capacity * HD;
 
@@ -230,10 +237,10 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
   float* pbuf = smem + (size_t)wave * 16 * (kSubKeys + 4);
 
   if (wave < sub_here) {  // (wave-uniform) a wave past the part's sub-chunks only joins the merge
-    // Every load is issued before anything waits, smallest first (loads complete
-    // in order, so waiting for an early one never waits for a later one): the
-    // row descriptors, the K fragments, Q, then the V fragments.  Row
-    // descriptors and Q go through range-checked buffer loads.
+    // Every load of the first sub-chunk is issued before anything waits,
+    // smallest first (loads complete in order, so waiting for an early one never
+    // waits for a later one): the row descriptors, the K fragments, Q, then the
+    // V fragments.  Row descriptors and Q go through range-checked buffer loads.
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0,
                                                                          a.M * (int)sizeof(RowDesc), 0x00020000);
     // (only the two fields used: a wider load leaves dead destination registers
@@ -241,13 +248,23 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
     const uint32_t roff = ((uint32_t)(r0 + lane) * (uint32_t)sizeof(RowDesc)) | ((uint32_t)(lane >= rps) << 31);
     const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
     const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
-    // K fragments of the sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity).
-    u32x4 kf[NT][KST];
-    const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
+    // K fragments of a sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity);
+    // V fragments: DT contiguous 1 KB fragments (32 positions x 16 dims each).
+    u32x4 kf[NT][KST], vf[DT];
+    auto load_k = [&](int k0) {
+      const uint16_t* kfrag = kb + (size_t)(k0 / 16) * KST * 512 + lane * 8;
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
+        for (int c = 0; c < KST; ++c) kf[t][c] = *(const u32x4*)(kfrag + (size_t)(t * KST + c) * 512);
+    };
+    auto load_v = [&](int k0) {
+      const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vf[dt] = *(const u32x4*)(vfrag + (size_t)dt * 512);
+    };
+    int k0 = (part * S + wave) * kSubKeys;
+    load_k(k0);
     // Q fragments (A operand): query qa = mt*16 + l%16 (zeros past nq).
     f32x4 qv4[KST][2];
     {
@@ -263,11 +280,7 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
             __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 128u * c + 16u, 0, 0));
       }
     }
-    // V fragments: DT contiguous 1 KB fragments (32 positions x 16 dims each).
-    u32x4 vf[DT];
-    const uint16_t* vfrag = vb + (size_t)(k0 / 32) * DT * 512 + lane * 8;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[dt] = *(const u32x4*)(vfrag + (size_t)dt * 512);
+    load_v(k0);
     // (compiler barrier: keeps what follows from being hoisted above the loads)
     asm volatile("" ::: "memory");
 
@@ -283,29 +296,34 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
       const int p = __shfl(mypos, min(qc, nq - 1) / group, kWave);
       qpos[r] = qc < nq ? p : -1;
     }
-    if (k0 < nk) {
+    const float scale = 1.0f / sqrtf((float)HD);
+    bf16x8 qhi[KST], qlo[KST];
+#pragma unroll
+    for (int c = 0; c < KST; ++c) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[j] = qv4[c][0][j] * scale;
+        v[4 + j] = qv4[c][1][j] * scale;
+      }
+      split_hilo(v, qhi[c], qlo[c]);
+    }
+
+    for (int j = wave; j < sub_here && k0 < nk; j += NW) {  // (wave-uniform)
+      if (j != wave) {  // the first sub-chunk's fragments were loaded above
+        load_k(k0);
+        load_v(k0);
+      }
       // keys past the context: zero their V entries (never multiply stale memory)
       const int nvalid = nk - (k0 + 8 * grp);
       if (nvalid < 8) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (2 * j >= nvalid) vf[dt][j] = 0u;
-            else if (2 * j + 1 >= nvalid) vf[dt][j] &= 0xffffu;
+          for (int q = 0; q < 4; ++q) {
+            if (2 * q >= nvalid) vf[dt][q] = 0u;
+            else if (2 * q + 1 >= nvalid) vf[dt][q] &= 0xffffu;
           }
-      }
-      const float scale = 1.0f / sqrtf((float)HD);
-      bf16x8 qhi[KST], qlo[KST];
-#pragma unroll
-      for (int c = 0; c < KST; ++c) {
-        float v[8];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          v[j] = qv4[c][0][j] * scale;
-          v[4 + j] = qv4[c][1][j] * scale;
-        }
-        split_hilo(v, qhi[c], qlo[c]);
       }
       floatx4 sf[NT];
 #pragma unroll
@@ -323,25 +341,31 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
           if (key > qpos[r]) acc[r] = -INFINITY;
         sf[t] = acc;
       }
+      // Online softmax: the running (max, sum, O) of each row is rescaled by
+      // exp(old max - new max) when this sub-chunk raises the max.
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float m = -INFINITY;
 #pragma unroll
         for (int t = 0; t < NT; ++t) m = fmaxf(m, sf[t][r]);
-        mx[r] = group16_max(m);
+        const float mnew = fmaxf(mx[r], group16_max(m));
+        const float alpha = mx[r] == -INFINITY ? 0.f : expf(mx[r] - mnew);
         float sum = 0.f;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-          const float p = mx[r] == -INFINITY || sf[t][r] == -INFINITY ? 0.f : expf(sf[t][r] - mx[r]);
+          const float p = mnew == -INFINITY || sf[t][r] == -INFINITY ? 0.f : expf(sf[t][r] - mnew);
           pbuf[(4 * grp + r) * (kSubKeys + 4) + 16 * t + c16] = p;
           sum += p;
         }
-        sm[r] = group16_sum(sum);
+        sm[r] = sm[r] * alpha + group16_sum(sum);
+        mx[r] = mnew;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) of[dt][r] *= alpha;
       }
       __builtin_amdgcn_wave_barrier();  // P written by all lanes of the wave before the transposed reads
       float pv[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) pv[j] = pbuf[c16 * (kSubKeys + 4) + 8 * grp + j];
+      for (int q = 0; q < 8; ++q) pv[q] = pbuf[c16 * (kSubKeys + 4) + 8 * grp + q];
       bf16x8 phi, plo;
       split_hilo(pv, phi, plo);
 #pragma unroll
@@ -350,6 +374,9 @@ __global__ __launch_bounds__(64 * kMaxPartWaves) void attn_block_kernel(AttnArgs
         of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vv, of[dt], 0, 0, 0);
         of[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vv, of[dt], 0, 0, 0);
       }
+      if constexpr (!LOOP) break;
+      __builtin_amdgcn_wave_barrier();  // the transposed reads of P done before the next sub-chunk writes it
+      k0 += NW * kSubKeys;
     }
   }
 
@@ -582,27 +609,45 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     const int nq = a.rps * (a.n_heads / a.n_kv_heads), n_mt = (nq + 15) / 16, RS = nq < 16 ? nq : 16;
     const int n_sub = (a.max_ctx + kSubKeys - 1) / kSubKeys;
     if (n_sub * kSubKeys > a.kv.capacity || n_sub > a.n_split * (a.chunk / kSubKeys)) return hipErrorInvalidValue;
-    // sub-chunks per part: the blocks should about fill the CUs once
     const long units = (long)a.n_kv_heads * B * n_mt;
-    int S = (int)((n_sub * units + device_compute_units() / 2) / device_compute_units());
-    S = S < 1 ? 1 : (S > kMaxPartWaves ? kMaxPartWaves : S);  // (reduced below while the last part is too big)
-    int n_part = 0, NW = 0;
-    for (;; --S) {
-      n_part = n_sub / S > 0 ? n_sub / S : 1;
-      NW = n_sub - (n_part - 1) * S;
-      if (S == 1 || (NW <= kMaxPartWaves && attn_block_lds(NW, RS, a.head_dim) <= 65536)) break;
+    const int cus = device_compute_units();
+    int S = 0, n_part = 0, NW = 0;
+    if (n_sub * units <= (long)cus * kMaxPartWaves) {
+      // One sub-chunk per wave, one round: parts of S sub-chunks (the last one
+      // takes the remainder), the blocks about filling the CUs once.
+      S = (int)((n_sub * units + cus / 2) / cus);
+      S = S < 1 ? 1 : (S > kMaxPartWaves ? kMaxPartWaves : S);  // (reduced below while the last part is too big)
+      for (;; --S) {
+        n_part = n_sub / S > 0 ? n_sub / S : 1;
+        NW = n_sub - (n_part - 1) * S;
+        if (S == 1 || (NW <= kMaxPartWaves && attn_block_lds(NW, RS, a.head_dim) <= 65536)) break;
+      }
+    } else {
+      // Long contexts: 4-wave blocks whose waves loop over the sub-chunks of
+      // their part; parts sized for about 8 blocks per CU (several resident
+      // per CU, short tails when sequences differ in length).
+      NW = kLoopWaves;
+      const long parts = std::max(1L, (8L * cus + units - 1) / units);
+      S = (int)((n_sub + parts - 1) / parts);
+      S = (S + NW - 1) / NW * NW;
+      n_part = (n_sub + S - 1) / S;
     }
     if (NW > kMaxPartWaves || attn_block_lds(NW, RS, a.head_dim) > 65536) return hipErrorInvalidValue;
     ab.n_split = n_part;
     ab.chunk = S * kSubKeys;
     dim3 grid(n_part * n_mt, a.n_kv_heads, B);
     const size_t lds = attn_block_lds(NW, RS, a.head_dim);
+    const bool loop = S > NW;
+#define SD_ATTN(HDV)                                                                                       \
+  if (loop) hipLaunchKernelGGL((attn_block_kernel<HDV, true>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); \
+  else hipLaunchKernelGGL((attn_block_kernel<HDV, false>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW);
     switch (a.head_dim) {
-      case 32: hipLaunchKernelGGL((attn_block_kernel<32>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
-      case 64: hipLaunchKernelGGL((attn_block_kernel<64>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
-      case 128: hipLaunchKernelGGL((attn_block_kernel<128>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); break;
+      case 32: SD_ATTN(32) break;
+      case 64: SD_ATTN(64) break;
+      case 128: SD_ATTN(128) break;
       default: return hipErrorInvalidValue;
     }
+#undef SD_ATTN
   } else {
     const size_t smem = attn_smem_bytes(a.chunk, a.head_dim);
     dim3 grid(a.n_split, a.n_kv_heads, B);

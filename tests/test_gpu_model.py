@@ -214,6 +214,13 @@ def test_bf16_7b_shape_multi_request_ragged():
     _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=2)
 
 
+def test_bf16_7b_shape_long_context_looping_attention():
+    # 2 sequences of 4500 and 6100 keys: 188 sub-chunks of 32 keys over 64
+    # (kv head, sequence) units -> parts of 8 sub-chunks on 4-wave blocks, each
+    # wave looping over 2 sub-chunks with the online softmax
+    _bf16_case(synth.LLAMA_7B, 1, [4500, 6100], g=4, seed=4)
+
+
 @pytest.mark.parametrize("B,g", [(13, 4), (16, 7), (25, 7)])
 def test_bf16_1b_shape_wide_rows(B, g):
     # 65, 128 and 200 rows (128 + 72 in two launches): the wide GEMM path with
