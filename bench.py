@@ -450,12 +450,14 @@ def run_switching(args):
     4-layer draft), 128 generated tokens.  Modes: static (the 4-layer draft
     throughout), resident (every draft resident), reload (one slot, blocking
     reload on a switch), memspec (K = 2 slots, Alg. 2 prefetches overlapped with
-    decoding, best resident draft, Alg. 3).  Wall time covers the whole run,
+    decoding, best resident draft, Alg. 3), mab (K = 2 slots, the MAB-Async
+    baseline: UCB with c = 2.0 over observed utilities, reactive asynchronous
+    loads, the active draft as the fallback).  Wall time covers the whole run,
     catch-up forwards and reloads included."""
     import torch
 
     from paper_2608_10362_amd import binding, synth
-    from paper_2608_10362_amd.runtime import HostImage, SwitchingRunner, score_stream
+    from paper_2608_10362_amd.runtime import HostImage, SwitchingRunner, observed_utility, score_stream
     shape = synth.LLAMA_7B
     layers, g, ctx, N, K, n_iter, n_tok = [2, 4, 8], 4, 1024, 4, 2, 400, 128
     cap = (ctx + n_iter * (g + 1) + 2 * g + 63) // 64 * 64
@@ -464,20 +466,22 @@ def run_switching(args):
     points = (n_iter + N - 1) // N
     schedule = synth.make_markov_schedule(points, 3, start=1, stay=0.8)
     scores = score_stream(schedule, 3)
+    utility = observed_utility(schedule, 3)
     pend = int(synth.make_prompt(1, shape.vocab)[0, 0])
     out = {}
     ref_text = None
-    for mode in ("static", "resident", "reload", "memspec"):
+    for mode in ("static", "resident", "reload", "memspec", "mab"):
         target = binding.Model(dw, shape.n_layers, max_rows=g + 1, max_ctx=cap)
         kv_t = binding.KVCache(target, 1, cap)
         r = SwitchingRunner(dw, target, kv_t, layers, g, 0.0, synth.SEED_SAMPLING, cap,
-                            "resident" if mode == "static" else mode, slots=K if mode == "memspec" else 1, image=image)
+                            "resident" if mode == "static" else mode, slots=K if mode in ("memspec", "mab") else 1,
+                            image=image)
         install_context(kv_t, shape.n_layers, shape, [ctx])
         for d, k in enumerate(layers):
             install_context(r.kv[d], k, shape, [ctx])
         r.start_from_context(ctx, pend)
         sched = [1] * points if mode == "static" else list(schedule)
-        st = r.run(n_iter, sched, scores, N, max_tokens=n_tok)
+        st = r.run(n_iter, sched, scores, N, max_tokens=n_tok, utility=utility)
         text = r.text[ctx:]
         if ref_text is None:
             ref_text = text
@@ -488,6 +492,7 @@ def run_switching(args):
                      "reloads": st.reloads, "reload_GB": round(st.reload_bytes / 1e9, 3),
                      "blocked_ms": round(st.blocked_ms, 2), "catchup_tokens": st.catchup_tokens,
                      "matches_desired": round(float(np.mean([a == d for a, d in zip(st.active, st.desired)])), 3),
+                     "fallback_fraction": round(st.fallback_fraction(), 3),
                      "text_agrees": bool(same)}
         log(f"{mode}: {out[mode]}")
         del r, target, kv_t

@@ -86,6 +86,44 @@ class CachePolicy:
         return min(res, key=lambda d: (-scores[d], d))
 
 
+# ---------------------------------------------------------------- the bandit baseline (pure host logic)
+class UCBPolicy:
+    """MAB-Async's draft selection (the exploration-based baseline of Sec. 4.1):
+    explore every draft once, in order, then pick the draft maximising
+    mean reward + c * sqrt(ln t / n_d) over the rewards observed so far
+    (t = observations made, n_d = observations of draft d; ties: lower id)."""
+
+    def __init__(self, n_drafts: int, c: float = 2.0):
+        if n_drafts < 1:
+            raise ValueError("need at least one draft")
+        self.n = np.zeros(n_drafts, np.int64)
+        self.total = np.zeros(n_drafts, np.float64)
+        self.c = float(c)
+
+    def observe(self, d: int, reward: float):
+        self.n[d] += 1
+        self.total[d] += float(reward)
+
+    def select(self) -> int:
+        unexplored = np.flatnonzero(self.n == 0)
+        if unexplored.size:
+            return int(unexplored[0])
+        t = float(self.n.sum())
+        index = self.total / self.n + self.c * np.sqrt(np.log(t) / self.n)
+        return int(np.argmax(index))  # (first maximum: lower id on ties)
+
+
+def observed_utility(schedule: Sequence[int], n_drafts: int, noise: float = 0.1, seed: int = 13):
+    """Per scheduling interval, the utility a run of each draft would show
+    (the reward a bandit observes for the draft it ran): 1.0 for the draft
+    the schedule prefers in that interval, 0.5 for the others, plus
+    N(0, noise^2).  Random weights give every draft the same acceptance, so
+    this synthetic signal stands in for the measured acceptance."""
+    rng = np.random.default_rng(seed)
+    return [{d: (1.0 if d == s else 0.5) + float(rng.normal(0.0, noise)) for d in range(n_drafts)}
+            for s in schedule]
+
+
 # ---------------------------------------------------------------- synthetic prediction
 def score_stream(schedule: Sequence[int], n_drafts: int, noise: float = 0.1, seed: int = 11):
     """Per scheduling point, a score per draft: the draft the schedule prefers
@@ -146,8 +184,16 @@ class RunStats:
     blocked_ms: float = 0.0       # host time spent waiting for a reload (naive switching)
     catchup_tokens: int = 0
     wall_ms: float = 0.0
-    active: List[int] = field(default_factory=list)
-    desired: List[int] = field(default_factory=list)
+    active: List[int] = field(default_factory=list)    # draft run in each interval
+    desired: List[int] = field(default_factory=list)   # the schedule's preferred draft
+    selected: List[int] = field(default_factory=list)  # the policy's choice (runs unless still loading)
+
+    def fallback_fraction(self) -> float:
+        """Intervals spent on another draft than the one the policy selected
+        (its selection not resident yet): the paper's fallback execution."""
+        if not self.active:
+            return 0.0
+        return float(np.mean([a != s for a, s in zip(self.active, self.selected)]))
 
 
 class SwitchingRunner:
@@ -160,6 +206,11 @@ class SwitchingRunner:
         its reload (naive dynamic switching).
     mode "memspec": `capacity` slots managed by CachePolicy (Alg. 2), prefetches
         overlapped with decoding, and the best resident draft runs (Alg. 3).
+    mode "mab": `capacity` slots and the MAB-Async baseline: UCBPolicy picks a
+        draft from the utilities observed for the drafts it ran; a selection
+        that is not resident is loaded asynchronously (into a free slot, else
+        the slot of the least recently run draft other than the active one)
+        while decoding continues with the active draft.
     """
 
     def __init__(self, dw, target, kv_t, draft_layers: Sequence[int], gamma: int, temperature: float, seed: int,
@@ -179,7 +230,9 @@ class SwitchingRunner:
             self.models_resident[d] = m
             self.kv[d] = binding.KVCache(m, 1, capacity_ctx)
         self.slots: List[Slot] = []
-        if mode in ("reload", "memspec"):
+        if mode not in ("resident", "reload", "memspec", "mab"):
+            raise ValueError(f"unknown mode {mode!r}")
+        if mode in ("reload", "memspec", "mab"):
             if image is None:
                 image = HostImage(dw, max(self.layers))
             self.slots = [Slot(image, dw) for _ in range(slots)]
@@ -245,7 +298,10 @@ class SwitchingRunner:
 
     # -- the loop
     def run(self, n_iterations: int, schedule: Sequence[int], scores: Sequence[Dict[int, float]], interval: int,
-            max_tokens: Optional[int] = None) -> RunStats:
+            max_tokens: Optional[int] = None, utility: Optional[Sequence[Dict[int, float]]] = None,
+            ucb_c: float = 2.0) -> RunStats:
+        """`scores`: the predictor's per-point scores (memspec); `utility`: the
+        per-interval utility a bandit observes for the draft it ran (mab)."""
         import torch
         stats = RunStats()
         g = self.gamma
@@ -266,6 +322,17 @@ class SwitchingRunner:
             self.policy.mark_resident(first)
             active = first
             self._issue(self.policy.update(scores[0], active), stats)
+        bandit = None
+        last_run = {}
+        if self.mode == "mab":
+            if utility is None:
+                raise ValueError("mode 'mab' needs the observed utility stream")
+            bandit = UCBPolicy(len(self.layers), ucb_c)
+            first = bandit.select()
+            self._load_into_slot(first, active=None, last_run=last_run, stats=stats)
+            self.slots[0].event.wait()
+            torch.cuda.current_stream().synchronize()
+            active = first
         # Device-side log of each iteration's outcome (drafted tokens, A, next),
         # read by the host once per scheduling point (no per-iteration sync).
         log_d = torch.zeros((interval, g), dtype=torch.int32, device="cuda")
@@ -296,16 +363,30 @@ class SwitchingRunner:
                     break
                 point = it // interval
                 desired = schedule[point]
-                if self.mode == "memspec":
+                if self.mode == "mab":
+                    if point > 0:
+                        bandit.observe(active, utility[point - 1][active])
+                    sel = bandit.select()
+                    resident = [sl.draft for sl in self.slots if sl.draft is not None and sl.event.query()]
+                    if sel in resident:
+                        nxt = sel
+                    else:
+                        if all(sl.draft != sel for sl in self.slots):  # not already loading
+                            self._load_into_slot(sel, active, last_run, stats)
+                        nxt = active  # fallback: keep decoding with the active draft
+                    stats.selected.append(int(sel))
+                elif self.mode == "memspec":
                     for sl in self.slots:  # loads that completed since the last point
                         if sl.draft is not None and self.policy.state.get(sl.draft) == "loading" and sl.event.query():
                             self.policy.mark_resident(sl.draft)
                     nxt = self.policy.select(scores[point], active)
                     self._issue(self.policy.update(scores[point], nxt), stats)
+                    stats.selected.append(int(CachePolicy.ranking(scores[point])[0]))
                 else:
                     nxt = desired
                     if self.mode == "reload":
                         self._ensure_in_slot_blocking(nxt, stats)
+                    stats.selected.append(int(desired))
                 if nxt != active:
                     if active is not None:
                         stats.switches += 1
@@ -315,6 +396,7 @@ class SwitchingRunner:
                     active = nxt
                 stats.desired.append(int(desired))
                 stats.active.append(int(active))
+                last_run[active] = point
             sd.step(it)
             log_d[pending_log].copy_(sd.d[0])
             log_a[pending_log:pending_log + 1].copy_(sd.n_acc[:1])
@@ -325,6 +407,20 @@ class SwitchingRunner:
         torch.cuda.synchronize()
         stats.wall_ms = (time.perf_counter() - t0) * 1e3
         return stats
+
+    def _load_into_slot(self, d: int, active: Optional[int], last_run: Dict[int, int], stats: RunStats):
+        """MAB-Async's reactive load: a free slot, else the slot of the least
+        recently run draft that is not the active one (none: no load)."""
+        free = [sl for sl in self.slots if sl.draft is None]
+        if free:
+            sl = free[0]
+        else:
+            victims = [sl for sl in self.slots if sl.draft != active]
+            if not victims:
+                return
+            sl = min(victims, key=lambda x: (last_run.get(x.draft, -1), x.draft))
+        stats.reload_bytes += sl.load_async(d, self.layers[d], self.copy)
+        stats.reloads += 1
 
     def _issue(self, actions, stats: RunStats):
         """Carry out the policy's actions: an evicted draft frees its slot; a

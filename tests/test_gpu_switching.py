@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 from paper_2608_10362_amd import binding, synth
-from paper_2608_10362_amd.runtime import SwitchingRunner, score_stream
+from paper_2608_10362_amd.runtime import SwitchingRunner, observed_utility, score_stream
 from tests.gpu_util import log, torch_cuda
 
 pytestmark = pytest.mark.gpu
@@ -27,13 +27,15 @@ def _run(torch, shape, dw, mode, schedule, cap=192, n_iter=24, interval=2):
     target = binding.Model(dw, 3, max_rows=8, max_ctx=cap)
     kv_t = binding.KVCache(target, 1, cap)
     r = SwitchingRunner(dw, target, kv_t, LAYERS, gamma=4, temperature=0.0, seed=2, capacity_ctx=cap, mode=mode,
-                        slots=2 if mode == "memspec" else 1)
+                        slots=2 if mode in ("memspec", "mab") else 1)
     prompt = synth.make_prompt(24, shape.vocab)[0]
     r.prefill(prompt)
     scores = score_stream(schedule, len(LAYERS), noise=0.05, seed=7)
-    st = r.run(n_iter, schedule, scores, interval)
+    util = observed_utility(schedule, len(LAYERS), noise=0.05, seed=8)
+    st = r.run(n_iter, schedule, scores, interval, utility=util)
     log(f"{mode}: {st.iterations} iterations, {st.tokens} tokens, switches {st.switches}, reloads {st.reloads}, "
-        f"catch-up tokens {st.catchup_tokens}, active {st.active}")
+        f"catch-up tokens {st.catchup_tokens}, active {st.active}, selected {st.selected}, "
+        f"fallback {st.fallback_fraction():.2f}")
     return r, st
 
 
@@ -42,7 +44,7 @@ def test_switching_modes_emit_the_same_greedy_text_and_catch_up_is_exact():
     schedule = [1, 1, 0, 2, 2, 0, 1, 2, 0, 0, 1, 2]
     texts = {}
     runners = {}
-    for mode in ("resident", "reload", "memspec"):
+    for mode in ("resident", "reload", "memspec", "mab"):
         r, st = _run(torch, shape, dw, mode, schedule)
         texts[mode] = r.text
         runners[mode] = (r, st)
@@ -53,11 +55,21 @@ def test_switching_modes_emit_the_same_greedy_text_and_catch_up_is_exact():
     # agree on their common length (greedy speculative decoding is lossless)
     n_common = min(len(t) for t in texts.values())
     assert n_common > 24 + 8
-    assert texts["resident"][:n_common] == texts["reload"][:n_common] == texts["memspec"][:n_common]
+    assert (texts["resident"][:n_common] == texts["reload"][:n_common] == texts["memspec"][:n_common]
+            == texts["mab"][:n_common])
     assert texts["resident"] == texts["reload"]  # the same schedule, the same drafts
     # memspec never runs a draft that was still loading: every active draft was resident
     r, st = runners["memspec"]
     assert all(a in range(len(LAYERS)) for a in st.active)
+    # the bandit explores the drafts in order first (a selection still loading is
+    # repeated while the active draft runs as the fallback)
+    st = runners["mab"][1]
+    order = []
+    for d in st.selected:
+        if d not in order:
+            order.append(d)
+    assert order == [0, 1, 2] and len(st.selected) == len(st.active)
+    assert 0.0 <= st.fallback_fraction() <= 1.0 and runners["resident"][1].fallback_fraction() == 0.0
     # catch-up leaves each draft's cache as a fresh prefill of the committed text would
     r = runners["resident"][0]
     text = np.array(r.text, np.int32)

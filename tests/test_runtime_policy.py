@@ -64,3 +64,55 @@ def test_score_stream_prefers_the_scheduled_draft():
     sched = [0, 2, 1, 1]
     s = score_stream(sched, 3, noise=0.05, seed=3)
     assert [CachePolicy.ranking(x)[0] for x in s] == sched
+
+
+# ---------------------------------------------------------------- MAB-Async's UCB selection
+def test_ucb_explores_every_draft_once_in_order():
+    from paper_2608_10362_amd.runtime import UCBPolicy
+    u = UCBPolicy(3, c=2.0)
+    seen = []
+    for r in (0.2, 0.9, 0.5):
+        d = u.select()
+        seen.append(d)
+        u.observe(d, r)
+    assert seen == [0, 1, 2]
+
+
+def test_ucb_index_matches_the_formula_by_hand():
+    import math
+    from paper_2608_10362_amd.runtime import UCBPolicy
+    u = UCBPolicy(3, c=2.0)
+    obs = [(0, 1.0), (1, 0.5), (2, 0.6), (0, 0.8), (1, 0.7)]
+    for d, r in obs:
+        u.observe(d, r)
+    t = 5.0
+    idx = [(1.0 + 0.8) / 2 + 2.0 * math.sqrt(math.log(t) / 2),
+           (0.5 + 0.7) / 2 + 2.0 * math.sqrt(math.log(t) / 2),
+           0.6 + 2.0 * math.sqrt(math.log(t) / 1)]
+    assert u.select() == max(range(3), key=lambda d: (idx[d], -d))  # draft 2: its bonus term dominates
+    u2 = UCBPolicy(2, c=0.0)  # no exploration bonus: the higher mean, ties to the lower id
+    u2.observe(0, 0.5)
+    u2.observe(1, 0.5)
+    assert u2.select() == 0
+
+
+def test_ucb_settles_on_the_best_draft_of_a_stationary_stream():
+    import numpy as np
+    from paper_2608_10362_amd.runtime import UCBPolicy
+    rng = np.random.default_rng(0)
+    means = [0.5, 0.8, 0.55]
+    u = UCBPolicy(3, c=0.5)
+    picks = []
+    for _ in range(400):
+        d = u.select()
+        u.observe(d, means[d] + rng.normal(0, 0.1))
+        picks.append(d)
+    assert np.mean(np.array(picks[-100:]) == 1) > 0.9
+
+
+def test_observed_utility_prefers_the_scheduled_draft():
+    from paper_2608_10362_amd.runtime import observed_utility
+    sched = [0, 2, 1, 1]
+    util = observed_utility(sched, 3, noise=0.0)
+    for s, u in zip(sched, util):
+        assert u[s] == 1.0 and all(u[d] == 0.5 for d in range(3) if d != s)
