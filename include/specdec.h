@@ -188,8 +188,10 @@ SPECDEC_API specdec_status specdec_kv_read_state(specdec_kv* kv, int32_t* len, i
                                      int32_t* status, void* stream);
 
 /* Commit a prompt: run the model over tokens[b, 0..n-2] (device int32 [batch, n])
- * in chunks, appending their K/V from position len[b], then len[b] += n-1 and
- * the pending token becomes tokens[b, n-1].  Not on the timed path (the paper
+ * in chunks of max_rows / batch tokens per sequence (float32 models: at most
+ * 64), appending their K/V from position len[b], then len[b] += n-1 and the
+ * pending token becomes tokens[b, n-1].  Also the catch-up forward of a draft
+ * that missed committed tokens.  Not on the timed verify path (the paper
  * excludes prompt encoding from throughput, Sec. 4.1). */
 SPECDEC_API specdec_status specdec_prefill(const specdec_model* model, specdec_kv* kv, int32_t n, const int32_t* tokens,
                                void* stream);

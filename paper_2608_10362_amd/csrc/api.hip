@@ -595,7 +595,10 @@ specdec_status specdec_prefill(const specdec_model* model, specdec_kv* kv, int32
   const int B = kv->batch;
   if (kv->len_upper + n - 1 > kv->capacity) return SPECDEC_ERR_KV_CAPACITY;
   hipStream_t s = (hipStream_t)stream;
-  const int C = std::max(1, std::min(model->max_rows / B, 64));
+  // Chunks of as many tokens per sequence as the handle's rows allow (bf16: passes
+  // of more than 64 rows run the wide GEMM; float32 models keep 64-row chunks).
+  const int per = model->max_rows / B;
+  const int C = std::max(1, model->desc.dtype == SPECDEC_BF16 ? per : std::min(per, 64));
   if (model->max_rows < B) return SPECDEC_ERR_SHAPE;
   for (int c0 = 0; c0 < n - 1; c0 += C) {
     const int rps = std::min(C, n - 1 - c0);

@@ -243,9 +243,13 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     // V fragments.  Row descriptors and Q go through range-checked buffer loads.
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0,
                                                                          a.M * (int)sizeof(RowDesc), 0x00020000);
-    // (only the two fields used: a wider load leaves dead destination registers
-    // the allocator reuses, which forces a wait for the load)
-    const uint32_t roff = ((uint32_t)(r0 + lane) * (uint32_t)sizeof(RowDesc)) | ((uint32_t)(lane >= rps) << 31);
+    // Lane l < 16 holds the descriptor of the row of query l of the tile
+    // (queries qa = mt*16 + l; rows r0 + qa / group).  (Only the two fields
+    // used: a wider load leaves dead destination registers the allocator
+    // reuses, which forces a wait for the load.)
+    const int ql = mt * 16 + lane;
+    const uint32_t roff = ((uint32_t)(r0 + min(ql, nq - 1) / group) * (uint32_t)sizeof(RowDesc)) |
+                          ((uint32_t)(lane >= 16 || ql >= nq) << 31);
     const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
     const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
     // K fragments of a sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity);
@@ -284,18 +288,15 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     // (compiler barrier: keeps what follows from being hoisted above the loads)
     asm volatile("" ::: "memory");
 
-    // nk = max(pos) + 1 over the sequence's valid rows.
-    const int mypos = (lane < rps && rd_valid) ? rd_pos : -1;
+    // nk = max(pos) + 1 over the tile's valid query rows: no key past it is read.
+    const int mypos = (lane < 16 && ql < nq && rd_valid) ? rd_pos : -1;
     int nk = mypos + 1;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
+    for (int o = 8; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
+    nk = __shfl(nk, 0, kWave);
     // positions of the 4 query rows this lane holds in the C layout (-1: none)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qc = mt * 16 + 4 * grp + r;
-      const int p = __shfl(mypos, min(qc, nq - 1) / group, kWave);
-      qpos[r] = qc < nq ? p : -1;
-    }
+    for (int r = 0; r < 4; ++r) qpos[r] = __shfl(mypos, 4 * grp + r, kWave);
     const float scale = 1.0f / sqrtf((float)HD);
     bf16x8 qhi[KST], qlo[KST];
 #pragma unroll

@@ -219,7 +219,7 @@ class SwitchingRunner:
         self.dw, self.target, self.kv_t = dw, target, kv_t
         self.layers = list(draft_layers)
         self.gamma, self.T, self.seed, self.mode = gamma, temperature, seed, mode
-        self.rows = max(2, gamma + 1)
+        self.rows = max(64, gamma + 1)  # (draft handles: catch-up forwards in chunks of up to 64 tokens)
         self.cap = capacity_ctx
         self.copy = torch.cuda.Stream()
         # per draft: its own KV cache (layer count of the draft)

@@ -229,6 +229,44 @@ def test_bf16_1b_shape_wide_rows(B, g):
     _bf16_case(synth.LLAMA_1B, 2, list(lengths), g=g, seed=3)
 
 
+# ---------------------------------------------------------------- prefill in large chunks
+@pytest.mark.parametrize("shape_name,B,rows,n", [("LLAMA_1B", 2, 256, 301), ("LLAMA_7B", 1, 256, 301)])
+def test_bf16_prefill_in_large_chunks(shape_name, B, rows, n):
+    """Prefill of n-1 prompt tokens per sequence in chunks of rows/B tokens
+    (1.1B: 128-token chunks of 2 sequences = 256-row passes in two wide launches,
+    GQA with 64 query tiles per kv head; 7B: 256-token chunks, MHA), then a
+    verify: the caches and the verify logits against the oracle's prefill."""
+    torch = torch_cuda()
+    shape = getattr(synth, shape_name)
+    L, g = 2, 4
+    cap = 384
+    W = synth.make_weights(shape, n_layers=L)
+    dw = binding.DeviceWeights(shape, W)
+    target = binding.Model(dw, L, max_rows=rows, max_ctx=cap)
+    kv = binding.KVCache(target, B, cap)
+    prompts = synth.make_prompt(n, shape.vocab, batch=B, seed=41)
+    drafts = synth.make_prompt(g, shape.vocab, batch=B, seed=42)
+    binding.specdec_prefill(target, kv, i32(prompts))
+    st = kv.read_state()
+    assert (st["len"] == n - 1).all() and (st["pending"][:, 1] == prompts[:, -1]).all() and st["status"] == 0
+    logits = torch.empty((B, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv, g, i32(drafts), g, logits)
+    got = logits.cpu().numpy()
+    m = om.Model(shape, W, n_layers=L)
+    worst, worst_kv = 0.0, 0.0
+    for b in range(B):
+        c = om.KVCache(shape, L, cap)
+        m.prefill(prompts[b, :-1], c)
+        ref = m.forward_block([prompts[b, -1]] + list(drafts[b]), c.length, c)
+        worst = max(worst, float(np.abs(got[b] - ref).max()))
+        for layer in range(L):
+            k, v = kv.read_context(layer, b, 0, n - 1)
+            worst_kv = max(worst_kv, float(np.abs(k.float().cpu().numpy() - c.k[layer][:n - 1]).max()),
+                           float(np.abs(v.float().cpu().numpy() - c.v[layer][:n - 1]).max()))
+    log(f"{shape_name} prefill B={B} chunk {rows // B}: verify max-abs logit error {worst:.3g}, K/V {worst_kv:.3g}")
+    assert worst < TOL_BF16 and worst_kv < 0.05
+
+
 # ---------------------------------------------------------------- context copy and errors
 def test_kv_context_roundtrip_is_exact(tiny):
     torch = torch_cuda()
