@@ -56,7 +56,10 @@ def round_to_bf16(x: np.ndarray) -> np.ndarray:
 
 
 def weight_f64(arr: np.ndarray, dtype: str) -> np.ndarray:
-    """A stored weight tensor (float32 array or bf16 bits) as float64."""
+    """A stored weight tensor (float32 array or bf16 bits) as float64; float64
+    arrays (effective weights of a quantized model, quant.py) are used as given."""
+    if isinstance(arr, np.ndarray) and arr.dtype == np.float64:
+        return arr
     if dtype == "bf16":
         return bf16_bits_to_f64(arr)
     return np.asarray(arr, dtype=np.float32).astype(np.float64)
