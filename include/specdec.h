@@ -62,6 +62,12 @@ typedef enum {
 } specdec_status;
 
 enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1 };
+/* Weight image formats of bf16 models (activations, KV and the LM head stay
+ * bf16 in both): BF16 stores every matrix in bf16; INT4 stores the layer
+ * matrices as 4-bit codes with one bf16 scale per row and group of 128
+ * input columns (the paper's models are INT4, Sec. 4.1; round-to-nearest
+ * groups stand in for GPTQ, which needs calibration data). */
+enum { SPECDEC_WEIGHTS_BF16 = 0, SPECDEC_WEIGHTS_INT4 = 1 };
 enum { SPECDEC_ROLE_TARGET = 0, SPECDEC_ROLE_DRAFT = 1 };
 enum { SPECDEC_INPUT_PROBS = 0, SPECDEC_INPUT_LOGITS = 1 };
 /* Philox counter purposes (see specdec_draw_u32). */
@@ -140,6 +146,25 @@ SPECDEC_API specdec_status specdec_pack_weights(const specdec_model_desc* desc, 
                                                 int32_t n_layers_used, void* packed, size_t packed_bytes,
                                                 void* stream);
 
+/* The same in a chosen weight format (SPECDEC_WEIGHTS_*).  INT4 image: the
+ * LM head as in the bf16 image, then per layer the seven matrices, each as
+ * INT4 code fragments followed by its scales (256-byte aligned):
+ *  - codes: 16-row x 32-column fragments of 256 bytes, fragment (t, s) at
+ *    byte 256*(t*K/32 + s); lane l = 16*g + i holds the 8 codes of row
+ *    16t + i, columns 32s + 8g .. +7, as one 32-bit word, code j in bits
+ *    4j..4j+3 (two's complement, -8..7);
+ *  - scales: bf16 [N/16][ceil(K/128)][16] (tile, group, row in tile).
+ * Quantization (on the device, from the bf16 matrices): per row and group of
+ * 128 columns, s = bf16(max|w| / 7) (float32 division, then rounding to
+ * nearest even), q = clamp(rint(w / s), -8, 7) (float32; q = 0 where s = 0).
+ * The model then computes with the effective weights q * s exactly.
+ * Requires K % 32 == 0 for every layer matrix.  Errors as specdec_pack_weights,
+ * INVALID_ARG for an unknown format. */
+SPECDEC_API size_t specdec_packed_bytes_fmt(const specdec_model_desc* desc, int32_t n_layers_used, int32_t format);
+SPECDEC_API specdec_status specdec_pack_weights_fmt(const specdec_model_desc* desc, const specdec_weights* weights,
+                                                    int32_t n_layers_used, int32_t format, void* packed,
+                                                    size_t packed_bytes, void* stream);
+
 /* Create a handle over caller-owned weights.  n_layers_used <= desc->n_layers
  * selects a layer prefix (a draft).  bf16 models take their matrices from
  * `packed` (an image written by specdec_pack_weights covering at least
@@ -154,6 +179,13 @@ SPECDEC_API specdec_status specdec_model_create(const specdec_model_desc* desc, 
                                     int32_t n_layers_used, const void* packed, size_t packed_bytes,
                                     int32_t max_rows, int32_t max_ctx,
                                     void* workspace, size_t workspace_bytes, specdec_model** out);
+/* The same over an image of a chosen weight format.  INT4 handles run passes
+ * of at most 64 rows (max_rows <= 64: verify and draft steps, prefill in
+ * 64-row chunks); UNSUPPORTED otherwise or for float32 models. */
+SPECDEC_API specdec_status specdec_model_create_fmt(const specdec_model_desc* desc, const specdec_weights* weights,
+                                                    int32_t n_layers_used, int32_t format, const void* packed,
+                                                    size_t packed_bytes, int32_t max_rows, int32_t max_ctx,
+                                                    void* workspace, size_t workspace_bytes, specdec_model** out);
 SPECDEC_API void specdec_model_destroy(specdec_model* model);
 
 /* Bytes of KV storage for `batch` sequences of `capacity` positions over the

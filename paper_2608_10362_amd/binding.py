@@ -61,6 +61,13 @@ _lib = None
 _SIGS = {
     "specdec_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32, ctypes.c_int32]),
     "specdec_packed_bytes": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32]),
+    "specdec_packed_bytes_fmt": (ctypes.c_size_t, [ctypes.POINTER(ModelDesc), ctypes.c_int32, ctypes.c_int32]),
+    "specdec_pack_weights_fmt": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
+                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "specdec_model_create_fmt": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
+                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32,
+                                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t,
+                                                ctypes.POINTER(ctypes.c_void_p)]),
     "specdec_pack_weights": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
                                             ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "specdec_model_create": (ctypes.c_int, [ctypes.POINTER(ModelDesc), ctypes.POINTER(Weights), ctypes.c_int32,
@@ -206,22 +213,31 @@ class DeviceWeights:
     KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
     MATS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
-    def __init__(self, shape, weights: Dict, device="cuda", keep_rowmajor: bool = False, stream=None):
+    FORMATS = {"bf16": 0, "int4": 1}  # SPECDEC_WEIGHTS_*
+
+    def __init__(self, shape, weights: Dict, device="cuda", keep_rowmajor: bool = False, stream=None,
+                 weight_format: str = "bf16"):
+        """``weight_format`` (bf16 models): "bf16", or "int4" for the INT4 image
+        (layer matrices quantized on the device, see specdec_pack_weights_fmt)."""
         import torch
+        if weight_format not in self.FORMATS or (weight_format != "bf16" and shape.dtype != "bf16"):
+            raise ValueError(f"weight format {weight_format!r} for a {shape.dtype} model")
+        self.weight_format = weight_format
         self.shape = shape
         self.t = {k: _to_device(weights[k], shape.dtype, device) for k in ("embed", "lm_head", "final_norm")}
         self.layers = [{k: _to_device(L[k], shape.dtype, device) for k in self.KEYS} for L in weights["layers"]]
         self.packed = None
         if shape.dtype == "bf16":
             desc = make_desc(shape.with_layers(self.n_layers))
-            nbytes = lib().specdec_packed_bytes(ctypes.byref(desc), self.n_layers)
+            fmt = self.FORMATS[weight_format]
+            nbytes = lib().specdec_packed_bytes_fmt(ctypes.byref(desc), self.n_layers, fmt)
             if nbytes == 0:
-                raise SpecdecError(-2, "specdec_packed_bytes")
+                raise SpecdecError(-2, "specdec_packed_bytes_fmt")
             self.packed = torch.empty(nbytes, dtype=torch.uint8, device=self.t["embed"].device)
             w, keep = self.c_struct(self.n_layers)
-            _check(lib().specdec_pack_weights(ctypes.byref(desc), ctypes.byref(w), self.n_layers,
-                                              self.packed.data_ptr(), nbytes, _stream(stream)),
-                   "specdec_pack_weights")
+            _check(lib().specdec_pack_weights_fmt(ctypes.byref(desc), ctypes.byref(w), self.n_layers, fmt,
+                                                  self.packed.data_ptr(), nbytes, _stream(stream)),
+                   "specdec_pack_weights_fmt")
             torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
             if not keep_rowmajor:
                 self.t["lm_head"] = None
@@ -264,10 +280,11 @@ class Model:
         if packed is not None:
             _dev(packed, "packed", torch.uint8, 1)
         self._packed = pk  # (kept alive with the handle)
-        _check(lib().specdec_model_create(ctypes.byref(self.desc), ctypes.byref(w), n_layers, _ptr(pk),
-                                          0 if pk is None else pk.numel(), max_rows, max_ctx,
-                                          self.workspace.data_ptr(), nbytes, ctypes.byref(h)),
-               "specdec_model_create")
+        _check(lib().specdec_model_create_fmt(ctypes.byref(self.desc), ctypes.byref(w), n_layers,
+                                              DeviceWeights.FORMATS[dw.weight_format], _ptr(pk),
+                                              0 if pk is None else pk.numel(), max_rows, max_ctx,
+                                              self.workspace.data_ptr(), nbytes, ctypes.byref(h)),
+               "specdec_model_create_fmt")
         self.handle = h
 
     def __del__(self):

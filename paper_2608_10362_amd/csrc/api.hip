@@ -19,6 +19,8 @@ struct specdec_model {
   const void* lm_head;
   const void* final_norm;
   std::vector<const void*> attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up, w_down;
+  int wfmt = SPECDEC_WEIGHTS_BF16;  // SPECDEC_WEIGHTS_INT4: the layer matrices above are INT4 code images
+  std::vector<const uint16_t*> sq, sk, sv, so, sg, su, sd;  // ... and these their group scales
   // workspace carve
   RowDesc* rows;
   float* rope_cs;
@@ -145,6 +147,7 @@ specdec_status hip_status(hipError_t e) { return e == hipSuccess ? SPECDEC_OK : 
 struct PackedMat {
   int N, K;
   size_t off;
+  size_t soff = 0;  // INT4 matrices: byte offset of the group scales
 };
 size_t image_layout(const specdec_model_desc* d, int n_layers, std::vector<PackedMat>* mats) {
   const int q = d->n_heads * d->head_dim, kv = d->n_kv_heads * d->head_dim;
@@ -164,6 +167,36 @@ size_t image_layout(const specdec_model_desc* d, int n_layers, std::vector<Packe
     add(d->d_model, d->ffn_dim);
   }
   return off;
+}
+
+// INT4 image: the LM head in bf16 (as above), then per layer the same seven
+// matrices as INT4 code fragments followed by their group scales.
+size_t image_layout_int4(const specdec_model_desc* d, int n_layers, std::vector<PackedMat>* mats) {
+  const int q = d->n_heads * d->head_dim, kv = d->n_kv_heads * d->head_dim;
+  size_t off = 0;
+  if (mats) mats->push_back(PackedMat{d->vocab, d->d_model, off});
+  off = align_up(off + packed_elems(d->vocab, d->d_model) * 2);
+  auto add = [&](int N, int K) {
+    PackedMat m{N, K, off};
+    off = align_up(off + packed_int4_frag_bytes(N, K));
+    m.soff = off;
+    off = align_up(off + packed_int4_scale_bytes(N, K));
+    if (mats) mats->push_back(m);
+  };
+  for (int l = 0; l < n_layers; ++l) {
+    add(q, d->d_model);
+    add(kv, d->d_model);
+    add(kv, d->d_model);
+    add(d->d_model, q);
+    add(d->ffn_dim, d->d_model);
+    add(d->ffn_dim, d->d_model);
+    add(d->d_model, d->ffn_dim);
+  }
+  return off;
+}
+
+size_t image_bytes(const specdec_model_desc* d, int n_layers, int fmt, std::vector<PackedMat>* mats) {
+  return fmt == SPECDEC_WEIGHTS_INT4 ? image_layout_int4(d, n_layers, mats) : image_layout(d, n_layers, mats);
 }
 
 #define SD_TRY(expr)                                   \
@@ -292,6 +325,8 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       q.rows = m->rows; q.rope_cs = m->rope_cs; q.qr = m->qr; q.kv = kv_layout(kv); q.layer = l;
       q.n_heads = H; q.n_kv_heads = G; q.head_dim = hd;
     }
+    const bool q4 = m->wfmt == SPECDEC_WEIGHTS_INT4;
+    if (q4) { q.q4 = 1; q.wscale[0] = m->sq[l]; q.wscale[1] = m->sk[l]; q.wscale[2] = m->sv[l]; }
     {
       Timed t(SPECDEC_KERNEL_QKV, s);
       SD_TRY(gemm_rows(dt, q, M, s));
@@ -317,6 +352,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     o.x = m->o; o.ldx = H * hd; o.K = H * hd;
     o.w[0] = m->wo[l]; o.n_seg[0] = d.d_model; o.n_rows = d.d_model; o.kind = EPI_RESID;
     o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss; o.xg_out = m->xg; o.gain_out = m->ffn_norm[l];
+    if (q4) { o.q4 = 1; o.wscale[0] = m->so[l]; }
     {
       Timed t(SPECDEC_KERNEL_O_PROJ, s);
       SD_TRY(gemm_rows(dt, o, M, s));
@@ -329,6 +365,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     gu.K = d.d_model;
     gu.w[0] = m->w_gate[l]; gu.w[1] = m->w_up[l]; gu.n_seg[0] = d.ffn_dim; gu.n_seg[1] = d.ffn_dim;
     gu.n_rows = d.ffn_dim; gu.kind = EPI_SWIGLU; gu.out = m->u; gu.ldo = d.ffn_dim;
+    if (q4) { gu.q4 = 1; gu.wscale[0] = m->sg[l]; gu.wscale[1] = m->su[l]; }
     {
       Timed t(SPECDEC_KERNEL_GATE_UP, s);
       SD_TRY(gemm_rows(dt, gu, M, s));
@@ -340,6 +377,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     dn.w[0] = m->w_down[l]; dn.n_seg[0] = d.d_model; dn.n_rows = d.d_model; dn.kind = EPI_RESID;
     dn.out = m->h; dn.ldo = d.d_model; dn.ss_out = m->ss; dn.xg_out = m->xg;
     dn.gain_out = l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm;
+    if (q4) { dn.q4 = 1; dn.wscale[0] = m->sd[l]; }
     {
       Timed t(SPECDEC_KERNEL_DOWN, s);
       SD_TRY(gemm_rows(dt, dn, M, s));
@@ -378,21 +416,28 @@ size_t specdec_workspace_bytes(const specdec_model_desc* desc, int32_t max_rows,
   return ws_layout(desc, max_rows, max_ctx).total;
 }
 
-size_t specdec_packed_bytes(const specdec_model_desc* desc, int32_t n_layers_used) {
+size_t specdec_packed_bytes_fmt(const specdec_model_desc* desc, int32_t n_layers_used, int32_t format) {
   if (check_desc(desc) != SPECDEC_OK || n_layers_used <= 0 || n_layers_used > desc->n_layers) return 0;
   if (desc->dtype != SPECDEC_BF16) return 0;
-  return image_layout(desc, n_layers_used, nullptr);
+  if (format != SPECDEC_WEIGHTS_BF16 && format != SPECDEC_WEIGHTS_INT4) return 0;
+  return image_bytes(desc, n_layers_used, format, nullptr);
 }
 
-specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
-                                    void* packed, size_t packed_bytes, void* stream) {
+size_t specdec_packed_bytes(const specdec_model_desc* desc, int32_t n_layers_used) {
+  return specdec_packed_bytes_fmt(desc, n_layers_used, SPECDEC_WEIGHTS_BF16);
+}
+
+specdec_status specdec_pack_weights_fmt(const specdec_model_desc* desc, const specdec_weights* w,
+                                        int32_t n_layers_used, int32_t format, void* packed, size_t packed_bytes,
+                                        void* stream) {
   specdec_status st = check_desc(desc);
   if (st != SPECDEC_OK) return st;
   if (desc->dtype != SPECDEC_BF16) return SPECDEC_ERR_UNSUPPORTED;
+  if (format != SPECDEC_WEIGHTS_BF16 && format != SPECDEC_WEIGHTS_INT4) return SPECDEC_ERR_INVALID_ARG;
   if (!w || !packed || n_layers_used <= 0 || n_layers_used > desc->n_layers) return SPECDEC_ERR_INVALID_ARG;
   if ((uintptr_t)packed % kAlign) return SPECDEC_ERR_INVALID_ARG;
   std::vector<PackedMat> mats;
-  if (packed_bytes < image_layout(desc, n_layers_used, &mats)) return SPECDEC_ERR_INVALID_ARG;
+  if (packed_bytes < image_bytes(desc, n_layers_used, format, &mats)) return SPECDEC_ERR_INVALID_ARG;
   if (!w->lm_head || !w->wq || !w->wk || !w->wv || !w->wo || !w->w_gate || !w->w_up || !w->w_down)
     return SPECDEC_ERR_INVALID_ARG;
   std::vector<const void*> src;
@@ -409,14 +454,31 @@ specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specde
     // Wq and Wk (matrices 1 and 2 of each layer's seven) carry the RoPE pair order
     const int in_layer = i == 0 ? -1 : (int)((i - 1) % 7);
     const int rope_hd = in_layer == 0 || in_layer == 1 ? desc->head_dim : 0;
-    SD_TRY(launch_pack(src[i], (char*)packed + mats[i].off, mats[i].N, mats[i].K, rope_hd, s));
+    if (format == SPECDEC_WEIGHTS_INT4 && i > 0)
+      SD_TRY(launch_pack_int4(src[i], (char*)packed + mats[i].off, (char*)packed + mats[i].soff, mats[i].N, mats[i].K,
+                              rope_hd, s));
+    else
+      SD_TRY(launch_pack(src[i], (char*)packed + mats[i].off, mats[i].N, mats[i].K, rope_hd, s));
   }
   return SPECDEC_OK;
+}
+
+specdec_status specdec_pack_weights(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
+                                    void* packed, size_t packed_bytes, void* stream) {
+  return specdec_pack_weights_fmt(desc, w, n_layers_used, SPECDEC_WEIGHTS_BF16, packed, packed_bytes, stream);
 }
 
 specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* w, int32_t n_layers_used,
                                     const void* packed, size_t packed_bytes, int32_t max_rows, int32_t max_ctx,
                                     void* workspace, size_t workspace_bytes, specdec_model** out) {
+  return specdec_model_create_fmt(desc, w, n_layers_used, SPECDEC_WEIGHTS_BF16, packed, packed_bytes, max_rows,
+                                  max_ctx, workspace, workspace_bytes, out);
+}
+
+specdec_status specdec_model_create_fmt(const specdec_model_desc* desc, const specdec_weights* w,
+                                        int32_t n_layers_used, int32_t format, const void* packed,
+                                        size_t packed_bytes, int32_t max_rows, int32_t max_ctx, void* workspace,
+                                        size_t workspace_bytes, specdec_model** out) {
   if (!out) return SPECDEC_ERR_INVALID_ARG;
   *out = nullptr;
   specdec_status st = check_desc(desc);
@@ -429,10 +491,13 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
   const WsLayout L = ws_layout(desc, max_rows, max_ctx);
   if (workspace_bytes < L.total) return SPECDEC_ERR_INVALID_ARG;
   const bool bf16 = desc->dtype == SPECDEC_BF16;
+  if (format != SPECDEC_WEIGHTS_BF16 && format != SPECDEC_WEIGHTS_INT4) return SPECDEC_ERR_INVALID_ARG;
+  // INT4 layer weights run the skinny GEMMs only: passes of at most 64 rows
+  if (format == SPECDEC_WEIGHTS_INT4 && (!bf16 || max_rows > kMaxGemmRows)) return SPECDEC_ERR_UNSUPPORTED;
   std::vector<PackedMat> mats;
   if (bf16) {
     if (!packed || (uintptr_t)packed % kAlign) return SPECDEC_ERR_INVALID_ARG;
-    if (packed_bytes < image_layout(desc, n_layers_used, &mats)) return SPECDEC_ERR_INVALID_ARG;
+    if (packed_bytes < image_bytes(desc, n_layers_used, format, &mats)) return SPECDEC_ERR_INVALID_ARG;
   } else if (packed) {
     return SPECDEC_ERR_INVALID_ARG;
   }
@@ -467,7 +532,13 @@ specdec_status specdec_model_create(const specdec_model_desc* desc, const specde
       m->w_gate.push_back(img + p[4].off);
       m->w_up.push_back(img + p[5].off);
       m->w_down.push_back(img + p[6].off);
+      if (format == SPECDEC_WEIGHTS_INT4) {
+        auto sc = [&](int j) { return (const uint16_t*)(img + p[j].soff); };
+        m->sq.push_back(sc(0)); m->sk.push_back(sc(1)); m->sv.push_back(sc(2)); m->so.push_back(sc(3));
+        m->sg.push_back(sc(4)); m->su.push_back(sc(5)); m->sd.push_back(sc(6));
+      }
     }
+    m->wfmt = format;
   } else {
     m->lm_head = w->lm_head;
     m->wq.assign(w->wq, w->wq + n_layers_used);

@@ -12,6 +12,7 @@
 // free because the pass is bandwidth-bound (about M flops per weight byte).
 // float32 weights (the tiny configuration) run on a plain vector kernel.
 #include <algorithm>
+#include <type_traits>
 
 #include "device_common.h"
 #include "internal.h"
@@ -139,6 +140,34 @@ __device__ __forceinline__ const uint16_t* weight_tile(const GemmArgs& a, int ki
   return (const uint16_t*)a.w[seg] + (size_t)(n / 16) * KS * 512;
 }
 
+// Segment and local row of row tile t of block blk (as weight_tile).
+__device__ __forceinline__ void tile_segment(const GemmArgs& a, int kind, int blk, int NC, int t, int& seg, int& n,
+                                             bool& ok) {
+  if (kind == EPI_SWIGLU) {
+    const int H = NC / 2;
+    seg = 16 * t >= H;
+    n = blk * H + 16 * t - seg * H;
+    ok = n < a.n_rows;
+    if (!ok) n = 0;
+  } else {
+    n = blk * NC + 16 * t;
+    ok = n < a.n_rows;
+    if (!ok) n = 0;
+    const int b1 = a.n_seg[0], b2 = b1 + a.n_seg[1];
+    seg = n < b1 ? 0 : (n < b2 ? 1 : 2);
+    n -= seg == 0 ? 0 : (seg == 1 ? b1 : b2);
+  }
+}
+
+// INT4 image of W [N, K]: 256-byte fragments (16 rows x 32 columns; lane
+// 16*(k%32/8) + n%16 holds the 8 codes of row n at columns 8*(k%32/8)..+7,
+// low nibble first), tile-major like the bf16 image, then the group scales
+// [N/16][KG][16] (bf16, groups of 128 columns).
+struct Q4Frag {
+  uint32_t codes;
+  uint32_t scale;  // bf16 bits of the group scale of the lane's row (lane % 16)
+};
+
 // ---------------------------------------------------------------- MFMA kernel (bf16 weights)
 // Persistent: one 16-wave block per CU loops over row tiles of NC = 16*T
 // weight rows (tile = blockIdx.x + i*gridDim.x).  Within a tile, wave w
@@ -149,8 +178,12 @@ __device__ __forceinline__ const uint16_t* weight_tile(const GemmArgs& a, int ki
 // MFMA operand layout (16x16x32): lane l holds A[l%16][8(l/16)+j] (x rows),
 // B[8(l/16)+j][l%16] (= W[n0 + l%16][k0 + 8(l/16) + j]: 16 bytes at lane*16 of
 // the packed 1 KB fragment), D[4(l/16)+r][l%16].
-template <int T, int MT, int UB, bool PIPE, int KIND>
+template <int T, int MT, int UB, bool PIPE, int KIND, bool Q4 = false>
 __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n_tiles) {
+  // Q4: INT4 weights (Q4Frag).  The MFMA takes the codes as bf16 (small
+  // integers, exact) and each k-step's product is multiplied by the lane's
+  // row scale in float32, so the effective weights are exactly code * scale.
+  using WReg = std::conditional_t<Q4, Q4Frag, u32x4>;
   constexpr int NC = 16 * T;
   constexpr int MP = 16 * MT;
   constexpr int NF = T * MT;              // accumulator fragments per wave
@@ -190,7 +223,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 wA[UB][T], wB[UB][T];
+  WReg wA[UB][T], wB[UB][T];
   f32x4 xA[UB][MT][2], xB[UB][MT][2];
   // Residual epilogue inputs (old h and the next RMSNorm gain) of the tile whose
   // last batch sits in the matching register buffer, fetched with that batch.
@@ -224,15 +257,23 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // makes the compiler wait for the data where the paths join).
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
   // load the q-th batch of this wave's work list (tile q / nbat, k-steps from (q % nbat) * UB)
-  auto load = [&](int q, u32x4 (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
+  auto load = [&](int q, WReg (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
     const int kb = (q % nbat) * UB;  // index into this wave's k-step list
-    __amdgpu_buffer_rsrc_t wr[T];
+    __amdgpu_buffer_rsrc_t wr[T], sr[T];
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       bool rok;
-      const uint16_t* base = weight_tile(a, KIND, tile, NC, t, KS, rok);
-      wr[t] = make_rsrc(base, rok ? (uint32_t)KS * 1024u : 0u);
+      if constexpr (Q4) {
+        int seg, n;
+        tile_segment(a, KIND, tile, NC, t, seg, n, rok);
+        const int KG = (K + 127) / 128;
+        wr[t] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * KS * 256, rok ? (uint32_t)KS * 256u : 0u);
+        sr[t] = make_rsrc(a.wscale[seg] + (size_t)(n / 16) * KG * 16, rok ? (uint32_t)KG * 32u : 0u);
+      } else {
+        const uint16_t* base = weight_tile(a, KIND, tile, NC, t, KS, rok);
+        wr[t] = make_rsrc(base, rok ? (uint32_t)KS * 1024u : 0u);
+      }
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -243,7 +284,16 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       const uint32_t wbad = (uint32_t)((kb + u) >= my_ks || ks >= KS) << 31;
       const uint32_t woff = ((uint32_t)ks * 1024u + lane * 16u) | wbad;
 #pragma unroll
-      for (int t = 0; t < T; ++t) wv[u][t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], woff, 0, kNonTemporal);
+      for (int t = 0; t < T; ++t) {
+        if constexpr (Q4) {
+          const uint32_t qoff = ((uint32_t)ks * 256u + lane * 4u) | wbad;
+          const uint32_t soff = ((uint32_t)(ks >> 2) * 32u + (lane & 15) * 2u) | wbad;
+          wv[u][t].codes = __builtin_amdgcn_raw_buffer_load_b32(wr[t], qoff, 0, kNonTemporal);
+          wv[u][t].scale = __builtin_amdgcn_raw_buffer_load_b16(sr[t], soff, 0, 0);
+        } else {
+          wv[u][t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], woff, 0, kNonTemporal);
+        }
+      }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = mt * 16 + mrow;
@@ -253,9 +303,21 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       }
     }
   };
-  auto compute = [&](u32x4 (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
+  auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
+      // Q4: the codes of each tile as bf16 operands and the row scales
+      bf16x8 bq[Q4 ? T : 1];
+      float sc[Q4 ? T : 1];
+      if constexpr (Q4) {
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          const uint32_t c = wv[u][t].codes;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) bq[t][j] = (__bf16)(float)((int)(c << (28 - 4 * j)) >> 28);
+          sc[t] = bf16_bits_to_f32((uint16_t)wv[u][t].scale);
+        }
+      }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         bf16x8 hi, lo;
@@ -268,9 +330,16 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
         }
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-          const bf16x8 b = __builtin_bit_cast(bf16x8, wv[u][t]);
-          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, b, acc[t][mt], 0, 0, 0);
-          acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, b, acc[t][mt], 0, 0, 0);
+          if constexpr (Q4) {
+            floatx4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq[t], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq[t], p, 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[t][mt][r] = fmaf(sc[t], p[r], acc[t][mt][r]);
+          } else {
+            const bf16x8 b = __builtin_bit_cast(bf16x8, wv[u][t]);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, b, acc[t][mt], 0, 0, 0);
+            acc[t][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, b, acc[t][mt], 0, 0, 0);
+          }
         }
       }
     }
@@ -872,19 +941,27 @@ template <int T, int MT, int KIND> struct BatchK {
   static constexpr bool PIPE = Batch<T, MT>::PIPE;
 };
 
-template <int T, int MT, int KIND>
+// (INT4 weights: a k-step's fragment is a quarter of the bf16 one, so a buffer
+// holds more k-steps to keep as many weight bytes in flight.)
+template <int T, int MT, int KIND, bool Q4> struct BatchQ {
+  static constexpr int UB = Q4 ? (MT == 1 ? (T == 1 ? 4 : 2) : 1) : BatchK<T, MT, KIND>::UB;
+  static constexpr bool PIPE = BatchK<T, MT, KIND>::PIPE;
+};
+
+template <int T, int MT, int KIND, bool Q4 = false>
 void launch_mfma_mt(const GemmArgs& a, int tiles, hipStream_t s) {
   const int grid = tiles < compute_units() ? tiles : compute_units();
-  hipLaunchKernelGGL((gemm_bf16_mfma<T, MT, BatchK<T, MT, KIND>::UB, BatchK<T, MT, KIND>::PIPE, KIND>), dim3(grid),
-                     dim3(kMfmaThreads), 0, s, a, tiles);
+  hipLaunchKernelGGL(
+      (gemm_bf16_mfma<T, MT, BatchQ<T, MT, KIND, Q4>::UB, BatchQ<T, MT, KIND, Q4>::PIPE, KIND, Q4>), dim3(grid),
+      dim3(kMfmaThreads), 0, s, a, tiles);
 }
 
-template <int T, int KIND>
+template <int T, int KIND, bool Q4 = false>
 hipError_t launch_mfma_t(const GemmArgs& a, int blocks, hipStream_t s) {
   const int MT = (a.M + 15) / 16;
-  if (MT <= 1) launch_mfma_mt<T, 1, KIND>(a, blocks, s);
-  else if (MT <= 2) launch_mfma_mt<T, 2, KIND>(a, blocks, s);
-  else if (MT <= 4) launch_mfma_mt<T, 4, KIND>(a, blocks, s);
+  if (MT <= 1) launch_mfma_mt<T, 1, KIND, Q4>(a, blocks, s);
+  else if (MT <= 2) launch_mfma_mt<T, 2, KIND, Q4>(a, blocks, s);
+  else if (MT <= 4) launch_mfma_mt<T, 4, KIND, Q4>(a, blocks, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -938,9 +1015,56 @@ __global__ void pack_kernel(const uint16_t* __restrict__ src, uint16_t* __restri
   *(u32x4*)(dst + i * 8) = v;
 }
 
+// INT4 quantization and packing, one thread per (packed row n, group of 128
+// columns): s = bf16(max|w| / 7) (IEEE division), q = clamp(rint(w / s), -8, 7)
+// (q = 0 where s = 0); the thread writes its row's 16 code words of the
+// group and the row's scale.  Rows follow the bf16 image's order (rope_hd).
+__global__ void pack_int4_kernel(const uint16_t* __restrict__ src, uint32_t* __restrict__ frag,
+                                 uint16_t* __restrict__ scale, int N, int K, int KS, int KG, int rope_hd) {
+  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i >= (size_t)N * KG) return;
+  const int n = (int)(i / KG), g = (int)(i % KG);
+  int row = n;
+  if (rope_hd > 0) {
+    const int t = n / 16, head = (16 * t) / rope_hd, tq = (16 * t) % rope_hd / 16, e = n & 15;
+    row = head * rope_hd + (e < 8 ? 8 * tq + e : rope_hd / 2 + 8 * tq + (e - 8));
+  }
+  const uint16_t* w = src + (size_t)row * K;
+  const int k0 = g * 128, k1 = min(K, k0 + 128);
+  float amax = 0.f;
+  for (int k = k0; k < k1; ++k) amax = fmaxf(amax, fabsf(bf16_bits_to_f32(w[k])));
+  const __bf16 sb = (__bf16)__fdiv_rn(amax, 7.0f);
+  const float sf = (float)sb;
+  scale[((size_t)(n / 16) * KG + g) * 16 + (n & 15)] = __builtin_bit_cast(uint16_t, sb);
+  for (int ks = k0 / 32; ks < min(KS, (k0 + 128) / 32); ++ks)
+    for (int kg = 0; kg < 4; ++kg) {
+      uint32_t word = 0u;
+      for (int e = 0; e < 8; ++e) {
+        const int k = ks * 32 + kg * 8 + e;
+        int q = 0;
+        if (k < K && sf != 0.f) q = (int)fminf(fmaxf(rintf(__fdiv_rn(bf16_bits_to_f32(w[k]), sf)), -8.f), 7.f);
+        word |= ((uint32_t)q & 0xFu) << (4 * e);
+      }
+      frag[((size_t)(n / 16) * KS + ks) * 64 + kg * 16 + (n & 15)] = word;
+    }
+}
+
 }  // namespace
 
 int device_compute_units() { return compute_units(); }
+
+size_t packed_int4_frag_bytes(int N, int K) { return (size_t)(N / 16) * ((K + 31) / 32) * 256; }
+size_t packed_int4_scale_bytes(int N, int K) { return (size_t)(N / 16) * ((K + 127) / 128) * 32; }
+
+hipError_t launch_pack_int4(const void* src, void* frag, void* scale, int N, int K, int rope_hd, hipStream_t s) {
+  if (N % 16 || K % 32) return hipErrorInvalidValue;
+  if (rope_hd < 0 || (rope_hd > 0 && (rope_hd % 16 || N % rope_hd))) return hipErrorInvalidValue;
+  const int KS = K / 32, KG = (K + 127) / 128;
+  const size_t n = (size_t)N * KG;
+  hipLaunchKernelGGL(pack_int4_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const uint16_t*)src,
+                     (uint32_t*)frag, (uint16_t*)scale, N, K, KS, KG, rope_hd);
+  return hipGetLastError();
+}
 
 size_t packed_elems(int N, int K) { return (size_t)(N / 16) * ((K + 31) / 32) * 512; }
 
@@ -1023,11 +1147,31 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || (a.K % 8) != 0 || (a.ldx % 4) != 0) return hipErrorInvalidValue;
   if (a.wide) {
+    if (a.q4) return hipErrorInvalidValue;  // (INT4 weights run passes of at most 64 rows)
     if (dtype != SPECDEC_BF16 || (a.kind == EPI_RESID && (!a.gain_bf16 || a.n_rows % 4))) return hipErrorInvalidValue;
     return launch_wide(a, s);
   }
   if (a.M > kMaxGemmRows) return hipErrorInvalidValue;
   const int blocks = gemm_row_blocks(dtype, a.kind, a.n_rows, a.M);
+  if (a.q4) {  // INT4 layer weights (passes of at most 64 rows)
+    if (dtype != SPECDEC_BF16 || (a.K % 32) != 0) return hipErrorInvalidValue;
+    const int T = mfma_tiles(a.kind, a.n_rows);
+    switch (a.kind) {
+      case EPI_RESID:
+        if (!a.gain_bf16) return hipErrorInvalidValue;
+        return T == 1 ? launch_mfma_t<1, EPI_RESID, true>(a, blocks, s)
+                      : (T == 2 ? launch_mfma_t<2, EPI_RESID, true>(a, blocks, s)
+                                : launch_mfma_t<3, EPI_RESID, true>(a, blocks, s));
+      case EPI_SWIGLU: return launch_mfma_t<2, EPI_SWIGLU, true>(a, blocks, s);
+      case EPI_QKV:
+        if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
+          return hipErrorInvalidValue;
+        return T == 1 ? launch_mfma_t<1, EPI_QKV, true>(a, blocks, s)
+                      : (T == 2 ? launch_mfma_t<2, EPI_QKV, true>(a, blocks, s)
+                                : launch_mfma_t<3, EPI_QKV, true>(a, blocks, s));
+      default: return hipErrorInvalidValue;
+    }
+  }
   if (dtype == SPECDEC_BF16) {
     if (a.kind == EPI_RESID && !a.gain_bf16) return hipErrorInvalidValue;
     const int T = mfma_tiles(a.kind, a.n_rows);

@@ -91,6 +91,9 @@ struct GemmArgs {
   // wide passes
   int wide;               // 1: the whole pass has more than kMaxGemmRows rows (set by the caller for every launch)
   float* ypart;           // RESID: split-K partial sums, wide_ypart_floats(n_rows) floats
+  // INT4 weights: w[] are INT4 images (packed_int4_*), wscale[] their group scales
+  int q4;
+  const uint16_t* wscale[3];
 };
 // Packed bf16 weight image (16-row x 32-column 1 KB fragments in MFMA operand
 // order).  rope_hd > 0 reorders the rows of each head of rope_hd rows so that
@@ -98,6 +101,14 @@ struct GemmArgs {
 // rotation pairs of RoPE side by side, 8 columns apart); 0 keeps the order.
 size_t packed_elems(int N, int K);
 hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s);
+// INT4 image of a bf16 W [N, K] (K % 32 == 0): code fragments of 256 bytes
+// (16 rows x 32 columns, the bf16 fragment's lane order, 4 bits per code, low
+// nibble first) and bf16 scales [N/16][ceil(K/128)][16]; the quantizer runs on
+// the device (groups of 128 columns, s = bf16(max|w| / 7), q = clamp(rint(w/s),
+// -8, 7)).  rope_hd as for launch_pack.
+size_t packed_int4_frag_bytes(int N, int K);
+size_t packed_int4_scale_bytes(int N, int K);
+hipError_t launch_pack_int4(const void* src, void* frag, void* scale, int N, int K, int rope_hd, hipStream_t s);
 // Number of row blocks the launcher uses for this GEMM (for ss partial counts)
 // in a pass of M rows.
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M);

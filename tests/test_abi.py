@@ -153,3 +153,31 @@ def test_reload_calls_reject_bad_arguments(lib):
     assert lib.specdec_load_async(fake, fake, 16, None, None) == -1
     assert lib.specdec_stream_wait_event(None, None) == -1
     assert lib.specdec_event_query(None, None) == -1
+
+
+def test_int4_image_sizes_and_format_errors(lib):
+    fake = ctypes.c_void_p(256)
+    h = ctypes.c_void_p()
+    d16 = binding.make_desc(synth.LLAMA_7B)
+    bf = lib.specdec_packed_bytes_fmt(ctypes.byref(d16), 2, 0)
+    q4 = lib.specdec_packed_bytes_fmt(ctypes.byref(d16), 2, 1)
+    assert bf == lib.specdec_packed_bytes(ctypes.byref(d16), 2)
+    # two 7B layers (2 x 202.4M weights) at 4 bits + 1/64 scale overhead, plus the bf16 LM head
+    head = 32000 * 4096 * 2
+    layer_w = 4 * 4096 * 4096 + 3 * 4096 * 11008
+    assert abs((q4 - head) - 2 * layer_w * (0.5 + 2 / 128)) < 1e5
+    assert abs((bf - head) - 2 * layer_w * 2) < 1e5
+    assert lib.specdec_packed_bytes_fmt(ctypes.byref(d16), 2, 7) == 0
+    assert lib.specdec_packed_bytes_fmt(ctypes.byref(binding.make_desc(synth.TINY)), 1, 1) == 0
+    arr = (ctypes.c_void_p * 2)(256, 256)
+    pp = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    w2 = binding.Weights(256, 256, 256, *([pp] * 9))
+    # unknown format; INT4 handles run at most 64 rows per pass
+    assert lib.specdec_pack_weights_fmt(ctypes.byref(d16), ctypes.byref(w2), 2, 5, fake, q4, None) == -1
+    assert lib.specdec_model_create_fmt(ctypes.byref(d16), ctypes.byref(w2), 2, 5, fake, q4, 8, 128, fake, 1 << 40,
+                                        ctypes.byref(h)) == -1
+    assert lib.specdec_model_create_fmt(ctypes.byref(d16), ctypes.byref(w2), 2, 1, fake, q4, 65, 128, fake, 1 << 40,
+                                        ctypes.byref(h)) == -6
+    assert lib.specdec_model_create_fmt(ctypes.byref(d16), ctypes.byref(w2), 2, 1, fake, q4 - 1, 8, 128, fake,
+                                        1 << 40, ctypes.byref(h)) == -1
+    assert not h.value
