@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of replaying HIP graphs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--weights", choices=("bf16", "int4"), default="bf16",
+                    help="layer weight format of the 7B verify line: bf16 (the headline), or INT4 codes with bf16 "
+                         "scales per row and group of 128 columns (the paper's model precision)")
     ap.add_argument("--prefill", action="store_true",
                     help="prompt prefill on the 7B-shaped target: a 2048-token prompt in chunks of 64..512 rows")
     ap.add_argument("--config", type=int, default=3, choices=(1, 2, 3, 4, 5),
@@ -64,8 +67,9 @@ def log(msg):
 
 
 # ---------------------------------------------------------------- synthetic model on the device
-def device_weights(shape, seed=0):
-    """Seeded N(0, 0.02^2) bf16 weights drawn on the device (RMSNorm gains 1.0)."""
+def device_weights(shape, seed=0, weight_format="bf16"):
+    """Seeded N(0, 0.02^2) bf16 weights drawn on the device (RMSNorm gains 1.0);
+    weight_format "int4" packs the layer matrices as INT4 (quantized on the device)."""
     import torch
     from paper_2608_10362_amd import binding
     gen = torch.Generator(device="cuda")
@@ -89,7 +93,7 @@ def device_weights(shape, seed=0):
                             "w_gate": mat(f, d), "w_up": mat(f, d), "w_down": mat(d, f)})
     w["final_norm"] = gain(d)
     w["lm_head"] = mat(shape.vocab, d)
-    return binding.DeviceWeights(shape, w)
+    return binding.DeviceWeights(shape, w, weight_format=weight_format)
 
 
 def install_context(kv, n_layers, shape, lengths, seed=5):
@@ -105,26 +109,33 @@ def install_context(kv, n_layers, shape, lengths, seed=5):
 
 
 # ---------------------------------------------------------------- algorithmic bytes
-def kernel_bytes(shape, ctx_read):
+def layer_weight_bytes(weights="bf16"):
+    """Bytes per layer-matrix weight: bf16, or INT4 codes plus one bf16 scale per 128."""
+    return 2.0 if weights == "bf16" else 0.5 + 2.0 / 128
+
+
+def kernel_bytes(shape, ctx_read, weights="bf16"):
     """Algorithmic HBM bytes per launch of each kernel kind (weights streamed once,
     KV read for the keys a launch attends to); activations (a few hundred KB) left out."""
     d, f, V = shape.d_model, shape.ffn_dim, shape.vocab
     e = 2
+    w = layer_weight_bytes(weights)
     return {
-        "qkv": ((shape.q_dim + 2 * shape.kv_dim) * d + d) * e,
-        "o_proj": d * shape.q_dim * e,
-        "gate_up": (2 * f * d + d) * e,
-        "down": d * f * e,
+        "qkv": int((shape.q_dim + 2 * shape.kv_dim) * d * w) + d * e,
+        "o_proj": int(d * shape.q_dim * w),
+        "gate_up": int(2 * f * d * w) + d * e,
+        "down": int(d * f * w),
         "lm_head": (V * d + d) * e,
         "attention": ctx_read * shape.n_kv_heads * shape.head_dim * 2 * e,
     }
 
 
-def verify_step_bytes(shape, ctx, gamma, batch):
+def verify_step_bytes(shape, ctx, gamma, batch, weights="bf16"):
     """Bytes one verify step must move: every weight once, the committed KV, the new KV."""
     L, d, f, V = shape.n_layers, shape.d_model, shape.ffn_dim, shape.vocab
     e = 2
-    per_layer = ((shape.q_dim + 2 * shape.kv_dim) * d + d * shape.q_dim + 3 * f * d + 2 * d) * e
+    per_layer = int(((shape.q_dim + 2 * shape.kv_dim) * d + d * shape.q_dim + 3 * f * d) * layer_weight_bytes(weights)) \
+        + 2 * d * e
     weights = L * per_layer + (V * d + d) * e + batch * (gamma + 1) * d * e
     kv_row = shape.n_kv_heads * shape.head_dim * 2 * e * L
     return weights + batch * ctx * kv_row + batch * (gamma + 1) * kv_row
@@ -593,7 +604,7 @@ def main():
     B, g, ctx, T = args.batch, args.gamma, args.ctx, args.temperature
     cap = ((ctx + g + 2 + 63) // 64) * 64
     t0 = time.time()
-    dw = device_weights(shape)
+    dw = device_weights(shape, weight_format=args.weights)
     target = binding.Model(dw, shape.n_layers, max_rows=max(B * (g + 1), 2 * B), max_ctx=cap)
     draft = binding.Model(dw, args.draft_layers, max_rows=max(B * (g + 1), 2 * B), max_ctx=cap)
     kv_t = binding.KVCache(target, B, cap)
@@ -664,7 +675,7 @@ def main():
     # re-launched back to back between HIP events on the library's stream.
     draft_part(0); verify_part(0)
     torch.cuda.synchronize()
-    kb_verify = kernel_bytes(shape, ctx + g + 1)
+    kb_verify = kernel_bytes(shape, ctx + g + 1, args.weights)
     # (bf16: RoPE and the KV append run in the QKV GEMM's epilogue, no rope_append launch)
     per_layer = {"embed": 1, "qkv": shape.n_layers, "attention": shape.n_layers,
                  "o_proj": shape.n_layers, "gate_up": shape.n_layers, "down": shape.n_layers, "lm_head": 1}
@@ -679,11 +690,12 @@ def main():
     dom = max((k for k in kernels if k in kb_verify and k != "attention"), key=lambda k: kernels[k]["ms_per_verify"])
     dom_bytes = kb_verify[dom]
     achieved = dom_bytes / (kernels[dom]["avg_us"] * 1e-6) / 1e9
-    vbytes = verify_step_bytes(shape, ctx, g, B)
+    vbytes = verify_step_bytes(shape, ctx, g, B, args.weights)
     verify_GBps = vbytes / (verify_ms * 1e-3) / 1e9
+    int4 = args.weights == "int4"
 
     result = {
-        "metric": METRIC,
+        "metric": METRIC if not int4 else "verify-step tokens/s (7B-shape, INT4 g128 layer weights, gamma=4, bs1)",
         "value": round(B * (g + 1) / (verify_ms * 1e-3), 2),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -695,13 +707,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"7B-shaped bf16 target verify + {args.draft_layers}-layer draft, gamma={g}, "
-                               f"batch {B}, context {ctx}, temperature {T}",
+        "config": {"workload": f"7B-shaped {'INT4-g128' if int4 else 'bf16'} target verify + "
+                               f"{args.draft_layers}-layer draft, gamma={g}, batch {B}, context {ctx}, temperature {T}",
                    "gamma": g, "batch": B, "ctx": ctx, "temperature": T, "draft_layers": args.draft_layers,
-                   "hip_graph": use_graph},
+                   "hip_graph": use_graph, "weights": args.weights},
         "roofline": {"bound": "hbm", "kernel": f"gemm {dom}", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": measured_traffic(dom), "bytes_per_launch": dom_bytes},
+                     "traffic": None if int4 else measured_traffic(dom), "bytes_per_launch": dom_bytes},
         "verify_ms": round(verify_ms, 4),
         "verify_ms_p10_p50_p90": [round(tm["verify_ms_p10"], 4), round(tm["verify_ms_p50"], 4),
                                   round(tm["verify_ms_p90"], 4)],
@@ -714,7 +726,7 @@ def main():
         "kernels": kernels,
         "step_profile": step_profile,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not int4:
         log("timing the CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(shape, ctx, g)
     print(json.dumps(result), flush=True)
