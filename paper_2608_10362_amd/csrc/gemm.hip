@@ -180,9 +180,12 @@ struct Q4Frag {
 // the packed 1 KB fragment), D[4(l/16)+r][l%16].
 template <int T, int MT, int UB, bool PIPE, int KIND, bool Q4 = false>
 __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n_tiles) {
-  // Q4: INT4 weights (Q4Frag).  The MFMA takes the codes as bf16 (small
-  // integers, exact) and each k-step's product is multiplied by the lane's
-  // row scale in float32, so the effective weights are exactly code * scale.
+  // Q4: INT4 weights (Q4Frag).  A code q is fed to the MFMA as the bf16 value
+  // 136 + q (bits 0x4300 | (q + 8): two byte permutes and an OR per four
+  // codes), and the bias is cancelled inside the accumulator by a product of
+  // the same x with the constant -136, shared by the unit's tiles; each
+  // k-step's product is then multiplied by the lane's row scale in float32,
+  // so the effective weights are code * scale.
   using WReg = std::conditional_t<Q4, Q4Frag, u32x4>;
   constexpr int NC = 16 * T;
   constexpr int MP = 16 * MT;
@@ -306,15 +309,21 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      // Q4: the codes of each tile as bf16 operands and the row scales
+      // Q4: the codes of each tile as biased bf16 operands and the row scales
       bf16x8 bq[Q4 ? T : 1];
       float sc[Q4 ? T : 1];
       if constexpr (Q4) {
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-          const uint32_t c = wv[u][t].codes;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) bq[t][j] = (__bf16)(float)((int)(c << (28 - 4 * j)) >> 28);
+          const uint32_t c = wv[u][t].codes ^ 0x88888888u;  // q + 8 in each nibble
+          const uint32_t even = c & 0x0F0F0F0Fu, odd = (c >> 4) & 0x0F0F0F0Fu;  // codes 0,2,4,6 / 1,3,5,7
+          u32x4 v;
+          // dword j/2 of the operand: code j in its low half, code j+1 in its high half
+          v[0] = __builtin_amdgcn_perm(odd, even, 0x0c040c00u) | 0x43004300u;
+          v[1] = __builtin_amdgcn_perm(odd, even, 0x0c050c01u) | 0x43004300u;
+          v[2] = __builtin_amdgcn_perm(odd, even, 0x0c060c02u) | 0x43004300u;
+          v[3] = __builtin_amdgcn_perm(odd, even, 0x0c070c03u) | 0x43004300u;
+          bq[t] = __builtin_bit_cast(bf16x8, v);
           sc[t] = bf16_bits_to_f32((uint16_t)wv[u][t].scale);
         }
       }
@@ -328,10 +337,16 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
           hi[j] = h;
           lo[j] = (__bf16)(v - (float)h);
         }
+        floatx4 bias = floatx4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (Q4) {  // -136 * sum_k x[m][k] in every column
+          const u32x4 m136 = u32x4{0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u};
+          bias = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, __builtin_bit_cast(bf16x8, m136), bias, 0, 0, 0);
+          bias = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, __builtin_bit_cast(bf16x8, m136), bias, 0, 0, 0);
+        }
 #pragma unroll
         for (int t = 0; t < T; ++t) {
           if constexpr (Q4) {
-            floatx4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq[t], floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            floatx4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bq[t], bias, 0, 0, 0);
             p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bq[t], p, 0, 0, 0);
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc[t][mt][r] = fmaf(sc[t], p[r], acc[t][mt][r]);
@@ -944,8 +959,9 @@ template <int T, int MT, int KIND> struct BatchK {
 // (INT4 weights: a k-step's fragment is a quarter of the bf16 one, so a buffer
 // holds more k-steps to keep as many weight bytes in flight.)
 template <int T, int MT, int KIND, bool Q4> struct BatchQ {
-  static constexpr int UB = Q4 ? (MT == 1 ? (T == 1 ? 4 : 2) : 1) : BatchK<T, MT, KIND>::UB;
-  static constexpr bool PIPE = BatchK<T, MT, KIND>::PIPE;
+  static constexpr int UB = Q4 ? (MT == 1 ? (T == 1 ? 3 : (T == 2 ? 2 : 1)) : 1) : BatchK<T, MT, KIND>::UB;
+  static constexpr bool PIPE_Q = !(Q4 && T == 3 && MT == 4);
+  static constexpr bool PIPE = BatchK<T, MT, KIND>::PIPE && PIPE_Q;
 };
 
 template <int T, int MT, int KIND, bool Q4 = false>
@@ -1155,7 +1171,11 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   const int blocks = gemm_row_blocks(dtype, a.kind, a.n_rows, a.M);
   if (a.q4) {  // INT4 layer weights (passes of at most 64 rows)
     if (dtype != SPECDEC_BF16 || (a.K % 32) != 0) return hipErrorInvalidValue;
-    const int T = mfma_tiles(a.kind, a.n_rows);
+    // (Q|K|V over more than 32 rows: one tile per unit, the registers going to
+    // the row tiles; the residual GEMMs keep mfma_tiles' count, which their
+    // RMSNorm partials follow)
+    const int T = a.M > 32 && a.kind == EPI_QKV ? 1 : mfma_tiles(a.kind, a.n_rows);
+    const int units = a.kind == EPI_QKV ? (a.n_rows + 16 * T - 1) / (16 * T) : blocks;
     switch (a.kind) {
       case EPI_RESID:
         if (!a.gain_bf16) return hipErrorInvalidValue;
@@ -1166,9 +1186,9 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
       case EPI_QKV:
         if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
           return hipErrorInvalidValue;
-        return T == 1 ? launch_mfma_t<1, EPI_QKV, true>(a, blocks, s)
-                      : (T == 2 ? launch_mfma_t<2, EPI_QKV, true>(a, blocks, s)
-                                : launch_mfma_t<3, EPI_QKV, true>(a, blocks, s));
+        return T == 1 ? launch_mfma_t<1, EPI_QKV, true>(a, units, s)
+                      : (T == 2 ? launch_mfma_t<2, EPI_QKV, true>(a, units, s)
+                                : launch_mfma_t<3, EPI_QKV, true>(a, units, s));
       default: return hipErrorInvalidValue;
     }
   }

@@ -117,9 +117,11 @@ def test_int4_draft_step_greedy():
     shape = synth.LLAMA_1B
     W = synth.make_weights(shape, n_layers=2)
     dw = binding.DeviceWeights(shape, W, weight_format="int4")
-    draft = binding.Model(dw, 1, max_rows=8, max_ctx=256)
+    # max_rows 64: the prompts are prefilled in 64-row passes (2 x 32 tokens: the
+    # INT4 GEMMs' 4-row-tile variants), then a 2-row draft step
+    draft = binding.Model(dw, 1, max_rows=64, max_ctx=256)
     kv = binding.KVCache(draft, 2, 256)
-    prompts = synth.make_prompt(40, shape.vocab, batch=2, seed=5)
+    prompts = synth.make_prompt(70, shape.vocab, batch=2, seed=5)
     binding.specdec_prefill(draft, kv, i32(prompts))
     g = 3
     d_out = torch.zeros((2, g), dtype=torch.int32, device="cuda")
@@ -132,5 +134,8 @@ def test_int4_draft_step_greedy():
         m.prefill(prompts[b, :-1], c)
         ref = m.forward_block([int(prompts[b, -1])], c.length, c)[0]
         assert np.abs(got[b] - ref).max() < TOL
+        k, v = kv.read_context(0, b, 0, 69)
+        assert np.abs(k.float().cpu().numpy() - c.k[0][:69]).max() < 0.05
+        assert np.abs(v.float().cpu().numpy() - c.v[0][:69]).max() < 0.05
         # greedy: the proposed token is the argmax of the proposing row
         assert int(d_out[b, 0]) == int(np.argmax(got[b]))
