@@ -321,7 +321,8 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     q.n_seg[0] = H * hd; q.n_seg[1] = G * hd; q.n_seg[2] = G * hd;
     q.n_rows = (H + 2 * G) * hd; q.kind = EPI_STORE; q.out = m->qkv; q.ldo = (H + 2 * G) * hd;
     if (dt == SPECDEC_BF16) {  // RoPE, the query store and the KV append run in the GEMM epilogue
-      q.kind = EPI_QKV; q.out = nullptr;
+      q.kind = EPI_QKV;  // (q.out stays the qkv scratch: passes of more than 128 rows store the projections there
+                         // and apply RoPE and the KV append in rope_append_kernel)
       q.rows = m->rows; q.rope_cs = m->rope_cs; q.qr = m->qr; q.kv = kv_layout(kv); q.layer = l;
       q.n_heads = H; q.n_kv_heads = G; q.head_dim = hd;
     }

@@ -886,6 +886,206 @@ __global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_spl
   if ((tid & 31) == 0 && m < M) a.ss_out[(size_t)blockIdx.x * a.ss_ld + m] = t;
 }
 
+// ---------------------------------------------------------------- tile MFMA kernel (bf16 weights, 129+ rows)
+// Launches of more than 128 rows (prefill chunks, up to 4 row tiles of 256 per
+// launch, row tiles adjacent in the grid so the blocks sharing a weight
+// column tile run together): compute-bound.  A block
+// covers 256 rows x 128 weight rows (SwiGLU: 64 gate and the 64 matching up
+// rows) with 8 waves in a 4 x 2 grid, each owning 64 x 64 = 4 x 4 MFMA tiles.
+// Per k-step the block stages in LDS the x slab (256 rows x 32 columns, split
+// into hi + lo bf16 A fragments; each wave moves whole fragments) and its 8
+// weight fragments (wave w moves fragment w); each wave then reads 8 A and
+// 4 B fragments for its 32 products (384 bytes of LDS per product, against
+// 1 KB when a wave owns one column tile).  x and weights are fetched two
+// k-steps ahead.  Epilogues in place: store (Q|K|V columns written back in
+// natural order, RoPE and the KV append then run in rope_append_kernel),
+// SwiGLU, and residual partial sums over n_split k ranges for
+// resid_reduce_kernel.
+constexpr int kTileThreads = 512;
+constexpr int kTileRows = 256, kTileCols = 128;
+constexpr int kTileSplitMax = 8;
+constexpr int kTileLaunchRows = 1024;  // rows per launch: up to 4 row tiles share each weight column tile
+constexpr int kTilePartialRows = 2048; // split-K partials held: n_split * launch rows <= this
+
+template <int KIND>  // EPI_STORE (also Q|K|V), EPI_SWIGLU, EPI_RESID (partials)
+__global__ __launch_bounds__(kTileThreads) void gemm_bf16_tile(GemmArgs a, int n_ctiles, int ks_per_split,
+                                                               int n_split) {
+  constexpr int MTB = kTileRows / 16, NTB = kTileCols / 16;
+  constexpr int PJ = kTileRows * 4 / kTileThreads;  // 32-byte x pieces per thread per slab
+  constexpr int RSR = kTileRows / (kTileThreads / kWave);
+  constexpr bool SCALE = KIND != EPI_RESID, SWIGLU = KIND == EPI_SWIGLU;
+  __shared__ u32x4 s_a[2][MTB][2][kWave];  // [buffer][m tile][hi, lo][lane]
+  __shared__ u32x4 s_b[2][NTB][kWave];     // [buffer][weight tile][lane]
+  __shared__ float scale[kTileRows];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int K = a.K, KS = (K + 31) / 32;
+  const int n_rt = (a.M + kTileRows - 1) / kTileRows;
+  const int rt = (int)blockIdx.x % n_rt, ct = ((int)blockIdx.x / n_rt) % n_ctiles;
+  const int split = (int)blockIdx.x / (n_rt * n_ctiles);
+  const int ks_begin = split * ks_per_split, ks_end = min(KS, ks_begin + ks_per_split);
+  const int n_k = ks_end - ks_begin, n_steps = (n_k + 1) & ~1;
+  const int m0 = rt * kTileRows, rows = min(a.M - m0, kTileRows);
+  // weight tile j of the block: SwiGLU tiles 0..3 gate, 4..7 up (same columns)
+  auto btile = [&](int j) { return SWIGLU ? (j < 2 ? wn * 2 + j : 4 + wn * 2 + (j - 2)) : wn * 4 + j; };
+
+  bool ok;
+  const uint16_t* wbase = weight_tile(a, KIND, ct, kTileCols, wave, KS, ok);  // (the tile this wave stages)
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(wbase, ok ? (uint32_t)KS * 1024u : 0u);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x + (size_t)m0 * a.ldx, (uint32_t)rows * a.ldx * 4u);
+
+  floatx4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  f32x4 xv[2][PJ][2];
+  u32x4 bv[2];
+
+  auto load = [&](int i, f32x4 (&xs)[PJ][2], u32x4& b) {
+    const uint32_t bad = (uint32_t)(i >= n_k) << 31;
+    b = __builtin_amdgcn_raw_buffer_load_b128(wr, ((uint32_t)(ks_begin + i) * 1024u + lane * 16u) | bad, 0,
+                                              kNonTemporal);
+#pragma unroll
+    for (int q = 0; q < PJ; ++q) {
+      const int p = tid + q * kTileThreads, m = (p >> 6) * 16 + (p & 15);
+      const int k = (ks_begin + i) * 32 + ((p >> 4) & 3) * 8;
+      const uint32_t off = (((uint32_t)m * a.ldx + k) * 4u) | bad | ((uint32_t)(k >= K) << 31);
+      xs[q][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      xs[q][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off + 16u, 0, 0));
+    }
+  };
+  auto store = [&](int buf, const f32x4 (&xs)[PJ][2], const u32x4& b) {
+#pragma unroll
+    for (int q = 0; q < PJ; ++q) {
+      const int p = tid + q * kTileThreads, mt = p >> 6, ln = p & 63;
+      bf16x8 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = xs[q][e >> 2][e & 3];
+        const __bf16 h = (__bf16)v;
+        hi[e] = h;
+        lo[e] = (__bf16)(v - (float)h);
+      }
+      s_a[buf][mt][0][ln] = __builtin_bit_cast(u32x4, hi);
+      s_a[buf][mt][1][ln] = __builtin_bit_cast(u32x4, lo);
+    }
+    s_b[buf][wave][lane] = b;
+  };
+  auto compute = [&](int buf) {
+    bf16x8 av[4][2], bw[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      av[i][0] = __builtin_bit_cast(bf16x8, s_a[buf][wm * 4 + i][0][lane]);
+      av[i][1] = __builtin_bit_cast(bf16x8, s_a[buf][wm * 4 + i][1][lane]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bw[j] = __builtin_bit_cast(bf16x8, s_b[buf][btile(j)][lane]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i][h], bw[j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);  // LDS reads
+    __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);  // then MFMAs
+  };
+
+  // Prologue: row-scale partial sums first, then slabs 0 and 1; slab 0 to LDS.
+  float rsv[SCALE ? RSR : 1];
+  if constexpr (SCALE) {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(a.ss_in, a.ss_in ? (uint32_t)a.n_ss * a.ss_ld * 4u : 0u);
+#pragma unroll
+    for (int i = 0; i < RSR; ++i) {
+      const int m = m0 + wave + (kTileThreads / kWave) * i;
+      const uint32_t off = ((uint32_t)lane * a.ss_ld + m) * 4u | ((uint32_t)(m >= a.M || lane >= a.n_ss) << 31);
+      rsv[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off, 0, 0));
+    }
+  }
+  load(0, xv[0], bv[0]);
+  load(1, xv[1], bv[1]);
+  if constexpr (SCALE) {
+#pragma unroll
+    for (int i = 0; i < RSR; ++i) {
+      const int r = wave + (kTileThreads / kWave) * i, m = m0 + r;
+      const float t = wave_sum(rsv[i]);  // (n_ss <= 64: checked by the launcher)
+      if (lane == 0) scale[r] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+    }
+  }
+  store(0, xv[0], bv[0]);
+  load(2, xv[0], bv[0]);
+  __syncthreads();
+
+  // Step i: multiply buffer i%2, move slab i+1 (register slot (i+1)%2) into the
+  // other buffer, fetch slab i+3 into that slot.  (Steps rounded up to even:
+  // the last one multiplies zeros when n_k is odd.)
+  for (int i0 = 0; i0 < n_steps; i0 += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = i0 + u;
+      __builtin_amdgcn_sched_barrier(0);
+      compute(u);
+      __builtin_amdgcn_sched_barrier(0);
+      store(u ^ 1, xv[u ^ 1], bv[u ^ 1]);
+      load(i + 3, xv[u ^ 1], bv[u ^ 1]);
+      __syncthreads();
+    }
+  }
+
+  // Epilogue.  acc[i][j][r]: row m0 + (wm*4 + i)*16 + 4*(lane/16) + r, column lane%16 of weight tile btile(j).
+  const int cl = lane & 15, rg = lane >> 4;
+  if constexpr (KIND == EPI_SWIGLU) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int f = ct * (kTileCols / 2) + (wn * 2 + j) * 16 + cl;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int mr = (wm * 4 + i) * 16 + 4 * rg + r;
+          if (mr < rows && f < a.n_rows)
+            a.out[(size_t)(m0 + mr) * a.ldo + f] =
+                silu_f(acc[i][j][r] * scale[mr]) * (acc[i][j + 2][r] * scale[mr]);
+        }
+    }
+  } else if constexpr (KIND == EPI_RESID) {
+    float* yp = a.ypart + (size_t)split * a.M * a.n_rows;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = ct * kTileCols + btile(j) * 16 + cl;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int mr = (wm * 4 + i) * 16 + 4 * rg + r;
+          if (mr < rows && n < a.n_rows) yp[(size_t)(m0 + mr) * a.n_rows + n] = acc[i][j][r];
+        }
+    }
+  } else {
+    // store; Q|K|V: Q and K columns come in the packed RoPE order (column c of
+    // a head's tile tq is dim 8*tq + c for c < 8, hd/2 + 8*tq + c - 8 otherwise)
+    const int hd = a.head_dim, nqk = a.n_seg[0] + a.n_seg[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = ct * kTileCols + btile(j) * 16 + cl;
+      int col = n;
+      if (a.kind == EPI_QKV && n < nqk) {
+        const int base = n >= a.n_seg[0] ? a.n_seg[0] : 0, r = n - base, w = r % hd, tq = w >> 4, ec = w & 15;
+        col = base + (r / hd) * hd + (ec < 8 ? 8 * tq + ec : hd / 2 + 8 * tq + ec - 8);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int mr = (wm * 4 + i) * 16 + 4 * rg + r;
+          if (mr < rows && n < a.n_rows) a.out[(size_t)(m0 + mr) * a.ldo + col] = acc[i][j][r] * scale[mr];
+        }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- vector kernel (float32 weights)
 // Block = 4 waves over NC weight rows; each wave takes NC/4 rows, lanes stride
 // over K; M processed 8 rows at a time.
@@ -1095,9 +1295,13 @@ hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hi
 }
 
 bool gemm_wide(int dtype, int M) { return dtype == SPECDEC_BF16 && M > kMaxGemmRows; }
-int gemm_launch_rows(int dtype, int M) { return gemm_wide(dtype, M) ? kWideRows : kMaxGemmRows; }
+int gemm_launch_rows(int dtype, int M) {
+  return !gemm_wide(dtype, M) ? kMaxGemmRows : (M > kWideRows ? kTileLaunchRows : kWideRows);
+}
 constexpr int kWideSplitMax = 4;
-size_t wide_ypart_floats(int n_rows) { return (size_t)kWideSplitMax * kWideRows * n_rows; }
+size_t wide_ypart_floats(int n_rows) {
+  return (size_t)std::max(kWideSplitMax * kWideRows, kTilePartialRows) * n_rows;
+}
 
 int gemm_row_blocks(int dtype, int kind, int n_rows, int M) {
   if (gemm_wide(dtype, M) && kind == EPI_RESID) return (n_rows + kWideCols - 1) / kWideCols;
@@ -1124,8 +1328,55 @@ void launch_wide_t(const GemmArgs& a, int blocks, int ks_per_split, int n_split,
   else launch_wide_mt<8, T, KIND>(a, blocks, ks_per_split, n_split, s);
 }
 
+// Launches of 129..1024 rows on the tile kernel (Q|K|V: a store of the
+// projections in natural column order, then rope_append_kernel).
+hipError_t launch_tile(const GemmArgs& a, hipStream_t s) {
+  if (a.M > kTileLaunchRows || (a.ss_in && a.n_ss > kWideMaxSs)) return hipErrorInvalidValue;
+  const int KS = (a.K + 31) / 32, n_rt = (a.M + kTileRows - 1) / kTileRows;
+  switch (a.kind) {
+    case EPI_STORE:
+    case EPI_QKV: {
+      if (a.kind == EPI_QKV && (!a.out || a.ldo < a.n_rows || a.head_dim % 16 || a.n_seg[0] % a.head_dim ||
+                                a.n_seg[1] % a.head_dim))
+        return hipErrorInvalidValue;
+      const int nct = (a.n_rows + kTileCols - 1) / kTileCols;
+      hipLaunchKernelGGL(gemm_bf16_tile<EPI_STORE>, dim3(n_rt * nct), dim3(kTileThreads), 0, s, a, nct, KS, 1);
+      if (a.kind == EPI_QKV) {
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        AttnArgs r{};
+        r.rows = a.rows; r.M = a.M; r.rps = a.M; r.n_heads = a.n_heads; r.n_kv_heads = a.n_kv_heads;
+        r.head_dim = a.head_dim; r.qkv = a.out; r.rope_cs = a.rope_cs; r.qr = a.qr; r.kv = a.kv; r.layer = a.layer;
+        return launch_rope_append(r, s);
+      }
+      break;
+    }
+    case EPI_SWIGLU: {
+      const int nct = (a.n_rows + kTileCols / 2 - 1) / (kTileCols / 2);
+      hipLaunchKernelGGL(gemm_bf16_tile<EPI_SWIGLU>, dim3(n_rt * nct), dim3(kTileThreads), 0, s, a, nct, KS, 1);
+      break;
+    }
+    case EPI_RESID: {
+      if (!a.ypart || a.n_rows % 4) return hipErrorInvalidValue;
+      const int nct = (a.n_rows + kTileCols - 1) / kTileCols, blocks = n_rt * nct;
+      int n_split = std::min(kTileSplitMax, std::max(1, (compute_units() + blocks - 1) / blocks));
+      n_split = std::min({n_split, KS, kTilePartialRows / a.M});
+      const int per = (KS + n_split - 1) / n_split;
+      n_split = (KS + per - 1) / per;
+      hipLaunchKernelGGL(gemm_bf16_tile<EPI_RESID>, dim3(blocks * n_split), dim3(kTileThreads), 0, s, a, nct, per,
+                         n_split);
+      hipLaunchKernelGGL(resid_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8),
+                         dim3(256), 0, s, a, n_split);
+      break;
+    }
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
-  if (a.M > kWideRows || (a.ss_in && a.n_ss > kWideMaxSs)) return hipErrorInvalidValue;
+  if (a.M > kWideRows) return launch_tile(a, s);
+  if (a.ss_in && a.n_ss > kWideMaxSs) return hipErrorInvalidValue;
   const int KS = (a.K + 31) / 32, cus = compute_units();
   switch (a.kind) {
     case EPI_STORE: {

@@ -230,12 +230,14 @@ def test_bf16_1b_shape_wide_rows(B, g):
 
 
 # ---------------------------------------------------------------- prefill in large chunks
-@pytest.mark.parametrize("shape_name,B,rows,n", [("LLAMA_1B", 2, 256, 301), ("LLAMA_7B", 1, 256, 301)])
+@pytest.mark.parametrize("shape_name,B,rows,n", [("LLAMA_1B", 2, 256, 301), ("LLAMA_7B", 1, 256, 301),
+                                                  ("LLAMA_1B", 2, 600, 301)])
 def test_bf16_prefill_in_large_chunks(shape_name, B, rows, n):
     """Prefill of n-1 prompt tokens per sequence in chunks of rows/B tokens
-    (1.1B: 128-token chunks of 2 sequences = 256-row passes in two wide launches,
-    GQA with 64 query tiles per kv head; 7B: 256-token chunks, MHA), then a
-    verify: the caches and the verify logits against the oracle's prefill."""
+    (1.1B: 128-token chunks of 2 sequences = 256-row passes, GQA with 64 query
+    tiles per kv head; 7B: 256-token chunks, MHA; 1.1B in one 600-row pass:
+    launches of three 256-row tiles, the last partial), then a verify: the
+    caches and the verify logits against the oracle's prefill."""
     torch = torch_cuda()
     shape = getattr(synth, shape_name)
     L, g = 2, 4
