@@ -149,10 +149,11 @@ SPECDEC_API specdec_status specdec_pack_weights(const specdec_model_desc* desc, 
 /* The same in a chosen weight format (SPECDEC_WEIGHTS_*).  INT4 image: the
  * LM head as in the bf16 image, then per layer the seven matrices, each as
  * INT4 code fragments followed by its scales (256-byte aligned):
- *  - codes: 16-row x 32-column fragments of 256 bytes, fragment (t, s) at
- *    byte 256*(t*K/32 + s); lane l = 16*g + i holds the 8 codes of row
- *    16t + i, columns 32s + 8g .. +7, as one 32-bit word, code j in bits
- *    4j..4j+3 (two's complement, -8..7);
+ *  - codes: per 16-row tile t and group G of 128 columns a 1 KB block at
+ *    byte 1024*(t*ceil(K/128) + G); lane l = 16*c + i holds 16 bytes at
+ *    16*l, four 32-bit words, word j holding the 8 codes of row 16t + i at
+ *    columns 128G + 32j + 8c .. +7, code e in bits 4e..4e+3 (two's
+ *    complement, -8..7; columns past K hold 0);
  *  - scales: bf16 [N/16][ceil(K/128)][16] (tile, group, row in tile).
  * Quantization (on the device, from the bf16 matrices): per row and group of
  * 128 columns, s = bf16(max|w| / 7) (float32 division, then rounding to

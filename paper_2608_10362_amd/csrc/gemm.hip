@@ -98,6 +98,47 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfi
   }
 }
 
+// Q|K|V epilogue over this block's final sums yfin[m][c], c < NC columns of
+// the concatenated Q|K|V rows (bf16 cache).  Columns of the Q and K segments
+// come in RoPE pairs: column c (c % 16 < 8) is dim j = 8 * (tile within the
+// head) + c % 8 of its head, column c ^ 8 is dim j + hd/2; x1' = x1 cos - x2
+// sin, x2' = x2 cos + x1 sin.  Rotated queries go to qr, K and V into the
+// cache at each valid row's position.  s_rows / s_cs: the rows' descriptors
+// and cos | sin tables.
+template <int NC, int NTH>
+__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, int blk, const float (*yfin)[NC + 1],
+                                             const float* scale, const RowDesc* s_rows, const float (*s_cs)[128]) {
+  const int M = a.M, hd = a.head_dim, half = hd >> 1, H = a.n_heads;
+  const int nq = a.n_seg[0], nqk = nq + a.n_seg[1], cap = a.kv.capacity;
+#pragma unroll 1
+  for (int i = threadIdx.x; i < M * NC; i += NTH) {
+    const int m = i / NC, c = i % NC, n = blk * NC + c;
+    if (n >= a.n_rows) continue;
+    const float x = yfin[m][c] * scale[m];
+    const RowDesc rd = s_rows[m];
+    if (n < nqk) {
+      const bool is_k = n >= nq;
+      const int r = is_k ? n - nq : n;
+      const int head = r / hd, w = r % hd, ec = w & 15;
+      const int j = 8 * (w >> 4) + (ec & 7);
+      const float y = yfin[m][c ^ 8] * scale[m];
+      const float cs = s_cs[m][j], sn = s_cs[m][half + j];
+      const float out = ec < 8 ? x * cs - y * sn : x * cs + y * sn;
+      const int d = ec < 8 ? j : half + j;
+      if (!is_k) {
+        a.qr[((size_t)m * H + head) * hd + d] = out;
+      } else if (rd.valid) {
+        uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+        Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::k(rd.pos, d, hd, cap), out);
+      }
+    } else if (rd.valid) {
+      const int r = n - nqk, head = r / hd, d = r % hd;
+      uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+      Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::v(rd.pos, d, hd, cap), x);
+    }
+  }
+}
+
 // Row pointer of weight row `r` of the block's concatenated row space.
 template <typename WT>
 __device__ __forceinline__ const WT* weight_row(const GemmArgs& a, int kind, int blk, int NC, int c, bool& ok) {
@@ -159,10 +200,11 @@ __device__ __forceinline__ void tile_segment(const GemmArgs& a, int kind, int bl
   }
 }
 
-// INT4 image of W [N, K]: 256-byte fragments (16 rows x 32 columns; lane
-// 16*(k%32/8) + n%16 holds the 8 codes of row n at columns 8*(k%32/8)..+7,
-// low nibble first), tile-major like the bf16 image, then the group scales
-// [N/16][KG][16] (bf16, groups of 128 columns).
+// INT4 image of W [N, K]: per 16-row tile and group of 128 columns a 1 KB
+// block in which lane l = 16*(k%32/8) + n%16 holds 16 bytes, the words of
+// the group's four k-steps; word j holds the 8 codes of row n at columns
+// 128g + 32j + 8*(l/16) .. +7, low nibble first.  Then the group scales
+// [N/16][KG][16] (bf16).
 struct Q4Frag {
   uint32_t codes;
   uint32_t scale;  // bf16 bits of the group scale of the lane's row (lane % 16)
@@ -271,7 +313,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
         int seg, n;
         tile_segment(a, KIND, tile, NC, t, seg, n, rok);
         const int KG = (K + 127) / 128;
-        wr[t] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * KS * 256, rok ? (uint32_t)KS * 256u : 0u);
+        wr[t] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * KG * 1024, rok ? (uint32_t)KG * 1024u : 0u);
         sr[t] = make_rsrc(a.wscale[seg] + (size_t)(n / 16) * KG * 16, rok ? (uint32_t)KG * 32u : 0u);
       } else {
         const uint16_t* base = weight_tile(a, KIND, tile, NC, t, KS, rok);
@@ -289,7 +331,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
 #pragma unroll
       for (int t = 0; t < T; ++t) {
         if constexpr (Q4) {
-          const uint32_t qoff = ((uint32_t)ks * 256u + lane * 4u) | wbad;
+          const uint32_t qoff = ((uint32_t)(ks >> 2) * 1024u + lane * 16u + (uint32_t)(ks & 3) * 4u) | wbad;
           const uint32_t soff = ((uint32_t)(ks >> 2) * 32u + (lane & 15) * 2u) | wbad;
           wv[u][t].codes = __builtin_amdgcn_raw_buffer_load_b32(wr[t], qoff, 0, kNonTemporal);
           wv[u][t].scale = __builtin_amdgcn_raw_buffer_load_b16(sr[t], soff, 0, 0);
@@ -379,38 +421,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
         a.ss_out[(size_t)blk * a.ss_ld + m] = t;
       }
     } else if constexpr (KIND == EPI_QKV) {
-      // Columns of the Q and K segments come in RoPE pairs: column c (c % 16 < 8)
-      // is dim j = 8 * (tile within the head) + c % 8 of its head, column c ^ 8
-      // is dim j + hd/2.  x1' = x1 cos - x2 sin, x2' = x2 cos + x1 sin.
-      const int hd = a.head_dim, half = hd >> 1, H = a.n_heads;
-      const int nq = a.n_seg[0], nqk = nq + a.n_seg[1], cap = a.kv.capacity;
-#pragma unroll 1
-      for (int i = tid; i < M * NC; i += kMfmaThreads) {
-        const int m = i / NC, c = i % NC, n = blk * NC + c;
-        if (n >= a.n_rows) continue;
-        const float x = yfin[m][c] * scale[m];
-        const RowDesc rd = s_rows[m];
-        if (n < nqk) {
-          const bool is_k = n >= nq;
-          const int r = is_k ? n - nq : n;
-          const int head = r / hd, w = r % hd, ec = w & 15;
-          const int j = 8 * (w >> 4) + (ec & 7);
-          const float y = yfin[m][c ^ 8] * scale[m];
-          const float cs = s_cs[m][j], sn = s_cs[m][half + j];
-          const float out = ec < 8 ? x * cs - y * sn : x * cs + y * sn;
-          const int d = ec < 8 ? j : half + j;
-          if (!is_k) {
-            a.qr[((size_t)m * H + head) * hd + d] = out;
-          } else if (rd.valid) {
-            uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
-            Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::k(rd.pos, d, hd, cap), out);
-          }
-        } else if (rd.valid) {
-          const int r = n - nqk, head = r / hd, d = r % hd;
-          uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
-          Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::v(rd.pos, d, hd, cap), x);
-        }
-      }
+      qkv_epilogue<NC, kMfmaThreads>(a, blk, yfin, scale, s_rows, s_cs);
     } else {
       epilogue<NC, KIND, kMfmaThreads>(a, blk, yfin, scale);
     }
@@ -548,6 +559,342 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       compute(wA, xA);
       finish(q, pA);
     }
+  }
+}
+
+// ---------------------------------------------------------------- INT4 kernel for passes of at most 16 rows
+// A block (one per CU, 8 waves) owns U units of TU 16-row tiles (unit
+// blockIdx.x + i*gridDim.x; a SwiGLU unit pairs a gate tile with an up tile)
+// and wave w reduces groups [w*gw, (w+1)*gw) of 128 columns of all of them.
+// Every code block (16 bytes per lane, tile and group) and group scale of the
+// wave is requested in the prologue, so the block's whole weight share is in
+// flight before the first multiply; the activations go through LDS instead
+// of registers.  Per window of GPW groups per wave, the block turns its x
+// chunks (8 columns of one row) into hi + lo bf16 operands, ordered as the
+// code unpacking orders columns, and sums each (group, row) to cancel the
+// +136 bias of the code operands: a group's product starts from -136 * sum x
+// and the group's scale multiplies it in float32.
+constexpr int kQ4Threads = 512;
+constexpr int kQ4Waves = kQ4Threads / kWave;
+constexpr int kQ4Rows = 16;                    // rows per launch
+constexpr int kQ4RowBlock = 16 * 32 + 16;      // window bytes of one (group, row): 16 chunks, padding
+constexpr int kQ4WindowBytes = 128 * 1024;
+constexpr int kQ4WindowRows = kQ4WindowBytes / kQ4RowBlock / kQ4Waves;  // GPW * M per window <= this (31)
+constexpr int kQ4Chunks = (kQ4Waves * kQ4WindowRows * 16 + kQ4Threads - 1) / kQ4Threads;  // per thread
+
+// One k-step's code word (8 columns of the lane's row) as biased bf16 MFMA
+// operands 136 + q (bits 0x4300 | (q + 8)): element 2d is column d, element
+// 2d + 1 column d + 4.  (The nibble's two's-complement sign bit flipped gives
+// q + 8; both that flip and the 0x4300 exponent bits are one XOR after the
+// mask, since the mask leaves those bits zero.)
+__device__ __forceinline__ bf16x8 q4_operand(uint32_t w) {
+  u32x4 v;
+  v[0] = (w & 0x000F000Fu) ^ 0x43084308u;
+  v[1] = ((w >> 4) & 0x000F000Fu) ^ 0x43084308u;
+  v[2] = ((w >> 8) & 0x000F000Fu) ^ 0x43084308u;
+  v[3] = ((w >> 12) & 0x000F000Fu) ^ 0x43084308u;
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int U, int TU, int GW, int GPW, int KIND>
+__global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_units, int gw) {
+  // GPW: groups per wave per window (GPW * M <= kQ4WindowRows); the windows
+  // are a compile-time sequence, so no branch joins paths with different
+  // loads in flight (which would force waits for every outstanding load).
+  constexpr int F = U * TU, NC = 16 * TU, NWIN = (GW + GPW - 1) / GPW;
+  constexpr bool QKV = KIND == EPI_QKV;
+  __shared__ __align__(16) unsigned char s_win[kQ4WindowBytes];    // x window, then the cross-wave sums
+  __shared__ __align__(16) float s_bias[kQ4Waves * GPW][16];  // per window group slot and row
+  __shared__ float yfin[U][kQ4Rows][NC + 1];
+  __shared__ float scale[kQ4Rows];
+  __shared__ RowDesc s_rows[QKV ? kQ4Rows : 1];
+  __shared__ float s_cs[QKV ? kQ4Rows : 1][QKV ? 128 : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int M = a.M, K = a.K, G = (K + 127) / 128;
+  const int my_g = max(0, min(G - wave * gw, gw));  // groups of this wave
+  const int n_chunks = kQ4Waves * GPW * M * 16;      // x chunks per window
+
+  // Window wi: chunk c = (slot*M + m)*16 + 4j + kq, slot = wave'*GPW + lgw,
+  // holds x[m][128*grp + 32j + 8kq .. +7] of group grp = wave'*gw + wi*GPW + lgw.
+  f32x4 xw[kQ4Chunks][2];
+  auto load_window = [&](int wi) {
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)M * a.ldx * 4u);
+#pragma unroll
+    for (int i = 0; i < kQ4Chunks; ++i) {
+      const int c = tid + i * kQ4Threads, jq = c & 15, r = c >> 4;
+      const int m = r % M, slot = r / M, lg = wi * GPW + slot % GPW;
+      const int grp = (slot / GPW) * gw + lg;
+      const int col = grp * 128 + (jq >> 2) * 32 + (jq & 3) * 8;
+      const uint32_t bad = (uint32_t)(c >= n_chunks || lg >= gw || grp >= G || col >= K) << 31;
+      const uint32_t off = (((uint32_t)m * a.ldx + col) * 4u) | bad;
+      xw[i][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
+      xw[i][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off + 16u, 0, 0));
+    }
+  };
+  auto store_window = [&]() {
+#pragma unroll
+    for (int i = 0; i < kQ4Chunks; ++i) {
+      const int c = tid + i * kQ4Threads, jq = c & 15, r = c >> 4;
+      if (c < n_chunks) {  // (all 16 chunks of a (group, row) or none: n_chunks % 16 == 0)
+        bf16x8 hi, lo;
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = xw[i][e & 1][e >> 1];  // columns 0, 4, 1, 5, 2, 6, 3, 7
+          const __bf16 h = (__bf16)v, l = (__bf16)(v - (float)h);
+          hi[e] = h;
+          lo[e] = l;
+          sum += (float)h + (float)l;
+        }
+        unsigned char* dst = s_win + r * kQ4RowBlock + jq * 32;
+        *(bf16x8*)dst = hi;
+        *(bf16x8*)(dst + 16) = lo;
+        // the (group, row)'s 16 chunks are lanes 16k .. 16k+15: fixed-order tree
+        sum += __shfl_xor(sum, 1, kWave);
+        sum += __shfl_xor(sum, 2, kWave);
+        sum += __shfl_xor(sum, 4, kWave);
+        sum += __shfl_xor(sum, 8, kWave);
+        if (jq == 0) s_bias[r / M][r % M] = -136.f * sum;
+      }
+    }
+  };
+
+  // Prologue: the first window's x, the row-scale partials and the QKV
+  // tables are requested before the codes (loads complete in order, so the
+  // conversions below wait for them alone).
+  load_window(0);
+  constexpr int RS_ROWS = kQ4Rows / kQ4Waves, RS_P = 4;
+  float rs_v[RS_ROWS][RS_P];
+  {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(a.ss_in, a.ss_in ? (uint32_t)a.n_ss * a.ss_ld * 4u : 0u);
+#pragma unroll
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kQ4Waves;
+#pragma unroll
+      for (int i = 0; i < RS_P; ++i) {
+        const int p = lane + i * kWave;
+        const uint32_t off = (m < M && p < a.n_ss) ? ((uint32_t)p * a.ss_ld + m) * 4u : kOutOfRange;
+        rs_v[r][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off, 0, 0));
+      }
+    }
+  }
+  constexpr int CS_E = QKV ? kQ4Rows * 128 / kQ4Threads : 1;
+  float cs_v[CS_E];
+  RowDesc rd_v{0, 0, 0, 0};
+  if constexpr (QKV) {
+    const __amdgpu_buffer_rsrc_t cr = make_rsrc(a.rope_cs, (uint32_t)M * a.head_dim * 4u);
+#pragma unroll
+    for (int e = 0; e < CS_E; ++e) {
+      const int i = tid + e * kQ4Threads, m = i / 128, j = i % 128;
+      const uint32_t off = j < a.head_dim ? ((uint32_t)m * a.head_dim + j) * 4u : kOutOfRange;
+      cs_v[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(cr, off, 0, 0));
+    }
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.rows, (uint32_t)M * (uint32_t)sizeof(RowDesc));
+    rd_v = __builtin_bit_cast(RowDesc, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rr, tid < kQ4Rows ? (uint32_t)tid * (uint32_t)sizeof(RowDesc) : kOutOfRange,
+                                           0, 0));
+  }
+  // Residual GEMMs (one 16-column unit): the old h and the next RMSNorm gain of
+  // this thread's output element.
+  constexpr bool PRE = KIND == EPI_RESID && U == 1;
+  float pre_h = 0.f;
+  uint32_t pre_g = 0u;
+  if constexpr (PRE) {
+    const int m = tid / 16, n = blockIdx.x * 16 + tid % 16;
+    const uint32_t bad = (uint32_t)(m >= M || n >= a.n_rows) << 31;
+    const __amdgpu_buffer_rsrc_t hr = make_rsrc(a.out, (uint32_t)M * a.ldo * 4u);
+    const __amdgpu_buffer_rsrc_t gr = make_rsrc(a.gain_out, (uint32_t)a.n_rows * 2u);
+    pre_h = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(hr, (((uint32_t)m * a.ldo + n) * 4u) | bad, 0, 0));
+    pre_g = __builtin_amdgcn_raw_buffer_load_b16(gr, ((uint32_t)n * 2u) | bad, 0, 0);
+  }
+  // The wave's code blocks and scales, group-major (the first group's arrive first).
+  u32x4 cw[F][GW];
+  uint32_t sw[F][GW];
+  {
+    __amdgpu_buffer_rsrc_t crs[F], srs[F];
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+      const int unit = blockIdx.x + (f / TU) * gridDim.x;
+      int seg, n;
+      bool ok;
+      tile_segment(a, KIND, unit, NC, f % TU, seg, n, ok);
+      ok = ok && unit < n_units;
+      crs[f] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * G * 1024, ok ? (uint32_t)G * 1024u : 0u);
+      srs[f] = make_rsrc(a.wscale[seg] + (size_t)(n / 16) * G * 16, ok ? (uint32_t)G * 32u : 0u);
+    }
+    // (scales first: a group's products wait for its scales, and loads complete
+    // in issue order; the scheduling fences keep that order)
+#pragma unroll
+    for (int lg = 0; lg < GW; ++lg) {
+      const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
+#pragma unroll
+      for (int f = 0; f < F; ++f)
+        sw[f][lg] = __builtin_amdgcn_raw_buffer_load_b16(
+            srs[f], ((uint32_t)(wave * gw + lg) * 32u + (lane & 15) * 2u) | bad, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int lg = 0; lg < GW; ++lg) {
+      const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
+#pragma unroll
+      for (int f = 0; f < F; ++f)
+        cw[f][lg] = __builtin_amdgcn_raw_buffer_load_b128(
+            crs[f], ((uint32_t)(wave * gw + lg) * 1024u + lane * 16u) | bad, 0, kNonTemporal);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  for (int i = tid; i < kQ4Waves * GPW * 16; i += kQ4Threads)
+    if ((i & 15) >= M) s_bias[i >> 4][i & 15] = 0.f;  // rows past M (never written by a window)
+#pragma unroll
+  for (int r = 0; r < RS_ROWS; ++r) {
+    const int m = wave + r * kQ4Waves;
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < RS_P; ++i) t += rs_v[r][i];
+    if (a.ss_in && m < M)
+      for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t += a.ss_in[(size_t)p * a.ss_ld + m];
+    t = wave_sum(t);
+    if (lane == 0) scale[m] = (a.ss_in && m < M) ? 1.0f / sqrtf(t / (float)K + a.eps) : 1.0f;
+  }
+  if constexpr (QKV) {
+#pragma unroll
+    for (int e = 0; e < CS_E; ++e) {
+      const int i = tid + e * kQ4Threads;
+      s_cs[i / 128][i % 128] = cs_v[e];
+    }
+    if (tid < kQ4Rows) s_rows[tid] = rd_v;
+  }
+  store_window();
+  __syncthreads();
+
+  floatx4 acc[F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) acc[f] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int kq = lane >> 4;
+  // STACK (at most 8 rows, GPW > 1 implies M <= 7): the hi parts of the rows
+  // go to A rows 0..7 and the lo parts to rows 8..15, so one product per
+  // k-step covers both; output rows m and m + 8 are added after the
+  // cross-wave sums.  Otherwise hi and lo are two products.
+  constexpr bool STACK = GPW > 1;
+  auto compute_group = [&](int lg) {
+    const int slot = wave * GPW + lg % GPW;
+    const floatx4 cb = *(const floatx4*)&s_bias[slot][4 * kq];
+    if constexpr (STACK) {
+      const unsigned char* xa =
+          s_win + (slot * M + min(lane & 7, M - 1)) * kQ4RowBlock + kq * 32 + ((lane >> 3) & 1) * 16;
+      floatx4 p[F];
+#pragma unroll
+      for (int f = 0; f < F; ++f) p[f] = cb;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x8 xv = *(const bf16x8*)(xa + j * 128);
+#pragma unroll
+        for (int f = 0; f < F; ++f)
+          p[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, q4_operand(cw[f][lg][j]), p[f], 0, 0, 0);
+      }
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const float sc = bf16_bits_to_f32((uint16_t)sw[f][lg]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, p[f][r], acc[f][r]);
+      }
+    } else {
+      const unsigned char* xb = s_win + (slot * M + min(lane & 15, M - 1)) * kQ4RowBlock + kq * 32;
+      floatx4 ph[F], pl[F];
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        ph[f] = cb;
+        pl[f] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x8 hi = *(const bf16x8*)(xb + j * 128), lo = *(const bf16x8*)(xb + j * 128 + 16);
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+          const bf16x8 b = q4_operand(cw[f][lg][j]);
+          ph[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, b, ph[f], 0, 0, 0);
+          pl[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, b, pl[f], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        const float sc = bf16_bits_to_f32((uint16_t)sw[f][lg]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, ph[f][r] + pl[f][r], acc[f][r]);
+      }
+    }
+  };
+  // (blocks of one tile have the registers to fetch the next window's x while
+  // the current one is multiplied; a window past the wave's groups loads
+  // nothing and converts zeros)
+  constexpr bool PREFETCH = F == 1;
+#pragma unroll
+  for (int w = 0; w < NWIN; ++w) {
+    if (w > 0) {
+      __syncthreads();
+      if constexpr (!PREFETCH) load_window(w);
+      store_window();
+      __syncthreads();
+    }
+    if constexpr (PREFETCH) {
+      if (w + 1 < NWIN) load_window(w + 1);
+    }
+#pragma unroll
+    for (int i = 0; i < GPW; ++i) {
+      const int lg = w * GPW + i;
+      if (lg < GW && lg < my_g) compute_group(lg);
+    }
+  }
+
+  // Cross-wave sums in fixed wave order: red[f][wave][lane][r] -> yfin.
+  __syncthreads();
+  float* red = (float*)s_win;
+#pragma unroll
+  for (int f = 0; f < F; ++f) *(floatx4*)&red[((f * kQ4Waves + wave) * kWave + lane) * 4] = acc[f];
+  __syncthreads();
+  for (int i = tid; i < F * kWave * 4; i += kQ4Threads) {
+    const int f = i / (kWave * 4), l = (i / 4) % kWave, r = i % 4;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kQ4Waves; ++w) s += red[((f * kQ4Waves + w) * kWave + l) * 4 + r];
+    yfin[f / TU][4 * (l >> 4) + r][(f % TU) * 16 + (l & 15)] = s;
+  }
+  __syncthreads();
+  if constexpr (STACK) {  // rows m (hi parts) + m + 8 (lo parts)
+    for (int i = tid; i < U * 8 * NC; i += kQ4Threads) {
+      const int u = i / (8 * NC), m = (i / NC) % 8, c = i % NC;
+      yfin[u][m][c] += yfin[u][m + 8][c];
+    }
+    __syncthreads();
+  }
+  if constexpr (PRE) {  // h += y; xg = h * gain; sum of squares of the unit's new h
+    const int m = tid / 16, c = tid % 16, n = blockIdx.x * 16 + c;
+    if (m < M) {
+      float hv = 0.f;
+      if (n < a.n_rows) {
+        hv = pre_h + yfin[0][m][c];
+        a.out[(size_t)m * a.ldo + n] = hv;
+        a.xg_out[(size_t)m * a.ldo + n] = hv * bf16_bits_to_f32((uint16_t)pre_g);
+      }
+      yfin[0][m][c] = hv;
+    }
+    __syncthreads();
+    if (tid < M) {
+      float t = 0.f;
+      for (int c2 = 0; c2 < 16; ++c2) t += yfin[0][tid][c2] * yfin[0][tid][c2];
+      a.ss_out[(size_t)blockIdx.x * a.ss_ld + tid] = t;
+    }
+    return;
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int unit = blockIdx.x + u * gridDim.x;
+    if (unit >= n_units) break;  // (block-uniform)
+    if constexpr (QKV) qkv_epilogue<NC, kQ4Threads>(a, unit, yfin[u], scale, s_rows, s_cs);
+    else epilogue<NC, KIND, kQ4Threads>(a, unit, yfin[u], scale);
   }
 }
 
@@ -1252,16 +1599,19 @@ __global__ void pack_int4_kernel(const uint16_t* __restrict__ src, uint32_t* __r
   const __bf16 sb = (__bf16)__fdiv_rn(amax, 7.0f);
   const float sf = (float)sb;
   scale[((size_t)(n / 16) * KG + g) * 16 + (n & 15)] = __builtin_bit_cast(uint16_t, sb);
-  for (int ks = k0 / 32; ks < min(KS, (k0 + 128) / 32); ++ks)
+  // (the group's four k-steps: a k-step past K keeps zero codes)
+  for (int j = 0; j < 4; ++j)
     for (int kg = 0; kg < 4; ++kg) {
+      const int ks = 4 * g + j;
       uint32_t word = 0u;
       for (int e = 0; e < 8; ++e) {
         const int k = ks * 32 + kg * 8 + e;
         int q = 0;
-        if (k < K && sf != 0.f) q = (int)fminf(fmaxf(rintf(__fdiv_rn(bf16_bits_to_f32(w[k]), sf)), -8.f), 7.f);
+        if (ks < KS && k < K && sf != 0.f)
+          q = (int)fminf(fmaxf(rintf(__fdiv_rn(bf16_bits_to_f32(w[k]), sf)), -8.f), 7.f);
         word |= ((uint32_t)q & 0xFu) << (4 * e);
       }
-      frag[((size_t)(n / 16) * KS + ks) * 64 + kg * 16 + (n & 15)] = word;
+      frag[(((size_t)(n / 16) * KG + g) * 64 + kg * 16 + (n & 15)) * 4 + j] = word;
     }
 }
 
@@ -1269,7 +1619,7 @@ __global__ void pack_int4_kernel(const uint16_t* __restrict__ src, uint32_t* __r
 
 int device_compute_units() { return compute_units(); }
 
-size_t packed_int4_frag_bytes(int N, int K) { return (size_t)(N / 16) * ((K + 31) / 32) * 256; }
+size_t packed_int4_frag_bytes(int N, int K) { return (size_t)(N / 16) * ((K + 127) / 128) * 1024; }
 size_t packed_int4_scale_bytes(int N, int K) { return (size_t)(N / 16) * ((K + 127) / 128) * 32; }
 
 hipError_t launch_pack_int4(const void* src, void* frag, void* scale, int N, int K, int rope_hd, hipStream_t s) {
@@ -1411,6 +1761,60 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
 }
 }  // namespace
 
+// INT4 passes of at most 16 rows on gemm_q4_lds: hipErrorNotSupported where
+// its register budget does not cover the shape (the caller then runs the
+// skinny kernel's INT4 path).  Groups per wave and window: all of them (one
+// window) while the rows allow, else one.
+template <int U, int TU, int GW, int KIND>
+static void launch_q4_w(const GemmArgs& a, int n_units, int gw, hipStream_t s) {
+  const int grid = std::min(n_units, compute_units());
+  constexpr int G1 = GW == 4 ? 4 : 6;  // (12 groups: two windows of 6 for up to 5 rows)
+  if (G1 * a.M <= kQ4WindowRows)
+    hipLaunchKernelGGL((gemm_q4_lds<U, TU, GW, G1, KIND>), dim3(grid), dim3(kQ4Threads), 0, s, a, n_units, gw);
+  else
+    hipLaunchKernelGGL((gemm_q4_lds<U, TU, GW, 1, KIND>), dim3(grid), dim3(kQ4Threads), 0, s, a, n_units, gw);
+}
+
+template <int U, int TU, int KIND>
+static hipError_t launch_q4_u(const GemmArgs& a, int n_units, int gw, hipStream_t s) {
+  if (gw <= 4) {
+    launch_q4_w<U, TU, 4, KIND>(a, n_units, gw, s);
+  } else if constexpr (U * TU == 1) {  // (12 groups per wave: single-tile units only)
+    if (gw > 12) return hipErrorNotSupported;
+    launch_q4_w<U, TU, 12, KIND>(a, n_units, gw, s);
+  } else {
+    return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+static hipError_t launch_q4_lds(const GemmArgs& a, hipStream_t s) {
+  if (a.M > kQ4Rows || a.n_rows % 16 || (a.kind == EPI_QKV && a.head_dim > 128)) return hipErrorNotSupported;
+  // (residual GEMMs: one tile per unit, as the RMSNorm partials of the consumer expect)
+  if (a.kind == EPI_RESID && mfma_tiles(EPI_RESID, a.n_rows) != 1) return hipErrorNotSupported;
+  const int n_units = a.n_rows / 16, cus = compute_units();
+  const int U = (n_units + cus - 1) / cus;
+  const int G = (a.K + 127) / 128, gw = (G + kQ4Waves - 1) / kQ4Waves;
+  switch (a.kind) {
+    case EPI_QKV:
+      if (U == 1) return launch_q4_u<1, 1, EPI_QKV>(a, n_units, gw, s);
+      if (U == 2) return launch_q4_u<2, 1, EPI_QKV>(a, n_units, gw, s);
+      if (U == 3) return launch_q4_u<3, 1, EPI_QKV>(a, n_units, gw, s);
+      break;
+    case EPI_SWIGLU:
+      if (U == 1) return launch_q4_u<1, 2, EPI_SWIGLU>(a, n_units, gw, s);
+      if (U == 2) return launch_q4_u<2, 2, EPI_SWIGLU>(a, n_units, gw, s);
+      if (U == 3) return launch_q4_u<3, 2, EPI_SWIGLU>(a, n_units, gw, s);
+      break;
+    case EPI_RESID:
+      if (U == 1) return launch_q4_u<1, 1, EPI_RESID>(a, n_units, gw, s);
+      if (U == 2) return launch_q4_u<2, 1, EPI_RESID>(a, n_units, gw, s);
+      break;
+    default: break;
+  }
+  return hipErrorNotSupported;
+}
+
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || (a.K % 8) != 0 || (a.ldx % 4) != 0) return hipErrorInvalidValue;
   if (a.wide) {
@@ -1422,6 +1826,12 @@ hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s) {
   const int blocks = gemm_row_blocks(dtype, a.kind, a.n_rows, a.M);
   if (a.q4) {  // INT4 layer weights (passes of at most 64 rows)
     if (dtype != SPECDEC_BF16 || (a.K % 32) != 0) return hipErrorInvalidValue;
+    if (a.kind == EPI_RESID && !a.gain_bf16) return hipErrorInvalidValue;
+    if (a.kind == EPI_QKV && (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim ||
+                              a.n_seg[1] % a.head_dim))
+      return hipErrorInvalidValue;
+    const hipError_t e = launch_q4_lds(a, s);
+    if (e != hipErrorNotSupported) return e;
     // (Q|K|V over more than 32 rows: one tile per unit, the registers going to
     // the row tiles; the residual GEMMs keep mfma_tiles' count, which their
     // RMSNorm partials follow)

@@ -101,8 +101,9 @@ struct GemmArgs {
 // rotation pairs of RoPE side by side, 8 columns apart); 0 keeps the order.
 size_t packed_elems(int N, int K);
 hipError_t launch_pack(const void* src, void* dst, int N, int K, int rope_hd, hipStream_t s);
-// INT4 image of a bf16 W [N, K] (K % 32 == 0): code fragments of 256 bytes
-// (16 rows x 32 columns, the bf16 fragment's lane order, 4 bits per code, low
+// INT4 image of a bf16 W [N, K] (K % 32 == 0): code blocks of 1 KB per 16-row
+// tile and group of 128 columns (lane l of the bf16 fragment's lane order holds
+// the 32-bit code words of the group's four k-steps, 4 bits per code, low
 // nibble first) and bf16 scales [N/16][ceil(K/128)][16]; the quantizer runs on
 // the device (groups of 128 columns, s = bf16(max|w| / 7), q = clamp(rint(w/s),
 // -8, 7)).  rope_hd as for launch_pack.

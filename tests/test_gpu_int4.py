@@ -29,11 +29,13 @@ def _matrices(shape):
 def _decode(img, off, soff, N, K):
     """Codes [N, K] and scale bits [N, ceil(K/128)] of one INT4 matrix of the image
     (layout as documented with specdec_pack_weights_fmt)."""
-    T, S, G = N // 16, K // 32, (K + 127) // 128
-    words = img[off:off + T * S * 256].view(np.uint32).reshape(T, S, 4, 16)  # [t][s][g][i]
-    codes = np.stack([((words >> np.uint32(4 * j)) & np.uint32(0xF)).astype(np.int16) for j in range(8)], -1)
-    codes = np.where(codes >= 8, codes - 16, codes).astype(np.int8)            # [t][s][g][i][j]
-    q = codes.transpose(0, 3, 1, 2, 4).reshape(N, K)                           # row 16t+i, col 32s+8g+j
+    T, G = N // 16, (K + 127) // 128
+    words = img[off:off + T * G * 1024].view(np.uint32).reshape(T, G, 4, 16, 4)  # [t][G][c][i][j]
+    codes = np.stack([((words >> np.uint32(4 * e)) & np.uint32(0xF)).astype(np.int16) for e in range(8)], -1)
+    codes = np.where(codes >= 8, codes - 16, codes).astype(np.int8)               # [t][G][c][i][j][e]
+    q = codes.transpose(0, 3, 1, 4, 2, 5).reshape(N, G * 128)                     # row 16t+i, col 128G+32j+8c+e
+    assert not q[:, K:].any()                                                     # columns past K hold 0
+    q = q[:, :K]
     s = img[soff:soff + T * G * 32].view(np.uint16).reshape(T, G, 16).transpose(0, 2, 1).reshape(N, G)
     return q, s
 
@@ -57,7 +59,7 @@ def test_device_quantizer_matches_the_oracle_bit_for_bit():
     img = dw.packed.cpu().numpy()
     off = _align(shape.vocab * shape.d_model * 2)  # the bf16 LM head comes first
     for name, N, K in _matrices(shape):
-        frag = _align(off + (N // 16) * (K // 32) * 256)
+        frag = _align(off + (N // 16) * ((K + 127) // 128) * 1024)
         q, s = _decode(img, off, frag, N, K)
         off = _align(frag + (N // 16) * ((K + 127) // 128) * 32)
         src = W["layers"][0][name]
@@ -104,12 +106,19 @@ def _int4_case(shape, n_layers, lengths, g, seed):
     return dw, W
 
 
-def test_int4_7b_shape_verify():
-    _int4_case(synth.LLAMA_7B, 2, [2048], g=4, seed=0)
+@pytest.mark.parametrize("g", [4, 8])
+def test_int4_7b_shape_verify(g):
+    # 5 rows: x of every 4096-column GEMM in one LDS window, the down projection
+    # in two; 9 rows: every GEMM over several windows
+    _int4_case(synth.LLAMA_7B, 2, [2048], g=g, seed=0)
 
 
-def test_int4_1b_shape_ragged_batch():
-    _int4_case(synth.LLAMA_1B, 2, [1, 64, 300, 129], g=4, seed=1)
+@pytest.mark.parametrize("lengths,g", [([1, 64, 300, 129], 4), ([1, 64, 300, 129], 3), ([517], 4)])
+def test_int4_1b_shape_verify(lengths, g):
+    # 20 rows: the skinny kernel's INT4 path; 16 rows: one group per wave and
+    # window; one sequence: two SwiGLU units per block, 6 groups per wave of
+    # the 5632-column down projection
+    _int4_case(synth.LLAMA_1B, 2, lengths, g=g, seed=1)
 
 
 def test_int4_draft_step_greedy():
