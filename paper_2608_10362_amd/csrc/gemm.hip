@@ -571,9 +571,8 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
 // flight before the first multiply; the activations go through LDS instead
 // of registers.  Per window of GPW groups per wave, the block turns its x
 // chunks (8 columns of one row) into hi + lo bf16 operands, ordered as the
-// code unpacking orders columns, and sums each (group, row) to cancel the
-// +136 bias of the code operands: a group's product starts from -136 * sum x
-// and the group's scale multiplies it in float32.
+// code unpacking orders columns; a group's sum over its four k-steps is
+// multiplied by the group's scale in float32.
 constexpr int kQ4Threads = 512;
 constexpr int kQ4Waves = kQ4Threads / kWave;
 constexpr int kQ4Rows = 16;                    // rows per launch
@@ -581,6 +580,9 @@ constexpr int kQ4RowBlock = 16 * 32 + 16;      // window bytes of one (group, ro
 constexpr int kQ4WindowBytes = 128 * 1024;
 constexpr int kQ4WindowRows = kQ4WindowBytes / kQ4RowBlock / kQ4Waves;  // GPW * M per window <= this (31)
 constexpr int kQ4Chunks = (kQ4Waves * kQ4WindowRows * 16 + kQ4Threads - 1) / kQ4Threads;  // per thread
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // One k-step's code word (8 columns of the lane's row) as biased bf16 MFMA
 // operands 136 + q (bits 0x4300 | (q + 8)): element 2d is column d, element
@@ -604,7 +606,6 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
   constexpr int F = U * TU, NC = 16 * TU, NWIN = (GW + GPW - 1) / GPW;
   constexpr bool QKV = KIND == EPI_QKV;
   __shared__ __align__(16) unsigned char s_win[kQ4WindowBytes];    // x window, then the cross-wave sums
-  __shared__ __align__(16) float s_bias[kQ4Waves * GPW][16];  // per window group slot and row
   __shared__ float yfin[U][kQ4Rows][NC + 1];
   __shared__ float scale[kQ4Rows];
   __shared__ RowDesc s_rows[QKV ? kQ4Rows : 1];
@@ -636,33 +637,30 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
 #pragma unroll
     for (int i = 0; i < kQ4Chunks; ++i) {
       const int c = tid + i * kQ4Threads, jq = c & 15, r = c >> 4;
-      if (c < n_chunks) {  // (all 16 chunks of a (group, row) or none: n_chunks % 16 == 0)
-        bf16x8 hi, lo;
-        float sum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float v = xw[i][e & 1][e >> 1];  // columns 0, 4, 1, 5, 2, 6, 3, 7
-          const __bf16 h = (__bf16)v, l = (__bf16)(v - (float)h);
-          hi[e] = h;
-          lo[e] = l;
-          sum += (float)h + (float)l;
-        }
+      if (c < n_chunks) {
+        // columns 0, 4, 1, 5, 2, 6, 3, 7 (the order of the unpacked codes)
+        const f32x2 p0 = {xw[i][0][0], xw[i][1][0]}, p1 = {xw[i][0][1], xw[i][1][1]};
+        const f32x2 p2 = {xw[i][0][2], xw[i][1][2]}, p3 = {xw[i][0][3], xw[i][1][3]};
+        const bf16x2 h0 = __builtin_convertvector(p0, bf16x2), h1 = __builtin_convertvector(p1, bf16x2);
+        const bf16x2 h2 = __builtin_convertvector(p2, bf16x2), h3 = __builtin_convertvector(p3, bf16x2);
+        const f32x2 r0 = p0 - __builtin_convertvector(h0, f32x2), r1 = p1 - __builtin_convertvector(h1, f32x2);
+        const f32x2 r2 = p2 - __builtin_convertvector(h2, f32x2), r3 = p3 - __builtin_convertvector(h3, f32x2);
+        const u32x4 hv = {__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1),
+                          __builtin_bit_cast(uint32_t, h2), __builtin_bit_cast(uint32_t, h3)};
+        const u32x4 lv = {__builtin_bit_cast(uint32_t, __builtin_convertvector(r0, bf16x2)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector(r1, bf16x2)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector(r2, bf16x2)),
+                          __builtin_bit_cast(uint32_t, __builtin_convertvector(r3, bf16x2))};
         unsigned char* dst = s_win + r * kQ4RowBlock + jq * 32;
-        *(bf16x8*)dst = hi;
-        *(bf16x8*)(dst + 16) = lo;
-        // the (group, row)'s 16 chunks are lanes 16k .. 16k+15: fixed-order tree
-        sum += __shfl_xor(sum, 1, kWave);
-        sum += __shfl_xor(sum, 2, kWave);
-        sum += __shfl_xor(sum, 4, kWave);
-        sum += __shfl_xor(sum, 8, kWave);
-        if (jq == 0) s_bias[r / M][r % M] = -136.f * sum;
+        *(u32x4*)dst = hv;
+        *(u32x4*)(dst + 16) = lv;
       }
     }
   };
 
   // Prologue: the first window's x, the row-scale partials and the QKV
-  // tables are requested before the codes (loads complete in order, so the
-  // conversions below wait for them alone).
+  // tables are requested before the scales and codes (loads complete in
+  // order, so the conversions below wait for them alone).
   load_window(0);
   constexpr int RS_ROWS = kQ4Rows / kQ4Waves, RS_P = 4;
   float rs_v[RS_ROWS][RS_P];
@@ -709,45 +707,46 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
         float, __builtin_amdgcn_raw_buffer_load_b32(hr, (((uint32_t)m * a.ldo + n) * 4u) | bad, 0, 0));
     pre_g = __builtin_amdgcn_raw_buffer_load_b16(gr, ((uint32_t)n * 2u) | bad, 0, 0);
   }
-  // The wave's code blocks and scales, group-major (the first group's arrive first).
+  // The wave's code blocks and scales, group-major.  All scales come first
+  // (a group's products wait for its scales, and loads complete in issue
+  // order); the codes of D groups are requested here and each later group's
+  // D groups ahead of its products, so the vector-memory issue of a large
+  // share (about 64 KB per CU per group issued) does not hold up the x
+  // conversion, and about 64 KB per CU stays in flight.
+  constexpr int D = F >= 6 ? 2 : (F >= 3 ? 3 : (F == 2 ? 4 : 8));
   u32x4 cw[F][GW];
   uint32_t sw[F][GW];
-  {
-    __amdgpu_buffer_rsrc_t crs[F], srs[F];
+  __amdgpu_buffer_rsrc_t crs[F], srs[F];
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
-      const int unit = blockIdx.x + (f / TU) * gridDim.x;
-      int seg, n;
-      bool ok;
-      tile_segment(a, KIND, unit, NC, f % TU, seg, n, ok);
-      ok = ok && unit < n_units;
-      crs[f] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * G * 1024, ok ? (uint32_t)G * 1024u : 0u);
-      srs[f] = make_rsrc(a.wscale[seg] + (size_t)(n / 16) * G * 16, ok ? (uint32_t)G * 32u : 0u);
-    }
-    // (scales first: a group's products wait for its scales, and loads complete
-    // in issue order; the scheduling fences keep that order)
-#pragma unroll
-    for (int lg = 0; lg < GW; ++lg) {
-      const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
-#pragma unroll
-      for (int f = 0; f < F; ++f)
-        sw[f][lg] = __builtin_amdgcn_raw_buffer_load_b16(
-            srs[f], ((uint32_t)(wave * gw + lg) * 32u + (lane & 15) * 2u) | bad, 0, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int lg = 0; lg < GW; ++lg) {
-      const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
-#pragma unroll
-      for (int f = 0; f < F; ++f)
-        cw[f][lg] = __builtin_amdgcn_raw_buffer_load_b128(
-            crs[f], ((uint32_t)(wave * gw + lg) * 1024u + lane * 16u) | bad, 0, kNonTemporal);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+  for (int f = 0; f < F; ++f) {
+    const int unit = blockIdx.x + (f / TU) * gridDim.x;
+    int seg, n;
+    bool ok;
+    tile_segment(a, KIND, unit, NC, f % TU, seg, n, ok);
+    ok = ok && unit < n_units;
+    crs[f] = make_rsrc((const char*)a.w[seg] + (size_t)(n / 16) * G * 1024, ok ? (uint32_t)G * 1024u : 0u);
+    srs[f] = make_rsrc(a.wscale[seg] + (size_t)(n / 16) * G * 16, ok ? (uint32_t)G * 32u : 0u);
   }
+#pragma unroll
+  for (int lg = 0; lg < GW; ++lg) {
+    const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
+#pragma unroll
+    for (int f = 0; f < F; ++f)
+      sw[f][lg] = __builtin_amdgcn_raw_buffer_load_b16(
+          srs[f], ((uint32_t)(wave * gw + lg) * 32u + (lane & 15) * 2u) | bad, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  auto issue_codes = [&](int lg) {
+    const uint32_t bad = (uint32_t)(lg >= my_g) << 31;
+#pragma unroll
+    for (int f = 0; f < F; ++f)
+      cw[f][lg] = __builtin_amdgcn_raw_buffer_load_b128(
+          crs[f], ((uint32_t)(wave * gw + lg) * 1024u + lane * 16u) | bad, 0, kNonTemporal);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+#pragma unroll
+  for (int lg = 0; lg < D && lg < GW; ++lg) issue_codes(lg);
 
-  for (int i = tid; i < kQ4Waves * GPW * 16; i += kQ4Threads)
-    if ((i & 15) >= M) s_bias[i >> 4][i & 15] = 0.f;  // rows past M (never written by a window)
 #pragma unroll
   for (int r = 0; r < RS_ROWS; ++r) {
     const int m = wave + r * kQ4Waves;
@@ -779,18 +778,23 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
   // k-step covers both; output rows m and m + 8 are added after the
   // cross-wave sums.  Otherwise hi and lo are two products.
   constexpr bool STACK = GPW > 1;
+  // The +136 bias of the code operands is cancelled by the product of the same
+  // x with -136 (bf16 0xC308), shared by the block's tiles and added to each
+  // tile's group sum before the scale.
+  const bf16x8 m136 = __builtin_bit_cast(bf16x8, u32x4{0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u});
   auto compute_group = [&](int lg) {
     const int slot = wave * GPW + lg % GPW;
-    const floatx4 cb = *(const floatx4*)&s_bias[slot][4 * kq];
+    floatx4 pb = floatx4{0.f, 0.f, 0.f, 0.f};
     if constexpr (STACK) {
       const unsigned char* xa =
           s_win + (slot * M + min(lane & 7, M - 1)) * kQ4RowBlock + kq * 32 + ((lane >> 3) & 1) * 16;
       floatx4 p[F];
 #pragma unroll
-      for (int f = 0; f < F; ++f) p[f] = cb;
+      for (int f = 0; f < F; ++f) p[f] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bf16x8 xv = *(const bf16x8*)(xa + j * 128);
+        pb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, m136, pb, 0, 0, 0);
 #pragma unroll
         for (int f = 0; f < F; ++f)
           p[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xv, q4_operand(cw[f][lg][j]), p[f], 0, 0, 0);
@@ -799,19 +803,21 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
       for (int f = 0; f < F; ++f) {
         const float sc = bf16_bits_to_f32((uint16_t)sw[f][lg]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, p[f][r], acc[f][r]);
+        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, p[f][r] + pb[r], acc[f][r]);
       }
     } else {
       const unsigned char* xb = s_win + (slot * M + min(lane & 15, M - 1)) * kQ4RowBlock + kq * 32;
       floatx4 ph[F], pl[F];
 #pragma unroll
       for (int f = 0; f < F; ++f) {
-        ph[f] = cb;
+        ph[f] = floatx4{0.f, 0.f, 0.f, 0.f};
         pl[f] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bf16x8 hi = *(const bf16x8*)(xb + j * 128), lo = *(const bf16x8*)(xb + j * 128 + 16);
+        pb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, m136, pb, 0, 0, 0);
+        pb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, m136, pb, 0, 0, 0);
 #pragma unroll
         for (int f = 0; f < F; ++f) {
           const bf16x8 b = q4_operand(cw[f][lg][j]);
@@ -823,7 +829,7 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
       for (int f = 0; f < F; ++f) {
         const float sc = bf16_bits_to_f32((uint16_t)sw[f][lg]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, ph[f][r] + pl[f][r], acc[f][r]);
+        for (int r = 0; r < 4; ++r) acc[f][r] = fmaf(sc, (ph[f][r] + pl[f][r]) + pb[r], acc[f][r]);
       }
     }
   };
@@ -845,6 +851,7 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
 #pragma unroll
     for (int i = 0; i < GPW; ++i) {
       const int lg = w * GPW + i;
+      if (lg + D < GW) issue_codes(lg + D);
       if (lg < GW && lg < my_g) compute_group(lg);
     }
   }
