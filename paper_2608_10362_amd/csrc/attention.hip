@@ -171,23 +171,34 @@ __device__ __forceinline__ void split_hilo(const float* v, bf16x8& hi, bf16x8& l
   }
 }
 
+// Reductions over the 16 lanes of a row of the wave (lanes 16k .. 16k+15)
+// with DPP moves: swaps within quads, then the half-row and row mirrors.
+// Every lane ends with the same value (each step combines two equal-order
+// partial results, and both operations commute).
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  v = fmaxf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_mov<0x141>(v));  // row_half_mirror
+  return fmaxf(v, dpp_mov<0x140>(v));  // row_mirror
 }
 __device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  return v + dpp_mov<0x140>(v);
 }
 
 // Dynamic LDS: per wave a P tile [16][36] (the transposed read of P V), then,
-// reused once every wave is past P V, the merge buffers [NW][RS][HD] of O and
-// [NW][RS][2] of (max, sum), RS = query rows of the tile.
+// reused once every wave is past P V, the merge buffers [NW][RS][HD + 4] of
+// O (rows padded against bank conflicts) and [NW][RS][2] of (max, sum), RS =
+// query rows of the tile.
 __host__ __device__ inline size_t attn_block_lds(int NW, int RS, int HD) {
   const size_t p = (size_t)NW * 16 * (kSubKeys + 4);
-  const size_t m = (size_t)NW * RS * (HD + 2);
+  const size_t m = (size_t)NW * RS * (HD + 6);
   return (p > m ? p : m) * sizeof(float);
 }
 
@@ -383,38 +394,53 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
 
   // Merge the waves' partials of this part (LDS reused: every wave is past P V).
   __syncthreads();
-  float* so = smem;                            // [NW][RS][HD]
-  float* sml = smem + (size_t)NW * RS * HD;    // [NW][RS][2]
+  constexpr int OS = HD + 4;                   // row stride of the O partials
+  float* so = smem;                            // [NW][RS][OS]
+  float* sml = smem + (size_t)NW * RS * OS;    // [NW][RS][2]
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int row = 4 * grp + r;
     if (row >= RS) continue;
     const bool live = qpos[r] >= 0 && mx[r] != -INFINITY;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) so[((size_t)wave * RS + row) * HD + dt * 16 + c16] = live ? of[dt][r] : 0.f;
+    for (int dt = 0; dt < DT; ++dt) so[((size_t)wave * RS + row) * OS + dt * 16 + c16] = live ? of[dt][r] : 0.f;
     if (c16 == 0) {
       sml[((size_t)wave * RS + row) * 2] = live ? mx[r] : -INFINITY;
       sml[((size_t)wave * RS + row) * 2 + 1] = live ? sm[r] : 0.f;
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < RS * HD; i += NW * kWave) {
-    const int row = i / HD, d = i % HD, qc = mt * 16 + row;
+  // One wave per row: the waves' weights exp(m_w - M) are uniform across the
+  // wave, each lane sums HD / 64 dims over the waves in fixed order.
+  constexpr int DPL = HD >= 64 ? HD / 64 : 1;
+  constexpr int MAXW = LOOP ? kLoopWaves : kMaxPartWaves;
+  for (int row = wave; row < RS; row += NW) {  // (wave-uniform)
     float M = -INFINITY;
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sml[((size_t)w * RS + row) * 2]);
+#pragma unroll
+    for (int w = 0; w < MAXW; ++w)
+      if (w < NW) M = fmaxf(M, sml[((size_t)w * RS + row) * 2]);
     if (M == -INFINITY) continue;  // no key of this part is visible to the row
-    float L = 0.f, O = 0.f;
-    for (int w = 0; w < NW; ++w) {
+    float L = 0.f, O[DPL];
+#pragma unroll
+    for (int j = 0; j < DPL; ++j) O[j] = 0.f;
+#pragma unroll
+    for (int w = 0; w < MAXW; ++w) {
+      if (w >= NW) break;
       const float mw = sml[((size_t)w * RS + row) * 2];
       if (mw == -INFINITY) continue;
       const float e = expf(mw - M);
       L += e * sml[((size_t)w * RS + row) * 2 + 1];
-      O += e * so[((size_t)w * RS + row) * HD + d];
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) O[j] += e * so[((size_t)w * RS + row) * OS + lane + 64 * j];
     }
+    const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
     const size_t slot = ((size_t)qrow * H + head) * n_part + part;
-    a.o_part[slot * HD + d] = O;
-    if (d == 0) {
+#pragma unroll
+    for (int j = 0; j < DPL; ++j)
+      if (lane + 64 * j < HD) a.o_part[slot * HD + lane + 64 * j] = O[j];
+    if (lane == 0) {
       a.ml_part[2 * slot] = M;
       a.ml_part[2 * slot + 1] = L;
     }
