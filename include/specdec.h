@@ -174,7 +174,10 @@ SPECDEC_API specdec_status specdec_pack_weights_fmt(const specdec_model_desc* de
  * packed = NULL and use the row-major matrices of `weights`.
  * `workspace` (device, >= specdec_workspace_bytes, 256-byte aligned) belongs
  * to the handle until specdec_model_destroy; two handles may share one
- * workspace only if their calls never overlap.  Launches nothing.
+ * workspace only if their calls never overlap.  Launches nothing (the
+ * handle's first forward pass clears a region of the workspace, the bf16
+ * attention's combine counters, with a small kernel on its stream; the
+ * counters are back at zero after every attention launch).
  * Errors: INVALID_ARG (nulls), SHAPE (unsupported dims), HIP. */
 SPECDEC_API specdec_status specdec_model_create(const specdec_model_desc* desc, const specdec_weights* weights,
                                     int32_t n_layers_used, const void* packed, size_t packed_bytes,

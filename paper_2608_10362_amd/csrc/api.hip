@@ -37,6 +37,8 @@ struct specdec_model {
   float* logits;
   void* samp;  // scratch of the draft's softmax / draw kernels
   float* ypart = nullptr;  // split-K partials of the wide residual GEMMs (passes of more than 64 rows)
+  uint32_t* attn_ctr = nullptr;           // bf16: the attention's combine counters (zero between launches)
+  mutable bool attn_ctr_ready = false;    // set once they have been zeroed on a stream
   int chunk, n_split_max;
   // layer-0 launches of the last forward pass, for specdec_time_kernel
   mutable bool rec_valid[SPECDEC_KERNEL_KINDS] = {};
@@ -94,7 +96,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, ypart, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, ypart, ctr, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -124,6 +126,7 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.logits = take(R * d->vocab * 4);
   w.samp = take(sampling_scratch_bytes(max_rows, 1, d->vocab));
   w.ypart = take(wide ? wide_ypart_floats(d->d_model) * 4 : 0);
+  w.ctr = take(d->dtype == SPECDEC_BF16 ? attention_counter_count(H, G, max_rows) * 4 : 0);
   w.total = off;
   return w;
 }
@@ -312,6 +315,11 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   at.o = m->o;
   at.status = kv_status(kv);
   at.seq_bound = M / ra.rps > 1;
+  if (m->attn_ctr && !m->attn_ctr_ready) {  // (a fill kernel: a capturing caller may record it)
+    SD_TRY(launch_fill_u32(m->attn_ctr, attention_counter_count(H, G, m->max_rows), 0u, s));
+    m->attn_ctr_ready = true;
+  }
+  at.counters = m->attn_ctr;
 
   for (int l = 0; l < m->n_layers; ++l) {
     GemmArgs q = base;  // RMSNorm + Q|K|V projections
@@ -567,6 +575,7 @@ specdec_status specdec_model_create_fmt(const specdec_model_desc* desc, const sp
   m->logits = (float*)(base + L.logits);
   m->samp = base + L.samp;
   m->ypart = gemm_wide(desc->dtype, max_rows) ? (float*)(base + L.ypart) : nullptr;
+  m->attn_ctr = desc->dtype == SPECDEC_BF16 ? (uint32_t*)(base + L.ctr) : nullptr;
   m->chunk = L.chunk;
   m->n_split_max = L.n_split;
   *out = m;

@@ -232,9 +232,9 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     const RowDesc last = a.rows[r0 + rps - 1];
     if (last.valid) {
       const int first = part * S * kSubKeys;
-      if (first > last.pos) return;  // (block-uniform, before any barrier) no key of this part is visible
+      if (first > last.pos) sub_here = 0;  // (block-uniform) no key of this part is visible
       const int need = (last.pos + 1 - first + kSubKeys - 1) / kSubKeys;
-      sub_here = need < sub_here ? need : sub_here;
+      sub_here = need < 0 ? 0 : (need < sub_here ? need : sub_here);
     }
   }
   const uint16_t* kb = k_block<uint16_t>(a.kv, a.layer, b, g);
@@ -437,13 +437,88 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
     const size_t slot = ((size_t)qrow * H + head) * n_part + part;
+    // (agent-scope stores: visible to the combining block on any XCD once
+    // they have completed)
 #pragma unroll
     for (int j = 0; j < DPL; ++j)
-      if (lane + 64 * j < HD) a.o_part[slot * HD + lane + 64 * j] = O[j];
+      if (lane + 64 * j < HD)
+        __hip_atomic_store(&a.o_part[slot * HD + lane + 64 * j], O[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (lane == 0) {
-      a.ml_part[2 * slot] = M;
-      a.ml_part[2 * slot + 1] = L;
+      __hip_atomic_store(&a.ml_part[2 * slot], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.ml_part[2 * slot + 1], L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+  }
+  if (!a.counters) return;
+
+  // The last block of this (sequence, tile, kv head) to finish combines the
+  // parts: every wave's partial stores have completed before the block's
+  // single counter increment, and the combining block reads the partials
+  // with agent-scope loads.  The counter goes back to zero for the next launch.
+  __shared__ int s_last;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int n_mt = gridDim.x / n_part;
+    uint32_t* ctr = a.counters + ((size_t)b * n_mt + mt) * G + g;
+    const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = old == (uint32_t)(n_part - 1);
+    if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = last;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  for (int row = wave; row < RS; row += NW) {  // (wave-uniform) one wave per query row of the tile
+    const int qc = mt * 16 + row;
+    const int qrow = r0 + qc / group, head = g * group + qc % group;
+    const RowDesc rd = a.rows[qrow];
+    float* o = a.o + ((size_t)qrow * H + head) * HD;
+    if (!rd.valid) {
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) o[lane + 64 * j] = 0.f;
+      continue;
+    }
+    // parts holding keys <= pos (the last part also holds the remainder)
+    const int nch = min(rd.pos / a.chunk + 1, n_part);
+    if (rd.pos + 1 > a.max_ctx && lane == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
+    const size_t base = ((size_t)qrow * H + head) * n_part;
+    // lane p < nch: part p's (max, sum); the first parts' outputs in the same round trip
+    constexpr int PB = 8;
+    const int pl = min(lane, nch - 1);
+    const float mp = __hip_atomic_load(&a.ml_part[2 * (base + pl)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const float lp = __hip_atomic_load(&a.ml_part[2 * (base + pl) + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    float acc[DPL];
+#pragma unroll
+    for (int j = 0; j < DPL; ++j) acc[j] = 0.f;
+    float mx = 0.f, wgt = 0.f;
+    for (int p0 = 0; p0 < nch; p0 += PB) {  // (wave-uniform)
+      float ov[PB][DPL];
+#pragma unroll
+      for (int pp = 0; pp < PB; ++pp) {
+        const int p = min(p0 + pp, nch - 1);  // (parts past nch get weight 0 below)
+#pragma unroll
+        for (int j = 0; j < DPL; ++j)
+          ov[pp][j] = lane + 64 * j < HD ? __hip_atomic_load(&a.o_part[(base + p) * HD + lane + 64 * j],
+                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                         : 0.f;
+      }
+      if (p0 == 0) {
+        mx = wave_max(lane < nch ? mp : -INFINITY);
+        wgt = lane < nch ? expf(mp - mx) : 0.f;
+      }
+#pragma unroll
+      for (int pp = 0; pp < PB; ++pp) {
+        const float w = __shfl(wgt, (p0 + pp) & 63, kWave);
+        const float wv = p0 + pp < nch ? w : 0.f;
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) acc[j] += wv * ov[pp][j];
+      }
+    }
+    const float L = wave_sum(wgt * lp);
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int j = 0; j < DPL; ++j)
+      if (lane + 64 * j < HD) o[lane + 64 * j] = acc[j] * inv;
   }
 }
 
@@ -629,6 +704,23 @@ hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
+  const size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+size_t attention_counter_count(int n_heads, int n_kv_heads, int max_rows) {
+  // sequences x query tiles <= max_rows * group / 16 + max_rows
+  const size_t group = (size_t)(n_heads / n_kv_heads);
+  return (size_t)n_kv_heads * ((size_t)max_rows * group / 16 + (size_t)max_rows + 1);
+}
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int B = a.M / a.rps;
   AttnArgs ab = a;  // the bf16 path chooses its own parts
@@ -662,6 +754,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     if (NW > kMaxPartWaves || attn_block_lds(NW, RS, a.head_dim) > 65536) return hipErrorInvalidValue;
     ab.n_split = n_part;
     ab.chunk = S * kSubKeys;
+    if (n_part > kWave) ab.counters = nullptr;  // (the in-kernel combine holds one part per lane)
     dim3 grid(n_part * n_mt, a.n_kv_heads, B);
     const size_t lds = attn_block_lds(NW, RS, a.head_dim);
     const bool loop = S > NW;
@@ -682,6 +775,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (ab.kv.dtype == SPECDEC_BF16 && ab.counters) return hipSuccess;  // combined by the blocks
   if (ab.kv.dtype == SPECDEC_BF16 && ab.n_split <= kCombineMaxSplits) {
     switch (ab.head_dim) {
       case 32: hipLaunchKernelGGL((attn_combine_wave_kernel<32>), dim3(ab.n_heads, ab.M), dim3(64), 0, s, ab); break;

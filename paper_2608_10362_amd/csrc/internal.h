@@ -156,7 +156,14 @@ struct AttnArgs {
   float* o;              // [M, h hd]
   int32_t* status;
   int seq_bound;         // 1: bound each sequence's keys by its own last row (batches of several sequences)
+  // bf16: one counter per (sequence, query tile, kv head), zero between launches;
+  // the last block of a (sequence, tile, head) to finish combines the parts
+  // (null: a separate combine kernel does).
+  uint32_t* counters;
 };
+// Counters a model workspace holds for the attention's in-kernel combine.
+size_t attention_counter_count(int n_heads, int n_kv_heads, int max_rows);
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s);
 int attention_chunk(int dtype, int head_dim);  // keys per split of the attention kernel
 int device_compute_units();                    // CUs of the current device (cached)
 hipError_t launch_rope_append(const AttnArgs& a, hipStream_t s);
