@@ -247,22 +247,26 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
   int qpos[4] = {-1, -1, -1, -1};
   float* pbuf = smem + (size_t)wave * 16 * (kSubKeys + 4);
 
-  if (wave < sub_here) {  // (wave-uniform) a wave past the part's sub-chunks only joins the merge
-    // Every load of the first sub-chunk is issued before anything waits,
-    // smallest first (loads complete in order, so waiting for an early one never
-    // waits for a later one): the row descriptors, the K fragments, Q, then the
-    // V fragments.  Row descriptors and Q go through range-checked buffer loads.
+  // Every load of the first sub-chunk is issued before anything waits,
+  // smallest first (loads complete in order, so waiting for an early one never
+  // waits for a later one): the row descriptors (every wave: the combining
+  // block reads them from its lanes too), the K fragments, Q, then the V
+  // fragments.  Row descriptors and Q go through range-checked buffer loads.
+  // Lane l < 16 holds the descriptor of the row of query l of the tile
+  // (queries qa = mt*16 + l; rows r0 + qa / group).  (Only the two fields
+  // used: a wider load leaves dead destination registers the allocator
+  // reuses, which forces a wait for the load.)
+  const int ql = mt * 16 + lane;
+  int rd_pos, rd_valid;
+  {
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(const_cast<RowDesc*>(a.rows), (short)0,
                                                                          a.M * (int)sizeof(RowDesc), 0x00020000);
-    // Lane l < 16 holds the descriptor of the row of query l of the tile
-    // (queries qa = mt*16 + l; rows r0 + qa / group).  (Only the two fields
-    // used: a wider load leaves dead destination registers the allocator
-    // reuses, which forces a wait for the load.)
-    const int ql = mt * 16 + lane;
     const uint32_t roff = ((uint32_t)(r0 + min(ql, nq - 1) / group) * (uint32_t)sizeof(RowDesc)) |
                           ((uint32_t)(lane >= 16 || ql >= nq) << 31);
-    const int rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
-    const int rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
+    rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
+    rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
+  }
+  if (wave < sub_here) {  // (wave-uniform) a wave past the part's sub-chunks only joins the merge
     // K fragments of a sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity);
     // V fragments: DT contiguous 1 KB fragments (32 positions x 16 dims each).
     u32x4 kf[NT][KST], vf[DT];
@@ -415,24 +419,31 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
   constexpr int DPL = HD >= 64 ? HD / 64 : 1;
   constexpr int MAXW = LOOP ? kLoopWaves : kMaxPartWaves;
   for (int row = wave; row < RS; row += NW) {  // (wave-uniform)
+    // (every read first, then the arithmetic: a wave past NW or without keys
+    // gets weight 0, and adding 0 * a finite partial changes no sum)
+    float mw[MAXW], lw[MAXW], ow[MAXW][DPL];
+#pragma unroll
+    for (int w = 0; w < MAXW; ++w) {
+      const size_t wr = (size_t)min(w, NW - 1) * RS + row;
+      mw[w] = sml[wr * 2];
+      lw[w] = sml[wr * 2 + 1];
+#pragma unroll
+      for (int j = 0; j < DPL; ++j) ow[w][j] = lane + 64 * j < HD ? so[wr * OS + lane + 64 * j] : 0.f;
+    }
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < MAXW; ++w)
-      if (w < NW) M = fmaxf(M, sml[((size_t)w * RS + row) * 2]);
+      if (w < NW) M = fmaxf(M, mw[w]);
     if (M == -INFINITY) continue;  // no key of this part is visible to the row
     float L = 0.f, O[DPL];
 #pragma unroll
     for (int j = 0; j < DPL; ++j) O[j] = 0.f;
 #pragma unroll
     for (int w = 0; w < MAXW; ++w) {
-      if (w >= NW) break;
-      const float mw = sml[((size_t)w * RS + row) * 2];
-      if (mw == -INFINITY) continue;
-      const float e = expf(mw - M);
-      L += e * sml[((size_t)w * RS + row) * 2 + 1];
+      const float e = w < NW && mw[w] != -INFINITY ? expf(mw[w] - M) : 0.f;
+      L += e * lw[w];
 #pragma unroll
-      for (int j = 0; j < DPL; ++j)
-        if (lane + 64 * j < HD) O[j] += e * so[((size_t)w * RS + row) * OS + lane + 64 * j];
+      for (int j = 0; j < DPL; ++j) O[j] += e * ow[w][j];
     }
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
@@ -470,7 +481,9 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
   for (int row = wave; row < RS; row += NW) {  // (wave-uniform) one wave per query row of the tile
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
-    const RowDesc rd = a.rows[qrow];
+    RowDesc rd;
+    rd.pos = __shfl(rd_pos, row, kWave);  // (lane `row` loaded this query's row descriptor)
+    rd.valid = __shfl(rd_valid, row, kWave);
     float* o = a.o + ((size_t)qrow * H + head) * HD;
     if (!rd.valid) {
 #pragma unroll
