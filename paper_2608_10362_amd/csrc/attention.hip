@@ -396,6 +396,33 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     }
   }
 
+  constexpr int DPL = HD >= 64 ? HD / 64 : 1;
+  if (NW == 1) {  // (block-uniform) the wave's own (max, sum, O) rows are the part's partials
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 4 * grp + r;
+      if (row >= RS || qpos[r] < 0 || mx[r] == -INFINITY) continue;
+      const int qc = mt * 16 + row;
+      const size_t slot = ((size_t)(r0 + qc / group) * H + g * group + qc % group) * n_part + part;
+      if (a.counters) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          __hip_atomic_store(&a.o_part[slot * HD + dt * 16 + c16], of[dt][r], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        if (c16 == 0) {
+          __hip_atomic_store(&a.ml_part[2 * slot], mx[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(&a.ml_part[2 * slot + 1], sm[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      } else {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) a.o_part[slot * HD + dt * 16 + c16] = of[dt][r];
+        if (c16 == 0) {
+          a.ml_part[2 * slot] = mx[r];
+          a.ml_part[2 * slot + 1] = sm[r];
+        }
+      }
+    }
+  } else {
   // Merge the waves' partials of this part (LDS reused: every wave is past P V).
   __syncthreads();
   constexpr int OS = HD + 4;                   // row stride of the O partials
@@ -416,48 +443,66 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
   __syncthreads();
   // One wave per row: the waves' weights exp(m_w - M) are uniform across the
   // wave, each lane sums HD / 64 dims over the waves in fixed order.
-  constexpr int DPL = HD >= 64 ? HD / 64 : 1;
   constexpr int MAXW = LOOP ? kLoopWaves : kMaxPartWaves;
   for (int row = wave; row < RS; row += NW) {  // (wave-uniform)
-    // (every read first, then the arithmetic: a wave past NW or without keys
-    // gets weight 0, and adding 0 * a finite partial changes no sum)
-    float mw[MAXW], lw[MAXW], ow[MAXW][DPL];
-#pragma unroll
-    for (int w = 0; w < MAXW; ++w) {
-      const size_t wr = (size_t)min(w, NW - 1) * RS + row;
-      mw[w] = sml[wr * 2];
-      lw[w] = sml[wr * 2 + 1];
-#pragma unroll
-      for (int j = 0; j < DPL; ++j) ow[w][j] = lane + 64 * j < HD ? so[wr * OS + lane + 64 * j] : 0.f;
-    }
+    // The waves' partials in groups of 4: every read of a group first, then
+    // the arithmetic (a wave past NW or without keys gets weight 0, and adding
+    // 0 * a finite partial changes no sum).
+    constexpr int WG = 4;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < MAXW; ++w)
-      if (w < NW) M = fmaxf(M, mw[w]);
+    for (int w0 = 0; w0 < MAXW; w0 += WG) {
+      if (w0 >= NW) break;
+#pragma unroll
+      for (int w = w0; w < w0 + WG; ++w)
+        if (w < NW) M = fmaxf(M, sml[((size_t)w * RS + row) * 2]);
+    }
     if (M == -INFINITY) continue;  // no key of this part is visible to the row
     float L = 0.f, O[DPL];
 #pragma unroll
     for (int j = 0; j < DPL; ++j) O[j] = 0.f;
 #pragma unroll
-    for (int w = 0; w < MAXW; ++w) {
-      const float e = w < NW && mw[w] != -INFINITY ? expf(mw[w] - M) : 0.f;
-      L += e * lw[w];
+    for (int w0 = 0; w0 < MAXW; w0 += WG) {
+      if (w0 >= NW) break;
+      float mw[WG], lw[WG], ow[WG][DPL];
 #pragma unroll
-      for (int j = 0; j < DPL; ++j) O[j] += e * ow[w][j];
+      for (int i = 0; i < WG; ++i) {
+        const size_t wr = (size_t)min(w0 + i, NW - 1) * RS + row;
+        mw[i] = sml[wr * 2];
+        lw[i] = sml[wr * 2 + 1];
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) ow[i][j] = lane + 64 * j < HD ? so[wr * OS + lane + 64 * j] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < WG; ++i) {
+        const float e = w0 + i < NW && mw[i] != -INFINITY ? expf(mw[i] - M) : 0.f;
+        L += e * lw[i];
+#pragma unroll
+        for (int j = 0; j < DPL; ++j) O[j] += e * ow[i][j];
+      }
     }
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
     const size_t slot = ((size_t)qrow * H + head) * n_part + part;
-    // (agent-scope stores: visible to the combining block on any XCD once
-    // they have completed)
+    if (a.counters) {  // (agent-scope stores: visible to the combining block on any XCD once completed)
 #pragma unroll
-    for (int j = 0; j < DPL; ++j)
-      if (lane + 64 * j < HD)
-        __hip_atomic_store(&a.o_part[slot * HD + lane + 64 * j], O[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (lane == 0) {
-      __hip_atomic_store(&a.ml_part[2 * slot], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.ml_part[2 * slot + 1], L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD)
+          __hip_atomic_store(&a.o_part[slot * HD + lane + 64 * j], O[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (lane == 0) {
+        __hip_atomic_store(&a.ml_part[2 * slot], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.ml_part[2 * slot + 1], L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    } else {  // (read by the combine kernel after this launch)
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) a.o_part[slot * HD + lane + 64 * j] = O[j];
+      if (lane == 0) {
+        a.ml_part[2 * slot] = M;
+        a.ml_part[2 * slot + 1] = L;
+      }
     }
+  }
   }
   if (!a.counters) return;
 
@@ -767,7 +812,10 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     if (NW > kMaxPartWaves || attn_block_lds(NW, RS, a.head_dim) > 65536) return hipErrorInvalidValue;
     ab.n_split = n_part;
     ab.chunk = S * kSubKeys;
-    if (n_part > kWave) ab.counters = nullptr;  // (the in-kernel combine holds one part per lane)
+    // In-kernel combine: one part per lane, and at most two query rows per wave
+    // of the combining block (its rows go one after another); otherwise the
+    // separate combine kernel (one wave per row and head).
+    if (n_part > kWave || (RS + NW - 1) / NW > 2) ab.counters = nullptr;
     dim3 grid(n_part * n_mt, a.n_kv_heads, B);
     const size_t lds = attn_block_lds(NW, RS, a.head_dim);
     const bool loop = S > NW;
