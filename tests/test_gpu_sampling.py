@@ -213,3 +213,62 @@ def test_kv_commit_all_accept_counts(role):
     kv.set_state(lens, pend, npend)
     binding.specdec_kv_commit(kv, g, role, i32(np.full(B, -1, np.int32)), i32(d), g, i32(nxt))
     np.testing.assert_array_equal(kv.read_state()["len"], lens)
+
+
+def _chi2_pvalue(counts, expected):
+    """Pearson chi-square p-value; bins with expected count below 5 are pooled."""
+    from scipy import stats
+    counts, expected = np.asarray(counts, float), np.asarray(expected, float)
+    small = expected < 5
+    if small.any():
+        counts = np.append(counts[~small], counts[small].sum())
+        expected = np.append(expected[~small], expected[small].sum())
+    chi2 = ((counts - expected) ** 2 / expected).sum()
+    return float(stats.chi2.sf(chi2, len(counts) - 1))
+
+
+def test_accept_distribution_matches_the_closed_form():
+    """Statistics of the device accept over many independent sequences (Philox
+    draws): with d_i ~ q_i, position i is accepted with probability
+    alpha_i = sum_x min(p_i(x), q_i(x)), so P(A = k) = alpha_1..alpha_k (1 - alpha_{k+1})
+    and P(A = gamma) = prod alpha_i (Sec. 2, speculative sampling); and the first
+    emitted token (d_1 when accepted, else the residual draw) is distributed
+    as p_1 exactly."""
+    torch = torch_cuda()
+    B, g, V, steps = 8192, 3, 50, 3
+    p1 = synth.make_prob_rows(g + 1, V, seed=41, concentration=0.8).astype(np.float64)
+    noise = synth.make_prob_rows(g, V, seed=42, concentration=0.8).astype(np.float64)
+    q1 = 0.6 * p1[:g] + 0.4 * noise
+    p1 = (p1 / p1.sum(axis=1, keepdims=True)).astype(np.float32)
+    q1 = (q1 / q1.sum(axis=1, keepdims=True)).astype(np.float32)
+    p = np.broadcast_to(p1, (B, g + 1, V)).copy()
+    q = np.broadcast_to(q1, (B, g, V)).copy()
+    rng = np.random.default_rng(43)
+    nacc = torch.zeros(B, dtype=torch.int32, device="cuda")
+    nxt = torch.zeros(B, dtype=torch.int32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = binding.accept_workspace(B, g, V)
+    A_all, first = [], []
+    for step in range(steps):
+        # drafts d_i ~ q_i (the draws of the draft model, here independent test inputs)
+        cdf = np.cumsum(q1.astype(np.float64), axis=1)
+        u = rng.random((B, g))
+        d = np.stack([np.minimum(np.searchsorted(cdf[i], u[:, i] * cdf[i, -1], side="right"), V - 1)
+                      for i in range(g)], axis=1).astype(np.int32)
+        binding.specdec_accept(B, g, V, binding.INPUT_PROBS, 1.0, f32(p), f32(q), i32(d), g, None, 9, step, nacc, nxt,
+                               status, ws)
+        A, n = nacc.cpu().numpy(), nxt.cpu().numpy()
+        assert int(status.item()) == 0
+        A_all.append(A)
+        first.append(np.where(A >= 1, d[:, 0], n))
+    A_all, first = np.concatenate(A_all), np.concatenate(first)
+    N = A_all.size
+    alpha = np.minimum(p1[:g].astype(np.float64), q1.astype(np.float64)).sum(axis=1)
+    pk = [np.prod(alpha[:k]) * (1 - alpha[k]) for k in range(g)] + [np.prod(alpha)]
+    hist_a = np.bincount(A_all, minlength=g + 1)
+    pa = _chi2_pvalue(hist_a, N * np.array(pk))
+    hist_t = np.bincount(first, minlength=V)
+    pt = _chi2_pvalue(hist_t, N * p1[0].astype(np.float64))
+    log(f"accept lengths {hist_a.tolist()} vs expected {np.round(N * np.array(pk)).astype(int).tolist()} "
+        f"(chi-square p = {pa:.3g}); first-token chi-square p = {pt:.3g} over {N} sequences")
+    assert pa > 1e-3 and pt > 1e-3
