@@ -794,6 +794,9 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
       // takes the remainder), the blocks about filling the CUs once.
       S = (int)((n_sub * units + cus / 2) / cus);
       S = S < 1 ? 1 : (S > kMaxPartWaves ? kMaxPartWaves : S);  // (reduced below while the last part is too big)
+      // (more units than CUs: a part never holds more sub-chunks than the keys
+      // have, so its waves take one sub-chunk each and never loop)
+      S = std::max(1, std::min(S, n_sub));
       for (;; --S) {
         n_part = n_sub / S > 0 ? n_sub / S : 1;
         NW = n_sub - (n_part - 1) * S;
@@ -819,6 +822,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     dim3 grid(n_part * n_mt, a.n_kv_heads, B);
     const size_t lds = attn_block_lds(NW, RS, a.head_dim);
     const bool loop = S > NW;
+    if (loop && NW > kLoopWaves) return hipErrorInvalidValue;  // (the looping kernel's block bound)
 #define SD_ATTN(HDV)                                                                                       \
   if (loop) hipLaunchKernelGGL((attn_block_kernel<HDV, true>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); \
   else hipLaunchKernelGGL((attn_block_kernel<HDV, false>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW);

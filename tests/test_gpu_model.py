@@ -214,6 +214,14 @@ def test_bf16_7b_shape_multi_request_ragged():
     _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=2)
 
 
+def test_bf16_7b_shape_many_short_sequences():
+    # 10 sequences of at most ~250 keys, gamma 6 (70 rows): more (kv head,
+    # sequence) units than CUs and fewer than 12 sub-chunks of 32 keys per
+    # sequence, so every attention part is a whole sequence, one wave per sub-chunk
+    lengths = synth.make_ragged_lengths(10, 100, 250, seed=6)
+    _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=5)
+
+
 def test_bf16_7b_shape_long_context_looping_attention():
     # 2 sequences of 4500 and 6100 keys: 188 sub-chunks of 32 keys over 64
     # (kv head, sequence) units -> parts of 8 sub-chunks on 4-wave blocks, each
