@@ -65,6 +65,20 @@ __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
   return v;
 }
+// wave_sum of N values at once: the same butterfly per value (bit-identical
+// results), each level's N shuffles issued before any of their sums, so the
+// N reductions share one shuffle round trip per level instead of taking N.
+template <int N>
+__device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float s[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) s[i] = __shfl_xor(v[i], o, kWave);
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] += s[i];
+  }
+}
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));

@@ -507,17 +507,23 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   }
   // s_m = 1/sqrt(sum_p ss[p][m] / K + eps): lanes sum their partials in p order
   // (held ones first, then any beyond 64*RS_P), fixed shuffle tree.
+  {
+    float t[RS_ROWS];
 #pragma unroll
-  for (int r = 0; r < RS_ROWS; ++r) {
-    const int m = wave + r * kMfmaWaves;
-    if (m >= MP) break;
-    float t = 0.f;
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kMfmaWaves;
+      t[r] = 0.f;
 #pragma unroll
-    for (int i = 0; i < RS_P; ++i) t += rs_v[r][i];
-    if (a.ss_in && m < a.M)
-      for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t += a.ss_in[(size_t)p * a.ss_ld + m];
-    t = wave_sum(t);
-    if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+      for (int i = 0; i < RS_P; ++i) t[r] += rs_v[r][i];
+      if (a.ss_in && m < a.M)
+        for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t[r] += a.ss_in[(size_t)p * a.ss_ld + m];
+    }
+    wave_sum_n(t);
+#pragma unroll
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kMfmaWaves;
+      if (lane == 0 && m < MP) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t[r] / (float)a.K + a.eps) : 1.0f;
+    }
   }
   if constexpr (HOIST) {
 #pragma unroll
@@ -747,16 +753,23 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
 #pragma unroll
   for (int lg = 0; lg < D && lg < GW; ++lg) issue_codes(lg);
 
+  {
+    float t[RS_ROWS];
 #pragma unroll
-  for (int r = 0; r < RS_ROWS; ++r) {
-    const int m = wave + r * kQ4Waves;
-    float t = 0.f;
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kQ4Waves;
+      t[r] = 0.f;
 #pragma unroll
-    for (int i = 0; i < RS_P; ++i) t += rs_v[r][i];
-    if (a.ss_in && m < M)
-      for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t += a.ss_in[(size_t)p * a.ss_ld + m];
-    t = wave_sum(t);
-    if (lane == 0) scale[m] = (a.ss_in && m < M) ? 1.0f / sqrtf(t / (float)K + a.eps) : 1.0f;
+      for (int i = 0; i < RS_P; ++i) t[r] += rs_v[r][i];
+      if (a.ss_in && m < M)
+        for (int p = lane + RS_P * kWave; p < a.n_ss; p += kWave) t[r] += a.ss_in[(size_t)p * a.ss_ld + m];
+    }
+    wave_sum_n(t);
+#pragma unroll
+    for (int r = 0; r < RS_ROWS; ++r) {
+      const int m = wave + r * kQ4Waves;
+      if (lane == 0) scale[m] = (a.ss_in && m < M) ? 1.0f / sqrtf(t[r] / (float)K + a.eps) : 1.0f;
+    }
   }
   if constexpr (QKV) {
 #pragma unroll
@@ -1079,11 +1092,11 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
   for (int u = 0; u < D; ++u) load_w(u, wv[u]);
   if constexpr (SCALE) {
     // s_m = 1/sqrt(sum_p ss[p][m] / K + eps): partial p in lane p, fixed shuffle tree
+    wave_sum_n(rsv);  // (n_ss <= 64: checked by the launcher)
 #pragma unroll
     for (int i = 0; i < RSR; ++i) {
       const int m = wave + 4 * G * i;
-      const float t = wave_sum(rsv[i]);  // (n_ss <= 64: checked by the launcher)
-      if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+      if (lane == 0) scale[m] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(rsv[i] / (float)a.K + a.eps) : 1.0f;
     }
   }
   if constexpr (QKV) {
@@ -1361,11 +1374,11 @@ __global__ __launch_bounds__(kTileThreads) void gemm_bf16_tile(GemmArgs a, int n
   load(0, xv[0], bv[0]);
   load(1, xv[1], bv[1]);
   if constexpr (SCALE) {
+    wave_sum_n(rsv);  // (n_ss <= 64: checked by the launcher)
 #pragma unroll
     for (int i = 0; i < RSR; ++i) {
       const int r = wave + (kTileThreads / kWave) * i, m = m0 + r;
-      const float t = wave_sum(rsv[i]);  // (n_ss <= 64: checked by the launcher)
-      if (lane == 0) scale[r] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(t / (float)a.K + a.eps) : 1.0f;
+      if (lane == 0) scale[r] = (a.ss_in && m < a.M) ? 1.0f / sqrtf(rsv[i] / (float)a.K + a.eps) : 1.0f;
     }
   }
   store(0, xv[0], bv[0]);
