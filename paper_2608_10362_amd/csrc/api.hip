@@ -36,6 +36,8 @@ struct specdec_model {
   float* u;
   float* logits;
   void* samp;  // scratch of the draft's softmax / draw kernels
+  uint16_t* xs_d = nullptr;  // bf16: the stacked x operand of the d_model-column GEMMs (passes of <= 16 rows)
+  uint16_t* xs_f = nullptr;  // bf16: the stacked SwiGLU output, the down projection's x
   float* ypart = nullptr;  // split-K partials of the wide residual GEMMs (passes of more than 64 rows)
   uint32_t* attn_ctr = nullptr;           // bf16: the attention's combine counters (zero between launches)
   mutable bool attn_ctr_ready = false;    // set once they have been zeroed on a stream
@@ -96,7 +98,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, ypart, ctr, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, xs_d, xs_f, ypart, ctr, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -125,6 +127,9 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.u = take(R * d->ffn_dim * 4);
   w.logits = take(R * d->vocab * 4);
   w.samp = take(sampling_scratch_bytes(max_rows, 1, d->vocab));
+  // (stacked operands: two 1 KB fragments per 32 columns)
+  w.xs_d = take(d->dtype == SPECDEC_BF16 ? (size_t)(d->d_model + 31) / 32 * 2048 : 0);
+  w.xs_f = take(d->dtype == SPECDEC_BF16 ? (size_t)(d->ffn_dim + 31) / 32 * 2048 : 0);
   w.ypart = take(wide ? wide_ypart_floats(d->d_model) * 4 : 0);
   w.ctr = take(d->dtype == SPECDEC_BF16 ? attention_counter_count(H, G, max_rows) * 4 : 0);
   w.total = off;
@@ -276,6 +281,14 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   ra.rope_cs = m->rope_cs;
   ra.h = m->h;
   ra.ss = m->ss;
+  // Passes of at most 16 rows on bf16 weights hand x from kernel to kernel also
+  // as a stacked operand (put_stacked): the skinny GEMMs then read one 16-byte
+  // fragment per k-step (two when M > 8) instead of two float32 loads per row
+  // tile.  The O projection keeps the attention's float32 output.
+  const bool stk = dt == SPECDEC_BF16 && m->wfmt != SPECDEC_WEIGHTS_INT4 && M <= 16 && m->xs_d;
+  const int stt = M <= 8 ? 1 : 2;
+  ra.xs = stk ? m->xs_d : nullptr;
+  ra.stt = stt;
   {
     Timed t(SPECDEC_KERNEL_EMBED, s);
     SD_TRY(launch_rows_embed(dt, ra, s));
@@ -293,6 +306,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   base.ss_ld = m->ss_ld;
   base.gain_bf16 = dt == SPECDEC_BF16;
   base.ypart = m->ypart;
+  base.stt = stt;
   int n_ss = 1;
   const int n_resid_blocks = gemm_row_blocks(dt, EPI_RESID, d.d_model, M);
 
@@ -336,6 +350,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     }
     const bool q4 = m->wfmt == SPECDEC_WEIGHTS_INT4;
     if (q4) { q.q4 = 1; q.wscale[0] = m->sq[l]; q.wscale[1] = m->sk[l]; q.wscale[2] = m->sv[l]; }
+    if (stk) q.xs = m->xs_d;
     {
       Timed t(SPECDEC_KERNEL_QKV, s);
       SD_TRY(gemm_rows(dt, q, M, s));
@@ -362,6 +377,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     o.w[0] = m->wo[l]; o.n_seg[0] = d.d_model; o.n_rows = d.d_model; o.kind = EPI_RESID;
     o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss; o.xg_out = m->xg; o.gain_out = m->ffn_norm[l];
     if (q4) { o.q4 = 1; o.wscale[0] = m->so[l]; }
+    if (stk) o.xs_out = m->xs_d;
     {
       Timed t(SPECDEC_KERNEL_O_PROJ, s);
       SD_TRY(gemm_rows(dt, o, M, s));
@@ -375,6 +391,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     gu.w[0] = m->w_gate[l]; gu.w[1] = m->w_up[l]; gu.n_seg[0] = d.ffn_dim; gu.n_seg[1] = d.ffn_dim;
     gu.n_rows = d.ffn_dim; gu.kind = EPI_SWIGLU; gu.out = m->u; gu.ldo = d.ffn_dim;
     if (q4) { gu.q4 = 1; gu.wscale[0] = m->sg[l]; gu.wscale[1] = m->su[l]; }
+    if (stk) { gu.xs = m->xs_d; gu.xs_out = m->xs_f; }
     {
       Timed t(SPECDEC_KERNEL_GATE_UP, s);
       SD_TRY(gemm_rows(dt, gu, M, s));
@@ -387,6 +404,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     dn.out = m->h; dn.ldo = d.d_model; dn.ss_out = m->ss; dn.xg_out = m->xg;
     dn.gain_out = l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm;
     if (q4) { dn.q4 = 1; dn.wscale[0] = m->sd[l]; }
+    if (stk) { dn.xs = m->xs_f; dn.xs_out = m->xs_d; }
     {
       Timed t(SPECDEC_KERNEL_DOWN, s);
       SD_TRY(gemm_rows(dt, dn, M, s));
@@ -398,6 +416,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   hd_.x = m->xg; hd_.ldx = d.d_model; hd_.ss_in = m->ss; hd_.n_ss = n_ss;
   hd_.K = d.d_model; hd_.w[0] = m->lm_head; hd_.n_seg[0] = d.vocab; hd_.n_rows = d.vocab;
   hd_.kind = EPI_STORE; hd_.out = logits; hd_.ldo = d.vocab;
+  if (stk) hd_.xs = m->xs_d;
   {
     Timed t(SPECDEC_KERNEL_LM_HEAD, s);
     SD_TRY(gemm_rows(dt, hd_, M, s));
@@ -574,6 +593,8 @@ specdec_status specdec_model_create_fmt(const specdec_model_desc* desc, const sp
   m->u = (float*)(base + L.u);
   m->logits = (float*)(base + L.logits);
   m->samp = base + L.samp;
+  m->xs_d = desc->dtype == SPECDEC_BF16 ? (uint16_t*)(base + L.xs_d) : nullptr;
+  m->xs_f = desc->dtype == SPECDEC_BF16 ? (uint16_t*)(base + L.xs_f) : nullptr;
   m->ypart = gemm_wide(desc->dtype, max_rows) ? (float*)(base + L.ypart) : nullptr;
   m->attn_ctr = desc->dtype == SPECDEC_BF16 ? (uint32_t*)(base + L.ctr) : nullptr;
   m->chunk = L.chunk;

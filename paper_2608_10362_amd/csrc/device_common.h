@@ -26,6 +26,21 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Stacked bf16 operand of at most 16 activation rows, the x operand of the
+// skinny GEMMs written by the kernels that produce x: per 32-column k-step,
+// stt fragments of 1 KB in MFMA operand order (lane 16*(k%32/8) + row,
+// element k%8).  stt = 1 (at most 8 rows): row m's hi part in fragment row m
+// and its lo part in row 8 + m, so one product gives both; stt = 2 (at most
+// 16 rows): the hi parts in fragment 0, the lo parts in fragment 1.  hi =
+// bf16(v), lo = bf16(v - hi) (round to nearest even, as the GEMMs' own split).
+__device__ __forceinline__ void put_stacked(uint16_t* xs, int stt, int m, int k, float v) {
+  const __bf16 h = (__bf16)v;
+  const __bf16 l = (__bf16)(v - (float)h);
+  const size_t at = (size_t)(k >> 5) * stt * 512 + (size_t)(16 * ((k & 31) >> 3) + m) * 8 + (k & 7);
+  xs[at] = __builtin_bit_cast(uint16_t, h);
+  xs[at + (stt == 1 ? 64 : 512)] = __builtin_bit_cast(uint16_t, l);
+}
+
 template <typename T> struct Storage;
 template <> struct Storage<float> {
   __device__ __forceinline__ static float load(const float* p) { return *p; }

@@ -74,7 +74,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfi
         float* hp = a.out + (size_t)m * a.ldo + n;
         hv = *hp + yfin[m][c];
         *hp = hv;
-        a.xg_out[(size_t)m * a.ldo + n] = hv * load_gain(a.gain_out, a.gain_bf16, n);
+        const float xv = hv * load_gain(a.gain_out, a.gain_bf16, n);
+        a.xg_out[(size_t)m * a.ldo + n] = xv;
+        if (a.xs_out) put_stacked(a.xs_out, a.stt, m, n, xv);
       }
       yfin[m][c] = hv;
     }
@@ -92,7 +94,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int blk, float (*yfi
       if (n < a.n_rows) {
         float g = yfin[m][c] * scale[m];
         float u = yfin[m][H + c] * scale[m];
-        a.out[(size_t)m * a.ldo + n] = silu_f(g) * u;
+        const float y = silu_f(g) * u;
+        a.out[(size_t)m * a.ldo + n] = y;
+        if (a.xs_out) put_stacked(a.xs_out, a.stt, m, n, y);
       }
     }
   }
@@ -220,7 +224,7 @@ struct Q4Frag {
 // MFMA operand layout (16x16x32): lane l holds A[l%16][8(l/16)+j] (x rows),
 // B[8(l/16)+j][l%16] (= W[n0 + l%16][k0 + 8(l/16) + j]: 16 bytes at lane*16 of
 // the packed 1 KB fragment), D[4(l/16)+r][l%16].
-template <int T, int MT, int UB, bool PIPE, int KIND, bool Q4 = false>
+template <int T, int MT, int UB, bool PIPE, int KIND, bool Q4 = false, int XS = 0>
 __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n_tiles) {
   // Q4: INT4 weights (Q4Frag).  A code q is fed to the MFMA as the bf16 value
   // 136 + q (bits 0x4300 | (q + 8): two byte permutes and an OR per four
@@ -228,7 +232,15 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // the same x with the constant -136, shared by the unit's tiles; each
   // k-step's product is then multiplied by the lane's row scale in float32,
   // so the effective weights are code * scale.
+  // XS > 0: x comes as the stacked operand a.xs (put_stacked, XS fragments
+  // per k-step, at most 8 rows when XS = 1, 16 when XS = 2) in place of the
+  // float32 rows: one 16-byte load per fragment and one product per fragment
+  // and tile.  The hi and lo parts accumulate apart (accumulator tiles 0 and
+  // 1, or rows m and 8 + m of tile 0) and are added once per tile before the
+  // cross-wave sums, the same arithmetic for either count of fragments.
+  static_assert(XS == 0 || (MT == 1 && !Q4), "stacked x: bf16 weights, one row tile");
   using WReg = std::conditional_t<Q4, Q4Frag, u32x4>;
+  constexpr int MA = XS ? XS : MT;  // accumulator row tiles
   constexpr int NC = 16 * T;
   constexpr int MP = 16 * MT;
   constexpr int NF = T * MT;              // accumulator fragments per wave
@@ -262,14 +274,14 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   const int my_tiles = (n_tiles - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
   const int total = my_tiles * nbat;
 
-  floatx4 acc[T][MT];
+  floatx4 acc[T][MA];
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < MA; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   WReg wA[UB][T], wB[UB][T];
-  f32x4 xA[UB][MT][2], xB[UB][MT][2];
+  f32x4 xA[UB][MA][2], xB[UB][MA][2];  // (stacked x: [u][fragment][0] holds the fragment's 16 bytes)
   // Residual epilogue inputs (old h and the next RMSNorm gain) of the tile whose
   // last batch sits in the matching register buffer, fetched with that batch.
   // (Only when every thread has at most one epilogue element; larger row
@@ -300,9 +312,10 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // reads zeros without touching memory, so rows beyond M, tiles beyond N and
   // k-steps beyond the wave's list need no branches (a branch around a load
   // makes the compiler wait for the data where the paths join).
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
+  const __amdgpu_buffer_rsrc_t xr = XS ? make_rsrc(a.xs, (uint32_t)KS * XS * 1024u)
+                                       : make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
   // load the q-th batch of this wave's work list (tile q / nbat, k-steps from (q % nbat) * UB)
-  auto load = [&](int q, WReg (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
+  auto load = [&](int q, WReg (&wv)[UB][T], f32x4 (&xv)[UB][MA][2]) {
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
     const int kb = (q % nbat) * UB;  // index into this wave's k-step list
     __amdgpu_buffer_rsrc_t wr[T], sr[T];
@@ -339,16 +352,37 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
           wv[u][t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], woff, 0, kNonTemporal);
         }
       }
+      if constexpr (XS) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + mrow;
-        const uint32_t xoff = (((uint32_t)m * a.ldx + k) * 4u) | wbad | ((uint32_t)(k >= K) << 31);
-        xv[u][mt][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff, 0, 0));
-        xv[u][mt][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16u, 0, 0));
+        for (int f = 0; f < XS; ++f) {
+          const uint32_t xoff = (((uint32_t)ks * XS + f) * 1024u + lane * 16u) | wbad;
+          xv[u][f][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff, 0, 0));
+        }
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + mrow;
+          const uint32_t xoff = (((uint32_t)m * a.ldx + k) * 4u) | wbad | ((uint32_t)(k >= K) << 31);
+          xv[u][mt][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff, 0, 0));
+          xv[u][mt][1] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16u, 0, 0));
+        }
       }
     }
   };
-  auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MT][2]) {
+  auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MA][2]) {
+    if constexpr (XS) {
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+#pragma unroll
+        for (int f = 0; f < XS; ++f) {
+          const bf16x8 xf = __builtin_bit_cast(bf16x8, xv[u][f][0]);
+#pragma unroll
+          for (int t = 0; t < T; ++t)
+            acc[t][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, __builtin_bit_cast(bf16x8, wv[u][t]), acc[t][f],
+                                                                0, 0, 0);
+        }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       // Q4: the codes of each tile as biased bf16 operands and the row scales
@@ -410,7 +444,9 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
         if (n < a.n_rows) {
           hv = p.h[0] + yfin[m][c];
           a.out[(size_t)m * a.ldo + n] = hv;
-          a.xg_out[(size_t)m * a.ldo + n] = hv * bf16_bits_to_f32((uint16_t)p.g[0]);
+          const float xv = hv * bf16_bits_to_f32((uint16_t)p.g[0]);
+          a.xg_out[(size_t)m * a.ldo + n] = xv;
+          if (a.xs_out) put_stacked(a.xs_out, a.stt, m, n, xv);
         }
         yfin[m][c] = hv;
       }
@@ -430,6 +466,18 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   auto finish = [&](int q, const Pre& p) {
     if (q % nbat != nbat - 1) return;
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
+    if constexpr (XS == 1) {  // hi (rows 0-7, lanes 0-31) + lo (rows 8-15, lanes 32-63)
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = acc[t][0][r], o = __shfl_xor(v, 32, kWave);
+          acc[t][0][r] = lane < 32 ? v + o : 0.f;
+        }
+    } else if constexpr (XS == 2) {  // hi (tile 0) + lo (tile 1)
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t][0] += acc[t][1];
+    }
 #pragma unroll
     for (int f0 = 0; f0 < NF; f0 += RR) {
 #pragma unroll
@@ -454,7 +502,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
 #pragma unroll
     for (int t = 0; t < T; ++t)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int mt = 0; mt < MA; ++mt) acc[t][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
     mfma_epilogue(tile, p);
     __syncthreads();  // yfin is reused by the next tile
   };
@@ -1531,17 +1579,25 @@ template <int T, int MT, int KIND, bool Q4> struct BatchQ {
   static constexpr bool PIPE = BatchK<T, MT, KIND>::PIPE && PIPE_Q;
 };
 
-template <int T, int MT, int KIND, bool Q4 = false>
+template <int T, int MT, int KIND, bool Q4 = false, int XS = 0>
 void launch_mfma_mt(const GemmArgs& a, int tiles, hipStream_t s) {
   const int grid = tiles < compute_units() ? tiles : compute_units();
   hipLaunchKernelGGL(
-      (gemm_bf16_mfma<T, MT, BatchQ<T, MT, KIND, Q4>::UB, BatchQ<T, MT, KIND, Q4>::PIPE, KIND, Q4>), dim3(grid),
+      (gemm_bf16_mfma<T, MT, BatchQ<T, MT, KIND, Q4>::UB, BatchQ<T, MT, KIND, Q4>::PIPE, KIND, Q4, XS>), dim3(grid),
       dim3(kMfmaThreads), 0, s, a, tiles);
 }
 
 template <int T, int KIND, bool Q4 = false>
 hipError_t launch_mfma_t(const GemmArgs& a, int blocks, hipStream_t s) {
   const int MT = (a.M + 15) / 16;
+  if constexpr (!Q4) {
+    if (a.xs) {  // stacked x (passes of at most 16 rows)
+      if (a.stt != (a.M <= 8 ? 1 : 2) || a.M > 16) return hipErrorInvalidValue;
+      if (a.stt == 1) launch_mfma_mt<T, 1, KIND, false, 1>(a, blocks, s);
+      else launch_mfma_mt<T, 1, KIND, false, 2>(a, blocks, s);
+      return hipGetLastError();
+    }
+  }
   if (MT <= 1) launch_mfma_mt<T, 1, KIND, Q4>(a, blocks, s);
   else if (MT <= 2) launch_mfma_mt<T, 2, KIND, Q4>(a, blocks, s);
   else if (MT <= 4) launch_mfma_mt<T, 4, KIND, Q4>(a, blocks, s);

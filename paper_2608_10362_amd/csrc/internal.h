@@ -91,6 +91,12 @@ struct GemmArgs {
   // wide passes
   int wide;               // 1: the whole pass has more than kMaxGemmRows rows (set by the caller for every launch)
   float* ypart;           // RESID: split-K partial sums, wide_ypart_floats(n_rows) floats
+  // Passes of at most 16 rows, bf16 weights: x also as a stacked operand
+  // (put_stacked, stt fragments per k-step), read instead of x when xs is set;
+  // RESID and SwiGLU epilogues also write their output stacked into xs_out.
+  const uint16_t* xs;
+  uint16_t* xs_out;
+  int stt;
   // INT4 weights: w[] are INT4 images (packed_int4_*), wscale[] their group scales
   int q4;
   const uint16_t* wscale[3];
@@ -136,6 +142,8 @@ struct RowsArgs {
   float* h;               // out [M, d]
   float* xg;              // out [M, d] h * gain
   float* ss;              // out [M] sum of squares of h rows
+  uint16_t* xs;           // out (or null): xg as a stacked operand (put_stacked), stt fragments per k-step
+  int stt;
 };
 hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s);
 

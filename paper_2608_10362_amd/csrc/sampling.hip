@@ -198,7 +198,9 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
   for (int k = threadIdx.x; k < a.d_model; k += blockDim.x) {
     const float v = Storage<ET>::load(e + k);
     h[k] = v;
-    xg[k] = v * Storage<ET>::load(gn + k);
+    const float xv = v * Storage<ET>::load(gn + k);
+    xg[k] = xv;
+    if (a.xs) put_stacked(a.xs, a.stt, r, k, xv);
     ss += v * v;
   }
   ss = block_sum(ss, red);
