@@ -37,7 +37,7 @@ struct specdec_model {
   float* logits;
   void* samp;  // scratch of the draft's softmax / draw kernels
   uint16_t* xs_d = nullptr;  // bf16: the stacked x operand of the d_model-column GEMMs (passes of <= 16 rows)
-  uint16_t* xs_f = nullptr;  // bf16: the stacked SwiGLU output, the down projection's x
+  uint16_t* xs_f = nullptr;  // bf16: the stacked attention output (the O projection's x), then SwiGLU output
   float* ypart = nullptr;  // split-K partials of the wide residual GEMMs (passes of more than 64 rows)
   uint32_t* attn_ctr = nullptr;           // bf16: the attention's combine counters (zero between launches)
   mutable bool attn_ctr_ready = false;    // set once they have been zeroed on a stream
@@ -129,7 +129,7 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.samp = take(sampling_scratch_bytes(max_rows, 1, d->vocab));
   // (stacked operands: two 1 KB fragments per 32 columns)
   w.xs_d = take(d->dtype == SPECDEC_BF16 ? (size_t)(d->d_model + 31) / 32 * 2048 : 0);
-  w.xs_f = take(d->dtype == SPECDEC_BF16 ? (size_t)(d->ffn_dim + 31) / 32 * 2048 : 0);
+  w.xs_f = take(d->dtype == SPECDEC_BF16 ? (size_t)(std::max(d->ffn_dim, H * hd) + 31) / 32 * 2048 : 0);
   w.ypart = take(wide ? wide_ypart_floats(d->d_model) * 4 : 0);
   w.ctr = take(d->dtype == SPECDEC_BF16 ? attention_counter_count(H, G, max_rows) * 4 : 0);
   w.total = off;
@@ -284,7 +284,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   // Passes of at most 16 rows on bf16 weights hand x from kernel to kernel also
   // as a stacked operand (put_stacked): the skinny GEMMs then read one 16-byte
   // fragment per k-step (two when M > 8) instead of two float32 loads per row
-  // tile.  The O projection keeps the attention's float32 output.
+  // tile.
   const bool stk = dt == SPECDEC_BF16 && m->wfmt != SPECDEC_WEIGHTS_INT4 && M <= 16 && m->xs_d;
   const int stt = M <= 8 ? 1 : 2;
   ra.xs = stk ? m->xs_d : nullptr;
@@ -334,6 +334,8 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     m->attn_ctr_ready = true;
   }
   at.counters = m->attn_ctr;
+  at.xs = stk ? m->xs_f : nullptr;
+  at.stt = stt;
 
   for (int l = 0; l < m->n_layers; ++l) {
     GemmArgs q = base;  // RMSNorm + Q|K|V projections
@@ -377,7 +379,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     o.w[0] = m->wo[l]; o.n_seg[0] = d.d_model; o.n_rows = d.d_model; o.kind = EPI_RESID;
     o.out = m->h; o.ldo = d.d_model; o.ss_out = m->ss; o.xg_out = m->xg; o.gain_out = m->ffn_norm[l];
     if (q4) { o.q4 = 1; o.wscale[0] = m->so[l]; }
-    if (stk) o.xs_out = m->xs_d;
+    if (stk) { o.xs = m->xs_f; o.xs_out = m->xs_d; }
     {
       Timed t(SPECDEC_KERNEL_O_PROJ, s);
       SD_TRY(gemm_rows(dt, o, M, s));

@@ -171,6 +171,13 @@ __device__ __forceinline__ void split_hilo(const float* v, bf16x8& hi, bf16x8& l
   }
 }
 
+// One element of the attention output o[row][head * hd + d], also into the
+// stacked operand of the O projection when the pass hands x over stacked.
+__device__ __forceinline__ void put_o(const AttnArgs& a, float* o, int row, int head, int d, float v) {
+  o[d] = v;
+  if (a.xs) put_stacked(a.xs, a.stt, row, head * a.head_dim + d, v);
+}
+
 // Reductions over the 16 lanes of a row of the wave (lanes 16k .. 16k+15)
 // with DPP moves: swaps within quads, then the half-row and row mirrors.
 // Every lane ends with the same value (each step combines two equal-order
@@ -533,7 +540,7 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     if (!rd.valid) {
 #pragma unroll
       for (int j = 0; j < DPL; ++j)
-        if (lane + 64 * j < HD) o[lane + 64 * j] = 0.f;
+        if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, 0.f);
       continue;
     }
     // parts holding keys <= pos (the last part also holds the remainder)
@@ -576,7 +583,7 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     const float inv = 1.0f / L;
 #pragma unroll
     for (int j = 0; j < DPL; ++j)
-      if (lane + 64 * j < HD) o[lane + 64 * j] = acc[j] * inv;
+      if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, acc[j] * inv);
   }
 }
 
@@ -592,7 +599,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
   const RowDesc rd = a.rows[r];
   float* o = a.o + ((size_t)r * H + head) * hd;
   if (!rd.valid) {
-    for (int dd = threadIdx.x; dd < hd; dd += blockDim.x) o[dd] = 0.f;
+    for (int dd = threadIdx.x; dd < hd; dd += blockDim.x) put_o(a, o, r, head, dd, 0.f);
     return;
   }
   // splits holding keys <= pos (with parts, the last one also holds the remainder)
@@ -621,7 +628,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
       acc3 += wsh[c + 3] * op[(size_t)(c + 3) * hd + dd];
     }
     for (; c < nch; ++c) acc0 += wsh[c] * op[(size_t)c * hd + dd];
-    o[dd] = ((acc0 + acc1) + (acc2 + acc3)) * inv;
+    put_o(a, o, r, head, dd, ((acc0 + acc1) + (acc2 + acc3)) * inv);
   }
 }
 
@@ -676,7 +683,7 @@ __global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
   if (!rd.valid) {
 #pragma unroll
     for (int d = 0; d < DPL; ++d)
-      if (lane + 64 * d < HD) o[lane + 64 * d] = 0.f;
+      if (lane + 64 * d < HD) put_o(a, o, r, head, lane + 64 * d, 0.f);
     return;
   }
   // parts holding keys <= pos (the last part also holds the remainder)
@@ -720,7 +727,7 @@ __global__ __launch_bounds__(64) void attn_combine_wave_kernel(AttnArgs a) {
   const float inv = 1.0f / L;
 #pragma unroll
   for (int d = 0; d < DPL; ++d)
-    if (lane + 64 * d < HD) o[lane + 64 * d] = ((acc[0][d] + acc[1][d]) + (acc[2][d] + acc[3][d])) * inv;
+    if (lane + 64 * d < HD) put_o(a, o, r, head, lane + 64 * d, ((acc[0][d] + acc[1][d]) + (acc[2][d] + acc[3][d])) * inv);
 }
 
 // ---------------------------------------------------------------- KV context copy

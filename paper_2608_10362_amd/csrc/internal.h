@@ -162,6 +162,8 @@ struct AttnArgs {
   float* o_part;         // [M, h, n_split, hd]
   float* ml_part;        // [M, h, n_split, 2]
   float* o;              // [M, h hd]
+  uint16_t* xs;          // or null: o also as a stacked operand (put_stacked), stt fragments per k-step
+  int stt;
   int32_t* status;
   int seq_bound;         // 1: bound each sequence's keys by its own last row (batches of several sequences)
   // bf16: one counter per (sequence, query tile, kv head), zero between launches;
