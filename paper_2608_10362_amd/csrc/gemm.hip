@@ -238,16 +238,21 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // and tile.  The hi and lo parts accumulate apart (accumulator tiles 0 and
   // 1, or rows m and 8 + m of tile 0) and are added once per tile before the
   // cross-wave sums, the same arithmetic for either count of fragments.
+  // XS = 3: XS = 1 with each wave's x fragments (at most 8 k-steps, K <= 4096)
+  // fetched once into LDS and read from there for every unit of the block.
   static_assert(XS == 0 || (MT == 1 && !Q4), "stacked x: bf16 weights, one row tile");
   using WReg = std::conditional_t<Q4, Q4Frag, u32x4>;
-  constexpr int MA = XS ? XS : MT;  // accumulator row tiles
+  constexpr bool XL = XS == 3;
+  constexpr int XF = XL ? 1 : XS;   // stacked fragments per k-step
+  constexpr int MA = XS ? XF : MT;  // accumulator row tiles
   constexpr int NC = 16 * T;
   constexpr int MP = 16 * MT;
   constexpr int NF = T * MT;              // accumulator fragments per wave
-  constexpr int RR = NF <= 2 ? NF : 2;    // fragments reduced per LDS round
+  constexpr int RR = XL ? 1 : (NF <= 2 ? NF : 2);  // fragments reduced per LDS round (XL: LDS goes to x)
   constexpr bool QKV = KIND == EPI_QKV;
   constexpr int E = (MP * NC + kMfmaThreads - 1) / kMfmaThreads;  // epilogue elements per thread
   __shared__ float red[RR][kMfmaWaves][kWave][4];
+  __shared__ u32x4 s_xl[XL ? kMfmaWaves : 1][XL ? 8 : 1][kWave];  // XL: wave w's x fragments, k-steps w + 16j
   __shared__ float yfin[MP][NC + 1];
   __shared__ float scale[MP];
   __shared__ RowDesc s_rows[QKV ? MP : 1];
@@ -312,7 +317,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // reads zeros without touching memory, so rows beyond M, tiles beyond N and
   // k-steps beyond the wave's list need no branches (a branch around a load
   // makes the compiler wait for the data where the paths join).
-  const __amdgpu_buffer_rsrc_t xr = XS ? make_rsrc(a.xs, (uint32_t)KS * XS * 1024u)
+  const __amdgpu_buffer_rsrc_t xr = XS ? make_rsrc(a.xs, (uint32_t)KS * XF * 1024u)
                                        : make_rsrc(a.x, (uint32_t)a.M * a.ldx * 4u);
   // load the q-th batch of this wave's work list (tile q / nbat, k-steps from (q % nbat) * UB)
   auto load = [&](int q, WReg (&wv)[UB][T], f32x4 (&xv)[UB][MA][2]) {
@@ -352,7 +357,9 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
           wv[u][t] = __builtin_amdgcn_raw_buffer_load_b128(wr[t], woff, 0, kNonTemporal);
         }
       }
-      if constexpr (XS) {
+      if constexpr (XL) {
+        // (x comes from LDS)
+      } else if constexpr (XS) {
 #pragma unroll
         for (int f = 0; f < XS; ++f) {
           const uint32_t xoff = (((uint32_t)ks * XS + f) * 1024u + lane * 16u) | wbad;
@@ -369,7 +376,19 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       }
     }
   };
-  auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MA][2]) {
+  auto compute = [&](WReg (&wv)[UB][T], f32x4 (&xv)[UB][MA][2], int q) {
+    if constexpr (XL) {
+      const int kb = (q % nbat) * UB;  // (past the wave's k-steps the weights read zeros)
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        const bf16x8 xf = __builtin_bit_cast(bf16x8, s_xl[wave][min(kb + u, 7)][lane]);
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+          acc[t][0] =
+              __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, __builtin_bit_cast(bf16x8, wv[u][t]), acc[t][0], 0, 0, 0);
+      }
+      return;
+    }
     if constexpr (XS) {
 #pragma unroll
       for (int u = 0; u < UB; ++u)
@@ -466,7 +485,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   auto finish = [&](int q, const Pre& p) {
     if (q % nbat != nbat - 1) return;
     const int tile = blockIdx.x + (q / nbat) * gridDim.x;
-    if constexpr (XS == 1) {  // hi (rows 0-7, lanes 0-31) + lo (rows 8-15, lanes 32-63)
+    if constexpr (XF == 1) {  // hi (rows 0-7, lanes 0-31) + lo (rows 8-15, lanes 32-63)
 #pragma unroll
       for (int t = 0; t < T; ++t)
 #pragma unroll
@@ -474,7 +493,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
           const float v = acc[t][0][r], o = __shfl_xor(v, 32, kWave);
           acc[t][0][r] = lane < 32 ? v + o : 0.f;
         }
-    } else if constexpr (XS == 2) {  // hi (tile 0) + lo (tile 1)
+    } else if constexpr (XF == 2) {  // hi (tile 0) + lo (tile 1)
 #pragma unroll
       for (int t = 0; t < T; ++t) acc[t][0] += acc[t][1];
     }
@@ -545,6 +564,15 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
                                            rr, tid < MP ? (uint32_t)tid * (uint32_t)sizeof(RowDesc) : kOutOfRange, 0, 0));
   }
   int q = 0;
+  u32x4 xl[XL ? 8 : 1];
+  if constexpr (XL) {  // this wave's x fragments, requested before the weights
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ks = ks0 + j * kstride;
+      xl[j] = __builtin_amdgcn_raw_buffer_load_b128(
+          xr, ((uint32_t)ks * 1024u + lane * 16u) | ((uint32_t)(j >= my_ks || ks >= KS) << 31), 0, 0);
+    }
+  }
   if (total > 0) {
     load(0, wA, xA);
     epi_fetch(0, pA);
@@ -552,6 +580,10 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   if (PIPE && total > 1) {
     load(1, wB, xB);
     epi_fetch(1, pB);
+  }
+  if constexpr (XL) {  // (read back by this wave only)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s_xl[wave][j][lane] = xl[j];
   }
   // s_m = 1/sqrt(sum_p ss[p][m] / K + eps): lanes sum their partials in p order
   // (held ones first, then any beyond 64*RS_P), fixed shuffle tree.
@@ -589,14 +621,14 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   }
   if (PIPE) {
     while (q < total) {
-      compute(wA, xA);
+      compute(wA, xA, q);
       finish(q, pA);
       if (q + 2 < total) {
         load(q + 2, wA, xA);
         epi_fetch(q + 2, pA);
       }
       if (++q >= total) break;
-      compute(wB, xB);
+      compute(wB, xB, q);
       finish(q, pB);
       if (q + 2 < total) {
         load(q + 2, wB, xB);
@@ -610,7 +642,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
         load(q, wA, xA);
         epi_fetch(q, pA);
       }
-      compute(wA, xA);
+      compute(wA, xA, q);
       finish(q, pA);
     }
   }
@@ -1593,7 +1625,11 @@ hipError_t launch_mfma_t(const GemmArgs& a, int blocks, hipStream_t s) {
   if constexpr (!Q4) {
     if (a.xs) {  // stacked x (passes of at most 16 rows)
       if (a.stt != (a.M <= 8 ? 1 : 2) || a.M > 16) return hipErrorInvalidValue;
-      if (a.stt == 1) launch_mfma_mt<T, 1, KIND, false, 1>(a, blocks, s);
+      // (x held in LDS: measured faster for the store, SwiGLU and residual GEMMs, slower for Q|K|V, whose
+      // epilogue tables then leave room for one reduction fragment per round only)
+      if (KIND != EPI_QKV && a.stt == 1 && (a.K + 31) / 32 <= 8 * kMfmaWaves)
+        launch_mfma_mt<T, 1, KIND, false, 3>(a, blocks, s);
+      else if (a.stt == 1) launch_mfma_mt<T, 1, KIND, false, 1>(a, blocks, s);
       else launch_mfma_mt<T, 1, KIND, false, 2>(a, blocks, s);
       return hipGetLastError();
     }
