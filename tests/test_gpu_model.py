@@ -214,6 +214,15 @@ def test_bf16_7b_shape_multi_request_ragged():
     _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=6, seed=2)
 
 
+@pytest.mark.parametrize("B,g", [(2, 3), (2, 7), (3, 4)])
+def test_bf16_1b_shape_stacked_operand_row_counts(B, g):
+    # 8, 16 and 15 rows: passes of at most 16 rows hand x between kernels as the
+    # stacked bf16 operand, one fragment (hi and lo rows of one MFMA) up to 8
+    # rows and two fragments above; K = 2048 also takes the LDS-resident form
+    lengths = synth.make_ragged_lengths(B, 50, 300, seed=7)
+    _bf16_case(synth.LLAMA_1B, 2, list(lengths), g=g, seed=6)
+
+
 def test_bf16_7b_shape_many_short_sequences():
     # 10 sequences of at most ~250 keys, gamma 6 (70 rows): more (kv head,
     # sequence) units than CUs and fewer than 12 sub-chunks of 32 keys per
