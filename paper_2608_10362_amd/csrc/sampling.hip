@@ -104,42 +104,6 @@ __device__ __forceinline__ MaxSum ms_merge(MaxSum a, MaxSum b) {
   const float m = fmaxf(a.m, b.m);
   return MaxSum{m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
 }
-__device__ MaxSum block_max_sum(const float* row, int V, float T, float* red2) {
-  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nt / kWave;
-  MaxSum st{-INFINITY, 0.f};
-  if ((V & 3) == 0 && ((uintptr_t)row & 15) == 0) {
-    const f32x4* r4 = (const f32x4*)row;
-    const int V4 = V >> 2;
-    int j = tid;
-    for (; j + 3 * nt < V4; j += 4 * nt) {
-      f32x4 v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = r4[j + u * nt];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) ms_add(st, v[u][e] / T);
-    }
-    for (; j < V4; j += nt) {
-      const f32x4 v = r4[j];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ms_add(st, v[e] / T);
-    }
-  } else {
-    for (int j = tid; j < V; j += nt) ms_add(st, row[j] / T);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    MaxSum other{__shfl_xor(st.m, o, kWave), __shfl_xor(st.s, o, kWave)};
-    st = ms_merge(st, other);
-  }
-  __syncthreads();
-  if (lane == 0) { red2[2 * wave] = st.m; red2[2 * wave + 1] = st.s; }
-  __syncthreads();
-  MaxSum tot{red2[0], red2[1]};
-  for (int w = 1; w < nw; ++w) tot = ms_merge(tot, MaxSum{red2[2 * w], red2[2 * w + 1]});
-  return tot;
-}
 
 // ---------------------------------------------------------------- rows + embedding
 template <typename ET>
