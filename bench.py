@@ -671,8 +671,9 @@ def main():
     step_profile = {k: {"ms_per_step": round(ms / args.profile_steps, 4),
                         "launches_per_step": n / args.profile_steps} for k, (ms, n) in per.items() if n}
 
-    # Per-kernel durations of the verify pass: each kernel of layer 0 (and the head)
-    # re-launched back to back between HIP events on the library's stream.
+    # Per-kernel durations of the verify pass: each kernel re-launched back to back
+    # between HIP events on the library's stream, layer after layer (so every launch
+    # streams weights and keys/values the launches before it did not touch).
     draft_part(0); verify_part(0)
     torch.cuda.synchronize()
     kb_verify = kernel_bytes(shape, ctx + g + 1, args.weights)

@@ -386,14 +386,19 @@ SPECDEC_API specdec_status specdec_timing_enable(int32_t enable);
  * the accumulators. */
 SPECDEC_API specdec_status specdec_timing_read(double* total_ms, int64_t* launches);
 
-/* Time one kernel in isolation: re-launch the layer-0 launch of kernel kind
- * `kind` (for SPECDEC_KERNEL_LM_HEAD the head GEMM) recorded by the last
- * forward pass (verify, draft step or prefill chunk) of `model`, `reps` times
- * back to back between two HIP events on `stream`, and return the average
- * duration in microseconds.  Measurement only: the re-launched kernels write
- * the model's workspace, the same K/V values at that pass's cache positions,
- * and (residual and head kinds) that pass's hidden state and logits, so the
- * pass's outputs must be consumed before timing.  Synchronizes the stream.
+/* Time one kernel in isolation: re-launch the launches of kernel kind `kind`
+ * recorded by the last forward pass (verify, draft step or prefill chunk) of
+ * `model`, `reps` times back to back between two HIP events on `stream`, the
+ * i-th launch being layer i mod L's (the head GEMM and the embedding have one
+ * launch each), after one untimed launch of layer 0; return the average
+ * duration in microseconds.  Consecutive launches thus stream different
+ * layers' weights (and keys and values), as the pass does, rather than
+ * re-reading data a cache may still hold.  Measurement only: the re-launched
+ * kernels write the model's workspace, K/V at that pass's cache positions of
+ * the layers they run (from the workspace's current contents) and (residual
+ * and head kinds) the hidden state and logits, so the pass's outputs must be
+ * consumed, and those cache entries rewritten, before the model is used again.
+ * Synchronizes the stream.
  * Errors: INVALID_ARG, UNSUPPORTED (kind not recorded yet), HIP. */
 SPECDEC_API specdec_status specdec_time_kernel(const specdec_model* model, int32_t kind, int32_t reps, void* stream,
                                                double* avg_us);

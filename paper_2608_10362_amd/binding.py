@@ -537,7 +537,7 @@ def specdec_timing_enable(enable: bool):
 
 
 def specdec_time_kernel(model: "Model", kind: str, reps: int = 20, stream=None) -> float:
-    """Average duration (us) of `kind` re-launched back to back (see the header)."""
+    """Average duration (us) of `kind` re-launched back to back, layer after layer (see the header)."""
     out = ctypes.c_double(0.0)
     _check(lib().specdec_time_kernel(model.handle, KERNEL_KINDS.index(kind), reps, _stream(stream),
                                      ctypes.byref(out)), "specdec_time_kernel")

@@ -42,11 +42,12 @@ struct specdec_model {
   uint32_t* attn_ctr = nullptr;           // bf16: the attention's combine counters (zero between launches)
   mutable bool attn_ctr_ready = false;    // set once they have been zeroed on a stream
   int chunk, n_split_max;
-  // layer-0 launches of the last forward pass, for specdec_time_kernel
+  // per-layer launches of the last forward pass, for specdec_time_kernel
+  // (entry l: layer l; the head and the embedding have one)
   mutable bool rec_valid[SPECDEC_KERNEL_KINDS] = {};
-  mutable GemmArgs rec_gemm[SPECDEC_KERNEL_KINDS];
+  mutable std::vector<GemmArgs> rec_gemm[SPECDEC_KERNEL_KINDS];
   mutable int rec_rows[SPECDEC_KERNEL_KINDS];
-  mutable AttnArgs rec_attn;
+  mutable std::vector<AttnArgs> rec_attn;
   mutable RowsArgs rec_embed;
 };
 
@@ -295,8 +296,10 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   }
   m->rec_embed = ra;
   m->rec_valid[SPECDEC_KERNEL_EMBED] = true;
-  auto rec = [&](int kind, const GemmArgs& g) {
-    m->rec_gemm[kind] = g;
+  auto rec = [&](int kind, int layer, const GemmArgs& g) {
+    std::vector<GemmArgs>& v = m->rec_gemm[kind];
+    v.resize((size_t)layer + 1);
+    v[(size_t)layer] = g;
     m->rec_rows[kind] = M;
     m->rec_valid[kind] = true;
   };
@@ -357,7 +360,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_QKV, s);
       SD_TRY(gemm_rows(dt, q, M, s));
     }
-    if (l == 0) rec(SPECDEC_KERNEL_QKV, q);
+    rec(SPECDEC_KERNEL_QKV, l, q);
 
     at.layer = l;
     if (dt != SPECDEC_BF16) {
@@ -368,8 +371,9 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_ATTENTION, s);
       SD_TRY(launch_attention(at, s));
     }
+    m->rec_attn.resize((size_t)l + 1);
+    m->rec_attn[(size_t)l] = at;
     if (l == 0) {
-      m->rec_attn = at;
       m->rec_valid[SPECDEC_KERNEL_ATTENTION] = true;
       m->rec_valid[SPECDEC_KERNEL_ROPE_APPEND] = dt != SPECDEC_BF16;
     }
@@ -384,7 +388,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_O_PROJ, s);
       SD_TRY(gemm_rows(dt, o, M, s));
     }
-    if (l == 0) rec(SPECDEC_KERNEL_O_PROJ, o);
+    rec(SPECDEC_KERNEL_O_PROJ, l, o);
     n_ss = n_resid_blocks;
 
     GemmArgs gu = base;  // RMSNorm + gate|up + SwiGLU
@@ -398,7 +402,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_GATE_UP, s);
       SD_TRY(gemm_rows(dt, gu, M, s));
     }
-    if (l == 0) rec(SPECDEC_KERNEL_GATE_UP, gu);
+    rec(SPECDEC_KERNEL_GATE_UP, l, gu);
 
     GemmArgs dn = base;  // down projection + residual
     dn.x = m->u; dn.ldx = d.ffn_dim; dn.K = d.ffn_dim;
@@ -411,7 +415,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
       Timed t(SPECDEC_KERNEL_DOWN, s);
       SD_TRY(gemm_rows(dt, dn, M, s));
     }
-    if (l == 0) rec(SPECDEC_KERNEL_DOWN, dn);
+    rec(SPECDEC_KERNEL_DOWN, l, dn);
   }
 
   GemmArgs hd_ = base;  // final RMSNorm + LM head
@@ -423,7 +427,7 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     Timed t(SPECDEC_KERNEL_LM_HEAD, s);
     SD_TRY(gemm_rows(dt, hd_, M, s));
   }
-  rec(SPECDEC_KERNEL_LM_HEAD, hd_);
+  rec(SPECDEC_KERNEL_LM_HEAD, 0, hd_);
   return SPECDEC_OK;
 }
 
@@ -963,12 +967,17 @@ specdec_status specdec_time_kernel(const specdec_model* m, int32_t kind, int32_t
   if (!m->rec_valid[kind]) return SPECDEC_ERR_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
   const int dt = m->desc.dtype;
-  auto launch = [&]() -> hipError_t {
+  // Launch i re-runs layer i mod L: each launch streams weights (and keys and
+  // values) that the launches just before it did not touch, as in the pass.
+  auto launch = [&](int i) -> hipError_t {
     switch (kind) {
       case SPECDEC_KERNEL_EMBED: return launch_rows_embed(dt, m->rec_embed, s);
-      case SPECDEC_KERNEL_ROPE_APPEND: return launch_rope_append(m->rec_attn, s);
-      case SPECDEC_KERNEL_ATTENTION: return launch_attention(m->rec_attn, s);
-      default: return gemm_rows(dt, m->rec_gemm[kind], m->rec_rows[kind], s);
+      case SPECDEC_KERNEL_ROPE_APPEND: return launch_rope_append(m->rec_attn[(size_t)i % m->rec_attn.size()], s);
+      case SPECDEC_KERNEL_ATTENTION: return launch_attention(m->rec_attn[(size_t)i % m->rec_attn.size()], s);
+      default: {
+        const std::vector<GemmArgs>& v = m->rec_gemm[kind];
+        return gemm_rows(dt, v[(size_t)i % v.size()], m->rec_rows[kind], s);
+      }
     }
   };
   hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -977,9 +986,9 @@ specdec_status specdec_time_kernel(const specdec_model* m, int32_t kind, int32_t
     (void)hipEventDestroy(e0);
     return SPECDEC_ERR_HIP;
   }
-  hipError_t err = launch();  // warm-up
+  hipError_t err = launch(0);  // warm-up
   if (err == hipSuccess) err = hipEventRecord(e0, s);
-  for (int i = 0; i < reps && err == hipSuccess; ++i) err = launch();
+  for (int i = 1; i <= reps && err == hipSuccess; ++i) err = launch(i);
   if (err == hipSuccess) err = hipEventRecord(e1, s);
   if (err == hipSuccess) err = hipEventSynchronize(e1);
   float ms = 0.f;
