@@ -235,3 +235,73 @@ def test_nonfinite_is_an_error():
     p[1, 2] = np.nan
     with pytest.raises(NonFiniteError):
         accept_sampling(p, q, [0], [0], 0)
+
+
+# ---------------------------------------------------------------- temperature (closed forms)
+def _temperature_pin_holds(softmax_fn) -> bool:
+    """softmax(l / T) against closed forms: logits (0, T ln 2) give (1/3, 2/3);
+    logits T ln w give w / sum(w); a constant shift changes nothing."""
+    ok = True
+    for T in (0.8, 1.0, 2.0, 0.25):
+        got = softmax_fn(np.array([0.0, T * np.log(2.0)]), T)
+        ok &= np.allclose(got, [1 / 3, 2 / 3], rtol=0, atol=1e-14)
+        w = np.array([1.0, 2.0, 3.0, 4.0, 10.0])
+        got = softmax_fn(T * np.log(w), T)
+        ok &= np.allclose(got, w / w.sum(), rtol=0, atol=1e-14)
+        got2 = softmax_fn(T * np.log(w) + 37.5, T)
+        ok &= np.allclose(got2, w / w.sum(), rtol=0, atol=1e-14)
+    return bool(ok)
+
+
+def test_softmax_temperature_closed_form():
+    from oracle.sampling import softmax
+    assert _temperature_pin_holds(softmax)
+    # T = 0 is the greedy mode, never a softmax
+    with pytest.raises(ValueError):
+        softmax(np.zeros(3), 0.0)
+
+
+def test_planted_temperature_mistake_fails_the_pin():
+    def times_t(logits, T):  # multiplies by T instead of dividing
+        z = np.asarray(logits, dtype=np.float64) * T
+        e = np.exp(z - z.max())
+        return e / e.sum()
+    assert not _temperature_pin_holds(times_t)
+
+
+# ---------------------------------------------------------------- degenerate residual (reading S4)
+# q dominates p everywhere, so the residual max(0, p - q) is all zero and a
+# rejection has nothing to draw from; the reading falls back to p itself with
+# the same word.  p is not proportional to q, so a fallback to q is told apart.
+_P_DOM = np.array([0.1, 0.3, 0.2], np.float32)
+_Q_DOM = np.array([0.5, 0.3, 0.2], np.float32)
+
+
+def _fallback_pin_holds(accept_fn) -> bool:
+    p1 = np.stack([_P_DOM, _P_DOM])
+    q1 = _Q_DOM[None, :]
+    # accept iff u * 0.5 < 0.1, i.e. u < 0.2: word 0 accepts, the top word rejects
+    if accept_fn(p1, q1, [0], [0], 0)[0] != 1 or accept_fn(p1, q1, [0], [0xFFFFFFFF], 0)[0] != 0:
+        return False
+    # emitted-token distribution given rejection, counted exactly over the resample word
+    out, start = {}, 0
+    for j in range(3):
+        end = _first_true(lambda x: accept_fn(p1, q1, [0], [0xFFFFFFFF], x)[1] > j, start, TOP)
+        out[j] = Fraction(end - start, TOP)
+        start = end
+    target = _P_DOM.astype(np.float64) / _P_DOM.astype(np.float64).sum()
+    # fixed-point weights of float32 p: within 2^-32 + 3 * 2^-40 of p / sum(p)
+    return all(abs(float(out[j]) - target[j]) < 1e-9 for j in range(3))
+
+
+def test_degenerate_residual_falls_back_to_p():
+    assert _fallback_pin_holds(accept_sampling)
+
+
+def test_planted_fallback_to_q_fails_the_pin():
+    def to_q(p, q, d, u, x):
+        A, nxt = accept_sampling(p, q, d, u, x)
+        if A < len(d) and not np.any(np.maximum(0, p[A] - q[A]) > 0):
+            nxt = sample_fixed_point(q[A], x)
+        return A, nxt
+    assert not _fallback_pin_holds(to_q)
