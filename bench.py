@@ -506,6 +506,9 @@ def run_switching(args):
                      "blocked_ms": round(st.blocked_ms, 2), "catchup_tokens": st.catchup_tokens,
                      "matches_desired": round(float(np.mean([a == d for a, d in zip(st.active, st.desired)])), 3),
                      "fallback_fraction": round(st.fallback_fraction(), 3),
+                     "desired_ms": round(st.desired_ms, 2), "fallback_ms": round(st.fallback_ms, 2),
+                     "prediction_ms": round(st.prediction_ms, 3),
+                     "time_breakdown": {k: round(v, 4) for k, v in st.time_breakdown().items()},
                      "text_agrees": bool(same)}
         log(f"{mode}: {out[mode]}")
         del r, target, kv_t

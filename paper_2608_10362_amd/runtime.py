@@ -187,6 +187,15 @@ class RunStats:
     active: List[int] = field(default_factory=list)    # draft run in each interval
     desired: List[int] = field(default_factory=list)   # the schedule's preferred draft
     selected: List[int] = field(default_factory=list)  # the policy's choice (runs unless still loading)
+    # Execution time breakdown (Sec. 4.3, "Execution Breakdown"): host wall time of
+    # the intervals decoded with the policy's preferred draft (desired) or with
+    # another resident draft while the preferred one is not available (fallback),
+    # and of the scheduling decisions themselves (prediction).  An interval runs
+    # from the end of its scheduling decision to the synchronising drain of its
+    # iteration log at the next point, so its GPU work is inside it.
+    desired_ms: float = 0.0
+    fallback_ms: float = 0.0
+    prediction_ms: float = 0.0
 
     def fallback_fraction(self) -> float:
         """Intervals spent on another draft than the one the policy selected
@@ -194,6 +203,14 @@ class RunStats:
         if not self.active:
             return 0.0
         return float(np.mean([a != s for a, s in zip(self.active, self.selected)]))
+
+    def time_breakdown(self) -> Dict[str, float]:
+        """Fractions of desired execution, fallback execution and prediction time."""
+        total = self.desired_ms + self.fallback_ms + self.prediction_ms
+        if total <= 0:
+            return {"desired": 0.0, "fallback": 0.0, "prediction": 0.0}
+        return {"desired": self.desired_ms / total, "fallback": self.fallback_ms / total,
+                "prediction": self.prediction_ms / total}
 
 
 class SwitchingRunner:
@@ -355,12 +372,27 @@ class SwitchingRunner:
             pending_log = 0
             return max_tokens is not None and stats.tokens >= max_tokens
 
+        t_exec = None          # start of the interval being decoded
+        exec_fallback = False  # whether it runs another draft than the policy's choice
+
+        def close_interval(now):
+            if t_exec is not None:
+                if exec_fallback:
+                    stats.fallback_ms += (now - t_exec) * 1e3
+                else:
+                    stats.desired_ms += (now - t_exec) * 1e3
+
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for it in range(n_iterations):
             if it % interval == 0:
-                if drain():
+                stop = drain()
+                now = time.perf_counter()
+                close_interval(now)
+                t_exec = None
+                if stop:
                     break
+                t_pred, blocked0 = now, stats.blocked_ms
                 point = it // interval
                 desired = schedule[point]
                 if self.mode == "mab":
@@ -387,6 +419,8 @@ class SwitchingRunner:
                     if self.mode == "reload":
                         self._ensure_in_slot_blocking(nxt, stats)
                     stats.selected.append(int(desired))
+                # (a blocking reload is counted in blocked_ms, not as prediction)
+                stats.prediction_ms += (time.perf_counter() - t_pred) * 1e3 - (stats.blocked_ms - blocked0)
                 if nxt != active:
                     if active is not None:
                         stats.switches += 1
@@ -397,6 +431,8 @@ class SwitchingRunner:
                 stats.desired.append(int(desired))
                 stats.active.append(int(active))
                 last_run[active] = point
+                t_exec = time.perf_counter()
+                exec_fallback = active != stats.selected[-1]
             sd.step(it)
             log_d[pending_log].copy_(sd.d[0])
             log_a[pending_log:pending_log + 1].copy_(sd.n_acc[:1])
@@ -405,7 +441,9 @@ class SwitchingRunner:
             stats.iterations += 1
         drain()
         torch.cuda.synchronize()
-        stats.wall_ms = (time.perf_counter() - t0) * 1e3
+        now = time.perf_counter()
+        close_interval(now)
+        stats.wall_ms = (now - t0) * 1e3
         return stats
 
     def _load_into_slot(self, d: int, active: Optional[int], last_run: Dict[int, int], stats: RunStats):

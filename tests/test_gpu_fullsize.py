@@ -4,7 +4,7 @@ workload: batch 1, resident context of 2048 positions, gamma 2 / 4 / 8, the
 
 - the verify logits of the 32-layer model against the float64 oracle's forward
   (teacher forcing on the drafted tokens), and the K/V appended by the last layer;
-- the draft's single-token steps (temperature 1) against the oracle;
+- the draft's single-token steps (temperatures 1 and 0.8) against the oracle;
 - the verify block against gamma+1 one-row verifies, bit for bit (Sec. 2: one
   target pass over the drafted block gives the same per-position distributions as
   decoding them one at a time; every reduction here has a fixed order that does not
@@ -22,7 +22,8 @@ import pytest
 from oracle import model as om
 from oracle import sampling
 from paper_2608_10362_amd import binding, synth
-from tests.gpu_util import i32, install_context, log, oracle_caches, torch_cuda
+from oracle.philox import PURPOSE_DRAFT, draw_u32
+from tests.gpu_util import draw_near_boundary, i32, install_context, log, oracle_caches, torch_cuda
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
@@ -90,10 +91,11 @@ def test_full_7b_verify_matches_oracle(full7b):
             assert int(np.argmax(got[i])) == int(np.argmax(ref[i]))
 
 
-def test_full_7b_draft_steps_match_oracle(full7b):
+@pytest.mark.parametrize("T", [1.0, 0.8])
+def test_full_7b_draft_steps_match_oracle(full7b, T):
     torch = torch_cuda()
     W, ctx, _, draft, _, kv_d = full7b
-    g, T, seed, step = 4, 1.0, 7, 3
+    g, seed, step = 4, 7, 3
     pend = _pending(33)
     _set(kv_d, CTX, pend)
     m = om.Model(SHAPE, W, n_layers=DRAFT_LAYERS)
@@ -114,7 +116,9 @@ def test_full_7b_draft_steps_match_oracle(full7b):
         log(f"4-layer draft slot {s}: logit error {err:.3g}, q error {qerr:.3g}, "
             f"token {int(d[0, s].item())} (oracle {tok_ref})")
         assert err < TOL_BF16 and qerr < 1e-4
-        assert int(d[0, s].item()) == tok_ref
+        if int(d[0, s].item()) != tok_ref:  # only where the oracle's draw is within the q error of an edge
+            word = draw_u32(seed, 0, step, PURPOSE_DRAFT, s)
+            assert draw_near_boundary(q_ref, word, tok_ref, rel=max(1e-5, 2 * qerr / float(q_ref.max())))
 
 
 @pytest.mark.parametrize("g", [2, 4, 8])

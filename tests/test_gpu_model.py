@@ -13,7 +13,8 @@ from oracle import model as om
 from oracle import sampling
 from oracle.specdec import greedy_decode
 from paper_2608_10362_amd import binding, synth
-from tests.gpu_util import f32, i32, install_context, log, oracle_caches, torch_cuda
+from tests.gpu_util import (SOFTMAX_REL_ERR, accept_explained, f32, i32, install_context, log, oracle_caches,
+                            torch_cuda, u32_tensor)
 
 pytestmark = pytest.mark.gpu
 
@@ -73,14 +74,14 @@ def tiny_wide():
     return shape, W, binding.Model(dw, 1, max_rows=16, max_ctx=256)
 
 
-@pytest.mark.parametrize("wide", [False, True])
-def test_tiny_draft_steps(tiny, tiny_wide, wide):
+@pytest.mark.parametrize("wide,T", [(False, 1.0), (True, 1.0), (False, 0.8), (True, 0.8)])
+def test_tiny_draft_steps(tiny, tiny_wide, wide, T):
     torch = torch_cuda()
     if wide:
         shape, W, draft = tiny_wide
     else:
         shape, W, _, draft = tiny
-    g, T, seed, step = 4, 1.0, 2, 9
+    g, seed, step = 4, 2, 9
     prompt = synth.make_prompt(40, shape.vocab)
     kv = binding.KVCache(draft, 1, 256)
     binding.specdec_prefill(draft, kv, i32(prompt))
@@ -162,7 +163,7 @@ def test_tiny_verify_equals_sequential_steps(tiny):
 
 
 # ---------------------------------------------------------------- bf16 Llama-shaped prefixes
-def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None):
+def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None, return_logits=False):
     torch = torch_cuda()
     B = len(lengths)
     capacity = capacity or int(np.ceil((max(lengths) + g + 1) / 64) * 64)
@@ -183,8 +184,10 @@ def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None):
     m = om.Model(shape, W, n_layers=n_layers)
     caches = oracle_caches(shape, n_layers, ctx, lengths, capacity)
     worst = 0.0
+    refs = []
     for b in range(B):
         ref = m.forward_block([int(pend[b])] + list(drafts[b]), int(lengths[b]), caches[b])
+        refs.append(ref)
         worst = max(worst, float(np.abs(got[b] - ref).max()))
         # the drafted tokens' K/V were appended at [len, len+g]
         k, v = kv.read_context(n_layers - 1, b, int(lengths[b]), g + 1)
@@ -192,6 +195,8 @@ def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None):
         assert np.abs(kf - caches[b].k[n_layers - 1][lengths[b]:lengths[b] + g + 1]).max() < 0.05
     log(f"bf16 verify max-abs logit error {worst:.3g}")
     assert worst < TOL_BF16
+    if return_logits:
+        return got, np.stack(refs), drafts
     return worst
 
 
@@ -236,6 +241,40 @@ def test_bf16_7b_shape_long_context_looping_attention():
     # (kv head, sequence) units -> parts of 8 sub-chunks on 4-wave blocks, each
     # wave looping over 2 sub-chunks with the online softmax
     _bf16_case(synth.LLAMA_7B, 1, [4500, 6100], g=4, seed=4)
+
+
+def test_bf16_7b_shape_long_context_workload_launch_and_accept():
+    # The exact launch of the 16-sequence long-context workload: contexts drawn
+    # from U[1024, 8192] with the lengths seed (up to 8022 keys), gamma 6 (112
+    # rows: the wide GEMMs and the looping attention), then the temperature-0.8
+    # accept on the device's verify logits (LOGITS mode) against the oracle's
+    # accept on its own logits, with synthetic draft distributions and words.
+    torch = torch_cuda()
+    B, g, V, T = 16, 6, synth.LLAMA_7B.vocab, 0.8
+    lengths = synth.make_ragged_lengths(B, 1024, 8192)
+    got, refs, _ = _bf16_case(synth.LLAMA_7B, 1, list(lengths), g=g, seed=8, return_logits=True)
+    err = float(np.abs(got - refs).max())
+    rng = np.random.default_rng(15)
+    q = sampling.softmax(rng.standard_normal((B, g, V)) * 1.3 + refs[:, :g] * 0.5, T).astype(np.float32)
+    d = np.array([[sampling.sample_fixed_point(q[b, i], int(rng.integers(0, 2 ** 32))) for i in range(g)]
+                  for b in range(B)], np.int32)
+    words = synth.make_rand_u32((B, g + 1), seed=14)
+    nacc = torch.zeros(B, dtype=torch.int32, device="cuda")
+    nxt = torch.zeros(B, dtype=torch.int32, device="cuda")
+    binding.specdec_accept(B, g, V, binding.INPUT_LOGITS, T, f32(got), f32(q), i32(d), g, u32_tensor(words), 0, 0,
+                           nacc, nxt)
+    A_dev, n_dev = nacc.cpu().numpy(), nxt.cpu().numpy()
+    # the device's softmax starts from its own logits: exp(dl / T) moves a probability,
+    # and its normaliser, by at most about err / T each
+    rel = 2 * err / T + SOFTMAX_REL_ERR
+    kinds = []
+    for b in range(B):
+        p = sampling.softmax(refs[b], T).astype(np.float32)
+        kind, detail = accept_explained(p, q[b], d[b], words[b], A_dev[b], n_dev[b], rel=rel)
+        log(f"seq {b} ctx {lengths[b]}: A device {A_dev[b]} next {n_dev[b]}: {kind} {detail}")
+        kinds.append(kind)
+    assert "mismatch" not in kinds and kinds.count("boundary") <= 2
+    assert len(set(A_dev.tolist())) > 1  # ragged acceptance: commit/rollback differ per sequence
 
 
 @pytest.mark.parametrize("B,g", [(13, 4), (16, 7), (25, 7)])

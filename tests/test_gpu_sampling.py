@@ -6,7 +6,7 @@ import pytest
 
 from oracle import kvstate, philox, sampling
 from paper_2608_10362_amd import binding, synth
-from tests.gpu_util import f32, i32, log, torch_cuda, u32_tensor
+from tests.gpu_util import accept_explained, f32, i32, log, torch_cuda, u32_tensor
 
 pytestmark = pytest.mark.gpu
 
@@ -170,13 +170,17 @@ def test_accept_logits_mode_matches_oracle():
     binding.specdec_accept(B, g, V, binding.INPUT_LOGITS, T, f32(logits), f32(q), i32(d), g, u32_tensor(words), 0, 0,
                            nacc, nxt)
     A_gpu, n_gpu = nacc.cpu().numpy(), nxt.cpu().numpy()
-    same = 0
+    kinds = []
     for b in range(B):
         p = sampling.softmax(logits[b].astype(np.float64), T).astype(np.float32)
-        A, n = sampling.accept_sampling(p, q[b], d[b], [int(w) for w in words[b, :g]], int(words[b, g]))
-        same += (A_gpu[b], n_gpu[b]) == (A, n)
-    # float32 softmax on the GPU vs float64 in the oracle: decisions may only differ at a boundary
-    assert same >= B - 1, (same, B)
+        kind, detail = accept_explained(p, q[b], d[b], words[b], A_gpu[b], n_gpu[b])
+        if kind != "equal":
+            log(f"row {b}: {kind}: {detail}")
+        kinds.append(kind)
+    # float32 softmax on the GPU vs float64 in the oracle: a decision may only
+    # differ where the oracle's own decision is within the float32 error of flipping
+    assert "mismatch" not in kinds
+    assert kinds.count("boundary") <= 1
 
 
 @pytest.mark.parametrize("role", [binding.ROLE_TARGET, binding.ROLE_DRAFT])
