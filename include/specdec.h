@@ -58,7 +58,8 @@ typedef enum {
   SPECDEC_ERR_NONFINITE = -4,   /* NaN/Inf probability or logit (device status) */
   SPECDEC_ERR_HIP = -5,         /* a HIP runtime call failed */
   SPECDEC_ERR_UNSUPPORTED = -6, /* valid request outside what is implemented */
-  SPECDEC_ERR_BAD_TOKEN = -7    /* token id outside [0, vocab) (device status) */
+  SPECDEC_ERR_BAD_TOKEN = -7,   /* token id outside [0, vocab) (device status) */
+  SPECDEC_ERR_SCRATCH_LIMIT = -8 /* needs more than the static scratch of specdec_accept_noalloc */
 } specdec_status;
 
 enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1 };
@@ -290,6 +291,27 @@ SPECDEC_API specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t 
 /* Bytes of the accept workspace for `batch` sequences of gamma+1 rows over a
  * vocabulary of `vocab` (0 for arguments specdec_accept rejects). */
 SPECDEC_API size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, int32_t vocab);
+
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture that may not call hipMalloc, tight serving loops, harnesses that
+ * forbid allocation.  specdec_accept without the workspace argument; every
+ * other argument, the result and the device status are those of
+ * specdec_accept, and the kernels are the same.
+ * Scratch: a static device array of SPECDEC_ACCEPT_NOALLOC_SCRATCH_BYTES in the
+ * library, held by each GPU the library runs on until the process ends; no
+ * call allocates or frees memory.  A request needing more scratch than the
+ * array (specdec_accept_workspace_bytes(batch, gamma, vocab) bytes, e.g. up to
+ * 64 sequences at gamma 8 over a 32000-token vocabulary) returns
+ * SPECDEC_ERR_SCRATCH_LIMIT and launches nothing.  Every call on one GPU
+ * shares the array and nothing in it needs to start at zero; calls that
+ * overlap on one GPU (unordered streams, or threads) race on it and must not
+ * be issued. */
+#define SPECDEC_ACCEPT_NOALLOC_SCRATCH_BYTES ((size_t)2 << 20)
+SPECDEC_API specdec_status specdec_accept_noalloc(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind,
+                                                  float temperature, const float* p, const float* q, const int32_t* d,
+                                                  int32_t ld_d, const uint32_t* rand, uint64_t seed, uint64_t step,
+                                                  int32_t* n_accepted, int32_t* next_token, int32_t* status,
+                                                  void* stream);
 
 /* KV commit / rollback after specdec_accept (device-side, graph friendly):
  *  TARGET: len += A+1; pending = [next]                       (n_pending = 1)

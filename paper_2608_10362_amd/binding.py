@@ -25,7 +25,12 @@ PURPOSE_DRAFT, PURPOSE_ACCEPT, PURPOSE_RESAMPLE = 0, 1, 2
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape", -3: "KV capacity exceeded",
           -4: "non-finite probability or logit", -5: "HIP runtime error", -6: "unsupported request",
-          -7: "token id out of range"}
+          -7: "token id out of range",
+          -8: "request needs more scratch than the static no-allocation buffer holds"}
+
+
+# Size of the static scratch of specdec_accept_noalloc (SPECDEC_ACCEPT_NOALLOC_SCRATCH_BYTES).
+ACCEPT_NOALLOC_SCRATCH_BYTES = 2 << 20
 
 
 class SpecdecError(RuntimeError):
@@ -100,6 +105,10 @@ _SIGS = {
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                       ctypes.c_void_p]),
     "specdec_accept_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "specdec_accept_noalloc": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_packed_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]),
     "specdec_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
@@ -489,6 +498,25 @@ def specdec_accept(batch: int, gamma: int, vocab: int, input_kind: int, temperat
     _check(lib().specdec_accept(batch, gamma, vocab, input_kind, temperature, p.data_ptr(), _ptr(q), _ptr(d), ld_d,
                                 _ptr(rand), seed, step, n_accepted.data_ptr(), next_token.data_ptr(), _ptr(status),
                                 workspace.data_ptr(), workspace.numel(), _stream(stream)), "specdec_accept")
+
+
+def specdec_accept_noalloc(batch: int, gamma: int, vocab: int, input_kind: int, temperature: float, p, q, d,
+                           ld_d: int, rand, seed: int, step: int, n_accepted, next_token, status=None, stream=None):
+    """specdec_accept with the library's static scratch (no workspace, no allocation)."""
+    import torch
+    _dev(p, "p", torch.float32, batch * (gamma + 1) * vocab)
+    _dev(q, "q", torch.float32, batch * gamma * vocab, optional=temperature == 0 or gamma == 0)
+    _dev(d, "d", torch.int32, (batch - 1) * ld_d + gamma, optional=gamma == 0)
+    if rand is not None:
+        _dev(rand, "rand", rand.dtype, batch * (gamma + 1))
+        if rand.dtype not in (torch.int32, torch.uint32):
+            raise ValueError("rand: expected 32-bit words")
+    _dev(n_accepted, "n_accepted", torch.int32, batch)
+    _dev(next_token, "next_token", torch.int32, batch)
+    _dev(status, "status", torch.int32, 1, optional=True)
+    _check(lib().specdec_accept_noalloc(batch, gamma, vocab, input_kind, temperature, p.data_ptr(), _ptr(q), _ptr(d),
+                                        ld_d, _ptr(rand), seed, step, n_accepted.data_ptr(), next_token.data_ptr(),
+                                        _ptr(status), _stream(stream)), "specdec_accept_noalloc")
 
 
 def specdec_kv_commit(kv: KVCache, gamma: int, role: int, n_accepted, d, ld_d: int, next_token, stream=None):

@@ -855,17 +855,33 @@ size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, int32_t voca
   return sampling_scratch_bytes(batch, gamma + 1, vocab);
 }
 
+}  // extern "C"
+
+namespace {
+// Argument checks shared by specdec_accept and specdec_accept_noalloc.
+specdec_status check_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
+                            const float* p, const float* q, const int32_t* d, int32_t ld_d,
+                            const int32_t* n_accepted, const int32_t* next_token) {
+  if (batch <= 0 || gamma < 0 || vocab <= 0 || !p || !n_accepted || !next_token || !(temperature >= 0.f))
+    return SPECDEC_ERR_INVALID_ARG;
+  if (gamma > 31) return SPECDEC_ERR_UNSUPPORTED;
+  if (input_kind != SPECDEC_INPUT_PROBS && input_kind != SPECDEC_INPUT_LOGITS) return SPECDEC_ERR_INVALID_ARG;
+  if (gamma > 0 && (!d || ld_d < gamma)) return SPECDEC_ERR_INVALID_ARG;
+  if (temperature > 0.f && gamma > 0 && !q) return SPECDEC_ERR_INVALID_ARG;
+  return SPECDEC_OK;
+}
+}  // namespace
+
+extern "C" {
+
 specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
                               const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
                               uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
                               int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
-  if (batch <= 0 || gamma < 0 || vocab <= 0 || !p || !n_accepted || !next_token || !(temperature >= 0.f))
-    return SPECDEC_ERR_INVALID_ARG;
-  if (gamma > 31) return SPECDEC_ERR_UNSUPPORTED;
+  const specdec_status st = check_accept(batch, gamma, vocab, input_kind, temperature, p, q, d, ld_d, n_accepted,
+                                         next_token);
+  if (st != SPECDEC_OK) return st;
   if (!workspace || workspace_bytes < sampling_scratch_bytes(batch, gamma + 1, vocab)) return SPECDEC_ERR_INVALID_ARG;
-  if (input_kind != SPECDEC_INPUT_PROBS && input_kind != SPECDEC_INPUT_LOGITS) return SPECDEC_ERR_INVALID_ARG;
-  if (gamma > 0 && (!d || ld_d < gamma)) return SPECDEC_ERR_INVALID_ARG;
-  if (temperature > 0.f && gamma > 0 && !q) return SPECDEC_ERR_INVALID_ARG;
   AcceptArgs a{};
   a.B = batch;
   a.gamma = gamma;
@@ -883,6 +899,37 @@ specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32
   a.next_token = next_token;
   a.status = status;
   a.scratch = workspace;
+  Timed t(SPECDEC_KERNEL_ACCEPT, (hipStream_t)stream);
+  return hip_status(launch_accept(a, (hipStream_t)stream));
+}
+
+specdec_status specdec_accept_noalloc(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind,
+                                      float temperature, const float* p, const float* q, const int32_t* d,
+                                      int32_t ld_d, const uint32_t* rand, uint64_t seed, uint64_t step,
+                                      int32_t* n_accepted, int32_t* next_token, int32_t* status, void* stream) {
+  const specdec_status st = check_accept(batch, gamma, vocab, input_kind, temperature, p, q, d, ld_d, n_accepted,
+                                         next_token);
+  if (st != SPECDEC_OK) return st;
+  if (sampling_scratch_bytes(batch, gamma + 1, vocab) > kStaticAcceptScratchBytes) return SPECDEC_ERR_SCRATCH_LIMIT;
+  void* scratch = nullptr;
+  if (static_accept_scratch(&scratch) != hipSuccess) return SPECDEC_ERR_HIP;
+  AcceptArgs a{};
+  a.B = batch;
+  a.gamma = gamma;
+  a.V = vocab;
+  a.input_kind = input_kind;
+  a.temperature = temperature;
+  a.p = p;
+  a.q = q;
+  a.d = d;
+  a.ld_d = ld_d;
+  a.rand = rand;
+  a.seed = seed;
+  a.step = step;
+  a.n_accepted = n_accepted;
+  a.next_token = next_token;
+  a.status = status;
+  a.scratch = scratch;  // (the device address of the static array, never the array's host-side name)
   Timed t(SPECDEC_KERNEL_ACCEPT, (hipStream_t)stream);
   return hip_status(launch_accept(a, (hipStream_t)stream));
 }
@@ -1010,6 +1057,7 @@ const char* specdec_status_string(specdec_status s) {
     case SPECDEC_ERR_HIP: return "HIP runtime error";
     case SPECDEC_ERR_UNSUPPORTED: return "unsupported request";
     case SPECDEC_ERR_BAD_TOKEN: return "token id out of range";
+    case SPECDEC_ERR_SCRATCH_LIMIT: return "request needs more scratch than the static no-allocation buffer holds";
   }
   return "unknown status";
 }

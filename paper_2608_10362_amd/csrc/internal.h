@@ -215,6 +215,10 @@ struct AcceptArgs {
   void* scratch;         // sampling_scratch_bytes(B, gamma + 1, V) bytes
 };
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+// The no-allocation accept's static scratch: its size, and its address on the
+// current device (looked up on the device's first call).
+constexpr size_t kStaticAcceptScratchBytes = SPECDEC_ACCEPT_NOALLOC_SCRATCH_BYTES;
+hipError_t static_accept_scratch(void** out);
 
 hipError_t launch_sample(int B, int V, const float* probs, int64_t ld, const uint32_t* rand, uint64_t seed,
                          uint64_t step, int purpose, int index, int32_t* out, hipStream_t s);

@@ -7,6 +7,8 @@
 // S = sum R_j, t = floor(x * S / 2^32) for a 32-bit word x, and returns the
 // smallest j with R_0 + ... + R_j > t.  Every sum is an integer sum, so the
 // result does not depend on how the block splits and orders the reduction.
+#include <mutex>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -659,6 +661,34 @@ hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
   f.ld_out = a.ld_d;
   hipLaunchKernelGGL(draw_final_kernel, dim3(a.B), dim3(kChunkThreads), 0, s, f);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- static scratch of the no-allocation accept
+// Device scratch of specdec_accept_noalloc: a file-scope array each GPU the
+// library runs on holds until the process ends.  In host code the array's name
+// is not a device address; its address on the current device comes from
+// hipGetSymbolAddress, looked up once per device (on that device's first call)
+// and kept.  Every call on a GPU shares the array.
+static __device__ __align__(256) unsigned char scratch[kStaticAcceptScratchBytes];
+
+hipError_t static_accept_scratch(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    ptr[dev] = p;
+  }
+  *out = ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {

@@ -116,6 +116,15 @@ def test_call_argument_errors_before_any_launch(lib):
                               None) == -1
     assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, fake, ws - 1,
                               None) == -1
+    # the no-allocation accept: the same argument errors, and a request beyond its
+    # static scratch is refused before any HIP call
+    assert lib.specdec_accept_noalloc(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None,
+                                      None) == -1
+    assert lib.specdec_accept_noalloc(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, fake, fake, None,
+                                      None) == -6
+    assert lib.specdec_accept_workspace_bytes(200, 8, 200000) > binding.ACCEPT_NOALLOC_SCRATCH_BYTES
+    assert lib.specdec_accept_noalloc(200, 8, 200000, 0, 1.0, fake, fake, fake, 8, None, 0, 0, fake, fake, None,
+                                      None) == -8
     assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1
     assert lib.specdec_sample(1, 10, None, 10, None, 0, 0, 0, 0, None, None) == -1
     assert lib.specdec_draw_u32(1, 0, 0, 0x10000, 0, ctypes.c_void_p(256), None) == -1

@@ -1,0 +1,82 @@
+"""The no-allocation accept (specdec_accept_noalloc, static device scratch)
+against specdec_accept with a caller workspace, through the C ABI: the
+accepted counts, next tokens and device status must be identical, on calls in
+a row whose sizes shrink (the static scratch keeps the previous call's
+contents, which must not matter)."""
+import numpy as np
+import pytest
+
+from oracle import sampling
+from paper_2608_10362_amd import binding, synth
+from tests.gpu_util import f32, i32, log, torch_cuda, u32_tensor
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(B, g, V, kind, T, explicit, seed, nan_row=None):
+    rng = np.random.default_rng(seed)
+    if kind == binding.INPUT_LOGITS:
+        p = (rng.standard_normal((B, g + 1, V)) * 1.3).astype(np.float32)
+        q = sampling.softmax(rng.standard_normal((B, g, V)) * 1.3 + p[:, :g] * 0.5, T if T > 0 else 1.0)
+    else:
+        p = synth.make_prob_rows(B * (g + 1), V, seed=seed, concentration=0.7).reshape(B, g + 1, V)
+        q = synth.make_prob_rows(B * g, V, seed=seed + 1, concentration=0.7).reshape(B, g, V)
+        q = 0.5 * q + 0.5 * p[:, :g]
+    q = q.astype(np.float32)
+    d = np.array([[sampling.sample_fixed_point(q[b, i], int(rng.integers(0, 2 ** 32))) for i in range(g)]
+                  for b in range(B)], np.int32).reshape(B, g)
+    if nan_row is not None:
+        p[nan_row, 0, 1] = np.nan
+    words = synth.make_rand_u32((B, g + 1), seed=seed + 2) if explicit else None
+    return p, q, d, words
+
+
+def _run_both(B, g, V, kind, T, explicit, seed, nan_row=None):
+    torch = torch_cuda()
+    p, q, d, words = _case(B, g, V, kind, T, explicit, seed, nan_row)
+    pd, qd, dd = f32(p), f32(q), i32(d)
+    rd = u32_tensor(words) if words is not None else None
+    outs = []
+    for noalloc in (False, True):
+        nacc = torch.full((B,), -9, dtype=torch.int32, device="cuda")
+        nxt = torch.full((B,), -9, dtype=torch.int32, device="cuda")
+        status = torch.zeros(1, dtype=torch.int32, device="cuda")
+        if noalloc:
+            binding.specdec_accept_noalloc(B, g, V, kind, T, pd, qd if T > 0 else None, dd, g, rd, 11, 5, nacc, nxt,
+                                           status)
+        else:
+            binding.specdec_accept(B, g, V, kind, T, pd, qd if T > 0 else None, dd, g, rd, 11, 5, nacc, nxt, status)
+        torch.cuda.synchronize()
+        outs.append((nacc.cpu().numpy(), nxt.cpu().numpy(), int(status.item())))
+    (a0, n0, s0), (a1, n1, s1) = outs
+    log(f"B={B} g={g} V={V} kind={kind} T={T} explicit={explicit}: A {a1.tolist()[:8]} status {s1}")
+    np.testing.assert_array_equal(a1, a0)
+    np.testing.assert_array_equal(n1, n0)
+    assert s1 == s0
+    return a1, n1, s1
+
+
+def test_noalloc_accept_equals_workspace_accept_on_shrinking_calls():
+    # a large call, then a smaller one over the same static scratch, then greedy and an error
+    a, n, s = _run_both(16, 6, 32000, binding.INPUT_LOGITS, 0.8, False, 21)
+    assert s == 0 and len(set(a.tolist())) > 1
+    a, n, s = _run_both(3, 4, 5000, binding.INPUT_PROBS, 1.0, True, 22)
+    assert s == 0
+    a, n, s = _run_both(5, 3, 777, binding.INPUT_LOGITS, 0.0, False, 23)
+    assert s == 0
+    a, n, s = _run_both(4, 2, 3000, binding.INPUT_PROBS, 1.0, True, 24, nan_row=2)
+    assert s == -4 and a[2] == -1
+
+
+def test_noalloc_accept_refuses_requests_beyond_its_scratch():
+    torch = torch_cuda()
+    B, g, V = 200, 8, 200000
+    assert binding.specdec_accept_workspace_bytes(B, g, V) > binding.ACCEPT_NOALLOC_SCRATCH_BYTES
+    dummy = torch.zeros(1, dtype=torch.float32, device="cuda")
+    with pytest.raises(binding.SpecdecError) as e:
+        binding.lib()  # (loaded)
+        st = binding.lib().specdec_accept_noalloc(B, g, V, binding.INPUT_PROBS, 1.0, dummy.data_ptr(),
+                                                  dummy.data_ptr(), dummy.data_ptr(), g, None, 0, 0,
+                                                  dummy.data_ptr(), dummy.data_ptr(), None, None)
+        binding._check(st, "specdec_accept_noalloc")
+    assert e.value.status == -8
