@@ -717,7 +717,10 @@ def main():
                    "hip_graph": use_graph, "weights": args.weights},
         "roofline": {"bound": "hbm", "kernel": f"gemm {dom}", "achieved": round(achieved, 1),
                      "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                     "traffic": None if int4 else measured_traffic(dom), "bytes_per_launch": dom_bytes},
+                     "traffic": None if int4 else measured_traffic(dom), "bytes_per_launch": dom_bytes,
+                     # the whole verify step (verify + accept) against the same peak
+                     "step": {"achieved": round(verify_GBps, 1), "frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
+                              "bytes": vbytes, "ms": round(verify_ms, 4)}},
         "verify_ms": round(verify_ms, 4),
         "verify_ms_p10_p50_p90": [round(tm["verify_ms_p10"], 4), round(tm["verify_ms_p50"], 4),
                                   round(tm["verify_ms_p90"], 4)],

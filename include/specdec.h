@@ -430,6 +430,10 @@ SPECDEC_API specdec_status specdec_time_kernel(const specdec_model* model, int32
 SPECDEC_API specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host_out);
 
 SPECDEC_API const char* specdec_status_string(specdec_status s);
+/* Name of the HIP error behind this thread's last SPECDEC_ERR_HIP (e.g.
+ * "hipErrorInvalidValue"), or "" if none; reading it clears it.  The string
+ * is static. */
+SPECDEC_API const char* specdec_last_hip_error(void);
 
 #ifdef __cplusplus
 }

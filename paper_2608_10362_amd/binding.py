@@ -126,6 +126,7 @@ _SIGS = {
                                         ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_device_status": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "specdec_last_hip_error": (ctypes.c_char_p, []),
     "specdec_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
     "specdec_timing_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_time_kernel": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
@@ -153,6 +154,8 @@ def lib() -> ctypes.CDLL:
 
 def _check(status: int, what: str):
     if status != 0:
+        if status == -5:  # name the HIP error behind it
+            what = f"{what} [{lib().specdec_last_hip_error().decode()}]"
         raise SpecdecError(status, what)
 
 

@@ -149,7 +149,14 @@ specdec_status check_desc(const specdec_model_desc* d) {
   return SPECDEC_OK;
 }
 
-specdec_status hip_status(hipError_t e) { return e == hipSuccess ? SPECDEC_OK : SPECDEC_ERR_HIP; }
+// The last HIP error a call of this thread returned SPECDEC_ERR_HIP for.
+thread_local hipError_t g_last_hip_error = hipSuccess;
+
+specdec_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return SPECDEC_OK;
+  g_last_hip_error = e;
+  return SPECDEC_ERR_HIP;
+}
 
 // Packed image: LM head, then per layer Wq, Wk, Wv, Wo, W_gate, W_up, W_down,
 // each 256-byte aligned.  Returns the bytes and the (N, K, byte offset) list.
@@ -211,7 +218,7 @@ size_t image_bytes(const specdec_model_desc* d, int n_layers, int fmt, std::vect
 #define SD_TRY(expr)                                   \
   do {                                                 \
     hipError_t _e = (expr);                            \
-    if (_e != hipSuccess) return SPECDEC_ERR_HIP;      \
+    if (_e != hipSuccess) return hip_status(_e);       \
   } while (0)
 
 int32_t* kv_len(const specdec_kv* kv) { return kv->state; }
@@ -1045,6 +1052,12 @@ specdec_status specdec_time_kernel(const specdec_model* m, int32_t kind, int32_t
   if (err != hipSuccess) return SPECDEC_ERR_HIP;
   *avg_us = 1e3 * (double)ms / reps;
   return SPECDEC_OK;
+}
+
+const char* specdec_last_hip_error(void) {
+  const hipError_t e = g_last_hip_error;
+  g_last_hip_error = hipSuccess;
+  return e == hipSuccess ? "" : hipGetErrorName(e);
 }
 
 const char* specdec_status_string(specdec_status s) {

@@ -311,14 +311,20 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     asm volatile("" ::: "memory");
 
     // nk = max(pos) + 1 over the tile's valid query rows: no key past it is read.
+    // (Lane reads rather than shuffles: the compiler then waits for the row
+    // descriptors alone, with the K, Q and V loads above still in flight; with
+    // shuffles it held the Q and V loads back until the descriptors arrived.)
     const int mypos = (lane < 16 && ql < nq && rd_valid) ? rd_pos : -1;
-    int nk = mypos + 1;
+    int lp[16];
 #pragma unroll
-    for (int o = 8; o > 0; o >>= 1) nk = max(nk, __shfl_xor(nk, o, kWave));
-    nk = __shfl(nk, 0, kWave);
+    for (int i = 0; i < 16; ++i) lp[i] = __builtin_amdgcn_readlane(mypos, i);
+    int nk = lp[0] + 1;
+#pragma unroll
+    for (int i = 1; i < 16; ++i) nk = max(nk, lp[i] + 1);
     // positions of the 4 query rows this lane holds in the C layout (-1: none)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) qpos[r] = __shfl(mypos, 4 * grp + r, kWave);
+    for (int r = 0; r < 4; ++r)
+      qpos[r] = grp == 0 ? lp[r] : (grp == 1 ? lp[4 + r] : (grp == 2 ? lp[8 + r] : lp[12 + r]));
     const float scale = 1.0f / sqrtf((float)HD);
     bf16x8 qhi[KST], qlo[KST];
 #pragma unroll
