@@ -620,20 +620,25 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
     }
   }
   if (PIPE) {
+    // A buffer is refilled as soon as its batch has been multiplied, before the
+    // tile's reduction and epilogue (which use only the accumulators, LDS and
+    // the epilogue inputs fetched with that batch): two batches stay in flight
+    // across tile boundaries.
+    // (Not for the INT4 three-tile kernels over more than 16 rows: the longer
+    // live ranges there cost spills.)
+    constexpr bool EARLY = !(Q4 && MT >= 2);
     while (q < total) {
       compute(wA, xA, q);
+      if (EARLY && q + 2 < total) load(q + 2, wA, xA);
       finish(q, pA);
-      if (q + 2 < total) {
-        load(q + 2, wA, xA);
-        epi_fetch(q + 2, pA);
-      }
+      if (!EARLY && q + 2 < total) load(q + 2, wA, xA);
+      if (q + 2 < total) epi_fetch(q + 2, pA);
       if (++q >= total) break;
       compute(wB, xB, q);
+      if (EARLY && q + 2 < total) load(q + 2, wB, xB);
       finish(q, pB);
-      if (q + 2 < total) {
-        load(q + 2, wB, xB);
-        epi_fetch(q + 2, pB);
-      }
+      if (!EARLY && q + 2 < total) load(q + 2, wB, xB);
+      if (q + 2 < total) epi_fetch(q + 2, pB);
       ++q;
     }
   } else {
