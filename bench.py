@@ -59,6 +59,11 @@ def parse():
                          "memory into a resident slot on a side stream, alone and under concurrent verify steps")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one 1 GiB device-to-device copy (reference for the HBM byte counters)")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="instead of the verify line, measure the streaming-read ceiling (64 MiB .. 4 GiB, cold)")
+    ap.add_argument("--kernels-only", action="store_true",
+                    help="only the 7B verify's kernels, each re-launched 20 times layer after layer, plus one 1 GiB "
+                         "streaming read and one 1 GiB copy (the launches a counter profile of the kernels reads)")
     return ap.parse_args()
 
 
@@ -142,22 +147,55 @@ def verify_step_bytes(shape, ctx, gamma, batch, weights="bf16"):
 
 
 def measured_traffic(kernel: str):
-    """HBM bytes per launch of the dominant GEMM from the committed rocprofv3 counter summary
-    (profiles/gemm_<kind>_7b_hbm_traffic.md), or None if absent or taken on other kernel source."""
+    """HBM bytes per launch of a verify GEMM from the committed rocprofv3 counter summary
+    (profiles/verify_7b_kernels_hbm_traffic.md), or None if absent or taken on other kernel source."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"gemm_{kernel}_7b_hbm_traffic.md")
+    path = os.path.join(ROOT, "profiles", "verify_7b_kernels_hbm_traffic.md")
     if not os.path.exists(path):
         return None
     fields = {}
     for line in open(path):
-        if ":" in line and not line.startswith(("|", "#", "`")):
+        if ":" in line and not line.startswith(("|", "#", "`", "-")):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
     src = os.path.join(ROOT, "paper_2608_10362_amd", "csrc", "gemm.hip")
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if fields.get("kernel_source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
+    if fields.get("kernel_source_sha256") != sha or f"traffic_{kernel}" not in fields:
         return None
-    return int(float(fields["traffic_bytes_per_launch"]))
+    return int(float(fields[f"traffic_{kernel}"]))
+
+
+# ---------------------------------------------------------------- streaming-read ceiling
+def read_ceiling(sizes_mib=(64, 256, 1024, 4096), buf_gib=8, reps=5):
+    """Read rate of the library's streaming-read probe (specdec_stream_read: the
+    weight stream's access pattern) over cold regions of an 8 GiB buffer: each
+    timed launch reads a region the launches just before it did not touch (the
+    last-level cache holds 256 MB).  Median of `reps` launches after one warm-up,
+    HIP events on the launch stream."""
+    import torch
+    from paper_2608_10362_amd import binding
+    buf = torch.empty(buf_gib << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+    out = {}
+    for mib in sizes_mib:
+        n = mib << 20
+        regions = (buf_gib << 30) // n
+        times = []
+        for r in range(reps + 1):
+            off = ((r * 2) % regions) * n  # (every other region: no neighbour left in the cache)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            binding.specdec_stream_read(buf[off:off + n], sink, stream=s)
+            e1.record(s)
+            e1.synchronize()
+            if r > 0:
+                times.append(e0.elapsed_time(e1) * 1e-3)
+        t = float(np.median(times))
+        out[f"{mib}MiB"] = {"bytes": n, "us": round(t * 1e6, 2), "GBps": round(n / t / 1e9, 1)}
+    del buf
+    torch.cuda.empty_cache()
+    return out
 
 
 # ---------------------------------------------------------------- CPU oracle baseline
@@ -582,6 +620,40 @@ def run_prefill(args):
 
 
 # ---------------------------------------------------------------- main
+def run_kernels_only(args, shape, B, g, ctx, cap):
+    """The verify pass's kernels alone (no draft, no graphs): one verify, then
+    each kernel kind re-launched 20 times by specdec_time_kernel (launch i runs
+    layer i mod 32, cold weights), then one 1 GiB streaming read and one 1 GiB
+    device copy.  Prints the per-kind average durations."""
+    import torch
+    from paper_2608_10362_amd import binding, synth
+    dw = device_weights(shape)
+    target = binding.Model(dw, shape.n_layers, max_rows=B * (g + 1), max_ctx=cap)
+    kv_t = binding.KVCache(target, B, cap)
+    install_context(kv_t, shape.n_layers, shape, [ctx] * B)
+    pend = synth.make_prompt(1, shape.vocab, batch=B)[:, 0]
+    kv_t.set_state(np.full(B, ctx, np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
+    drafts = torch.from_numpy(synth.make_prompt(g, shape.vocab, batch=B, seed=32)).cuda()
+    logits = torch.empty((B, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv_t, g, drafts, g, logits)
+    torch.cuda.synchronize()
+    kb = kernel_bytes(shape, ctx + g + 1)
+    out = {}
+    for k in ("embed", "qkv", "attention", "o_proj", "gate_up", "down", "lm_head"):
+        us = binding.specdec_time_kernel(target, k, reps=20)
+        out[k] = {"avg_us": round(us, 3), "launches": 20, "bytes": kb.get(k)}
+        log(f"{k}: {us:.2f} us")
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    binding.specdec_stream_read(src, sink)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"metric": "7B verify kernels, re-launched layer after layer", "kernels": out,
+                      "config": {"workload": f"7B-shaped bf16 verify, gamma={g}, batch {B}, context {ctx}"}}),
+          flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -597,6 +669,12 @@ def main():
     if args.prefill:
         run_prefill(args)
         return
+    if args.ceiling:
+        rc = read_ceiling()
+        print(json.dumps({"metric": "streaming-read ceiling (specdec_stream_read, cold regions)",
+                          "value": rc["1024MiB"]["GBps"], "unit": "GB/s", "n_gpus": 1, "peak_GBps": PEAK_HBM_GBPS,
+                          "frac_of_peak": round(rc["1024MiB"]["GBps"] / PEAK_HBM_GBPS, 4), "sizes": rc}), flush=True)
+        return
     if args.config == 4:
         run_switching(args)
         return
@@ -606,6 +684,9 @@ def main():
     shape = synth.LLAMA_7B
     B, g, ctx, T = args.batch, args.gamma, args.ctx, args.temperature
     cap = ((ctx + g + 2 + 63) // 64) * 64
+    if args.kernels_only:
+        run_kernels_only(args, shape, B, g, ctx, cap)
+        return
     t0 = time.time()
     dw = device_weights(shape, weight_format=args.weights)
     target = binding.Model(dw, shape.n_layers, max_rows=max(B * (g + 1), 2 * B), max_ctx=cap)
@@ -696,6 +777,7 @@ def main():
     achieved = dom_bytes / (kernels[dom]["avg_us"] * 1e-6) / 1e9
     vbytes = verify_step_bytes(shape, ctx, g, B, args.weights)
     verify_GBps = vbytes / (verify_ms * 1e-3) / 1e9
+    ceiling = read_ceiling(sizes_mib=(1024,))["1024MiB"]
     int4 = args.weights == "int4"
 
     result = {
@@ -720,12 +802,17 @@ def main():
                      "traffic": None if int4 else measured_traffic(dom), "bytes_per_launch": dom_bytes,
                      # the whole verify step (verify + accept) against the same peak
                      "step": {"achieved": round(verify_GBps, 1), "frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
-                              "bytes": vbytes, "ms": round(verify_ms, 4)}},
+                              "bytes": vbytes, "ms": round(verify_ms, 4),
+                              "frac_of_read_ceiling": round(verify_GBps / ceiling["GBps"], 4)},
+                     # the same device's streaming-read rate for the weight stream's access pattern
+                     "read_ceiling": {"GBps": ceiling["GBps"], "frac_of_peak": round(ceiling["GBps"] / PEAK_HBM_GBPS, 4),
+                                      "bytes": ceiling["bytes"], "kernel": "specdec_stream_read"}},
         "verify_ms": round(verify_ms, 4),
         "verify_ms_p10_p50_p90": [round(tm["verify_ms_p10"], 4), round(tm["verify_ms_p50"], 4),
                                   round(tm["verify_ms_p90"], 4)],
         "verify_hbm_GBps": round(verify_GBps, 1),
         "verify_hbm_frac": round(verify_GBps / PEAK_HBM_GBPS, 4),
+        "verify_frac_of_read_ceiling": round(verify_GBps / ceiling["GBps"], 4),
         "verify_bytes": vbytes,
         "generated_tokens_per_s": round(B * (mean_A + 1) / (step_ms * 1e-3), 2),
         "mean_accepted": round(mean_A, 3),

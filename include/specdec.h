@@ -429,6 +429,17 @@ SPECDEC_API specdec_status specdec_time_kernel(const specdec_model* model, int32
  * written to *host_out if non-NULL). */
 SPECDEC_API specdec_status specdec_device_status(specdec_kv* kv, void* stream, int32_t* host_out);
 
+/* Streaming-read ceiling (measurement): reads the first floor(bytes / 1024) KB
+ * at buf (device, 16-byte aligned) with the weight stream's access pattern:
+ * one 16-wave block per CU, each wave reading 1 KB per load, two batches of
+ * four loads per wave in flight, nontemporal.  The loaded data is XOR-ed into
+ * a value that is stored to *sink (device, 4 bytes) only in a case that does
+ * not occur for real data.  Asynchronous on `stream`; time it with events on
+ * that stream to get the device's read rate for this pattern.
+ * Errors: INVALID_ARG (null or misaligned pointer), HIP (a block's range above
+ * 4 GiB). */
+SPECDEC_API specdec_status specdec_stream_read(const void* buf, size_t bytes, uint32_t* sink, void* stream);
+
 SPECDEC_API const char* specdec_status_string(specdec_status s);
 /* Name of the HIP error behind this thread's last SPECDEC_ERR_HIP (e.g.
  * "hipErrorInvalidValue"), or "" if none; reading it clears it.  The string

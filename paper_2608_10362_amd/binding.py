@@ -127,6 +127,7 @@ _SIGS = {
     "specdec_device_status": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "specdec_last_hip_error": (ctypes.c_char_p, []),
+    "specdec_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
     "specdec_timing_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_time_kernel": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
@@ -557,6 +558,17 @@ def specdec_device_status(kv: KVCache, stream=None) -> int:
     out = ctypes.c_int32(0)
     lib().specdec_device_status(ctypes.byref(kv.kv), _stream(stream), ctypes.byref(out))
     return out.value
+
+
+def specdec_stream_read(buf, sink, nbytes=None, stream=None):
+    """Streaming-read ceiling probe over a device tensor (see the header)."""
+    _dev(buf, "buf", None, 1)
+    _dev(sink, "sink", None, 1)
+    size = buf.numel() * buf.element_size()
+    n = size if nbytes is None else int(nbytes)
+    if not 0 <= n <= size:
+        raise ValueError("nbytes: outside the buffer")
+    _check(lib().specdec_stream_read(buf.data_ptr(), n, sink.data_ptr(), _stream(stream)), "specdec_stream_read")
 
 
 def specdec_status_string(status: int) -> str:

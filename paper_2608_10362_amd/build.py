@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libspecdec.so")
-SOURCES = ["api.hip", "gemm.hip", "attention.hip", "sampling.hip"]
+SOURCES = ["api.hip", "gemm.hip", "attention.hip", "sampling.hip", "stream.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

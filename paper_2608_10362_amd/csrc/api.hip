@@ -1054,6 +1054,11 @@ specdec_status specdec_time_kernel(const specdec_model* m, int32_t kind, int32_t
   return SPECDEC_OK;
 }
 
+specdec_status specdec_stream_read(const void* buf, size_t bytes, uint32_t* sink, void* stream) {
+  if (!buf || !sink || ((uintptr_t)buf & 15)) return SPECDEC_ERR_INVALID_ARG;
+  return hip_status(launch_stream_read(buf, bytes, sink, (hipStream_t)stream));
+}
+
 const char* specdec_last_hip_error(void) {
   const hipError_t e = g_last_hip_error;
   g_last_hip_error = hipSuccess;

@@ -236,6 +236,9 @@ struct CommitArgs {
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t s);
 
+// Streaming-read ceiling probe (stream.hip): reads bytes / 1024 KB-chunks of buf.
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
+
 hipError_t launch_kv_copy(const KvLayout& kv, int layer, int b, int pos0, int n, const void* k, const void* v,
                           void* k_out, void* v_out, hipStream_t s);
 

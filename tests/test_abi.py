@@ -125,6 +125,8 @@ def test_call_argument_errors_before_any_launch(lib):
     assert lib.specdec_accept_workspace_bytes(200, 8, 200000) > binding.ACCEPT_NOALLOC_SCRATCH_BYTES
     assert lib.specdec_accept_noalloc(200, 8, 200000, 0, 1.0, fake, fake, fake, 8, None, 0, 0, fake, fake, None,
                                       None) == -8
+    assert lib.specdec_stream_read(None, 1024, fake, None) == -1
+    assert lib.specdec_stream_read(ctypes.c_void_p(257), 1024, fake, None) == -1  # (16-byte alignment)
     assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1
     assert lib.specdec_sample(1, 10, None, 10, None, 0, 0, 0, 0, None, None) == -1
     assert lib.specdec_draw_u32(1, 0, 0, 0x10000, 0, ctypes.c_void_p(256), None) == -1

@@ -52,3 +52,15 @@ def test_time_kernel_cycles_layers_and_keeps_the_context():
     after = logits.cpu().numpy()
     assert kv.read_state()["status"] == 0
     assert np.array_equal(before, after)
+
+
+def test_stream_read_reads_and_writes_nothing():
+    """The streaming-read ceiling probe over a buffer whose size is not a whole
+    number of its chunks: it runs, and it never writes its sink for real data."""
+    torch = torch_cuda()
+    buf = torch.ones((64 << 20) + 123, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    binding.specdec_stream_read(buf, sink)
+    binding.specdec_stream_read(buf, sink, nbytes=5000)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 0
