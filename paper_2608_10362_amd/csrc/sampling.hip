@@ -174,15 +174,15 @@ __global__ __launch_bounds__(256) void rows_embed_kernel(RowsArgs a) {
 }
 
 // ---------------------------------------------------------------- multi-block softmax / accept / draw
-// A vocabulary row is cut into NC chunks; one block per (chunk, row) so that
-// a single decision uses many CUs:
-//   stats     per (chunk, row): online (max, sum exp) of z = x / T, argmax, finiteness
-//   decide    per sequence: merge the chunk statistics (fixed order), accept scan
-//   partials  per (chunk, sequence): integer weight sums of the row to draw from
-//             (the draft's q is also written here)
-//   final     per sequence: find the chunk holding t, scan it, emit the token
+// A vocabulary row is cut into NC chunks so that a single decision uses many
+// CUs, in two launches:
+//   stats         per (chunk, row): online (max, sum exp) of z = x / T, argmax, finiteness
+//   decide-draw   per (chunk, sequence): every block merges the chunk statistics
+//                 (fixed order) and takes the decision; each sums the integer
+//                 weights of its chunk of the row to draw from (the draft's q is
+//                 also written here); the last block of the sequence finds the
+//                 chunk holding t, scans it and emits the token
 constexpr int kChunkThreads = 256;
-constexpr int kMfmaWavesSamp = 16;  // waves of the decide kernel
 
 __host__ __device__ __forceinline__ int n_chunks(int V) {
   int nc = (V + 1023) / 1024;
@@ -197,6 +197,7 @@ struct StatPart {
 struct DrawPart {
   unsigned long long res, prob;
 };
+// A sequence's decision, kept in LDS by every block of the decide-and-draw launch.
 struct SeqState {
   int A;            // accepted count (-1 error, -2 no draw needed)
   int pad;
@@ -205,8 +206,8 @@ struct SeqState {
 
 struct Scratch {
   StatPart* stats;  // [rows_total][NC]
-  SeqState* seq;    // [B]
   DrawPart* draw;   // [B][NC]
+  uint32_t* count;  // [B] blocks of the decide-and-draw launch done (zeroed by the stats launch)
 };
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 __host__ __device__ inline Scratch carve(void* base, int B, int rows, int V) {
@@ -215,9 +216,9 @@ __host__ __device__ inline Scratch carve(void* base, int B, int rows, int V) {
   Scratch s;
   s.stats = (StatPart*)p;
   p += align256(sizeof(StatPart) * (size_t)B * rows * NC);
-  s.seq = (SeqState*)p;
-  p += align256(sizeof(SeqState) * (size_t)B);
   s.draw = (DrawPart*)p;
+  p += align256(sizeof(DrawPart) * (size_t)B * NC);
+  s.count = (uint32_t*)p;
   return s;
 }
 
@@ -231,13 +232,15 @@ __device__ __forceinline__ float prob_of(const float* row, int j, bool logits, f
 // x + (b * row_stride + row_off + i) * V.
 // Every value of the row, and of the row `chk` pairs with it (the draft's q
 // row i of an accept, rows i < chk_rows), must be finite.
+// It also zeroes the sequence's counter of the decide-and-draw launch that follows.
 __global__ __launch_bounds__(kChunkThreads) void stats_kernel(const float* x, int V, int rows_per_seq, int row_stride,
                                                               int row_off, float T, const float* chk, int chk_rows,
-                                                              StatPart* out) {
+                                                              StatPart* out, uint32_t* count) {
   __shared__ float sm_m[4], sm_s[4], sm_v[4];
   __shared__ int sm_i[4], sm_b[4];
   const int c = blockIdx.x, r = blockIdx.y, NC = gridDim.x;
   const int b = r / rows_per_seq, i = r % rows_per_seq;
+  if (c == 0 && i == 0 && threadIdx.x == 0) count[b] = 0u;
   const float* row = x + ((size_t)b * row_stride + row_off + i) * V;
   const int cs = chunk_size(V), j0 = c * cs, j1 = min(V, j0 + cs);
   MaxSum st{-INFINITY, 0.f};
@@ -300,90 +303,31 @@ __device__ StatPart wave_merge_stats(const StatPart* parts, int NC) {
   return p;
 }
 
-// decide: grid B, block 1024.  Wave w merges the statistics of rows w, w+16;
-// then wave 0 evaluates the gamma accept tests in parallel lanes and takes
-// the first event (rejection or error) in draft order.
-__global__ __launch_bounds__(1024) void accept_decide_kernel(AcceptArgs a) {
-  const int b = blockIdx.x, g = a.gamma, V = a.V, NC = n_chunks(V);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  Scratch sc = carve(a.scratch, a.B, g + 1, V);
-  const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
-  const float T = a.temperature;
-  __shared__ int amax[kMaxGamma + 1];
-  __shared__ float2 ms[kMaxGamma + 1];
-  __shared__ int bad_rows;
-  if (threadIdx.x == 0) bad_rows = 0;
-  __syncthreads();
-  for (int r = w; r <= g; r += kMfmaWavesSamp) {
-    const StatPart p = wave_merge_stats(sc.stats + ((size_t)b * (g + 1) + r) * NC, NC);
-    if (lane == 0) {
-      amax[r] = p.amax_i;
-      ms[r] = make_float2(p.m, p.s);
-      sc.seq[b].ms[r] = make_float2(p.m, p.s);
-      if (p.bad || (logits && T > 0.f && (!isfinite(p.m) || !isfinite(p.s)))) atomicOr(&bad_rows, 1);
-    }
-  }
-  __syncthreads();
-  if (w != 0) return;
-  const int32_t* d = a.d + (size_t)b * a.ld_d;
-  int bad = bad_rows;
-  int A = g;
-  if (!bad) {
-    // lane i < g: event of draft position i (1 = rejection, 2 = error)
-    int ev = 0;
-    if (lane < g) {
-      const int di = d[lane];
-      if (T == 0.f) {
-        ev = amax[lane] != di ? 1 : 0;
-      } else if (di < 0 || di >= V) {
-        ev = 2;
-      } else {
-        const float pd = prob_of(a.p + ((size_t)b * (g + 1) + lane) * V, di, logits, T, ms[lane]);
-        const float qd = a.q[((size_t)b * g + lane) * V + di];
-        const uint32_t wd = a.rand ? a.rand[(size_t)b * (g + 1) + lane]
-                                   : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, lane);
-        ev = !isfinite(qd) ? 2 : (!(__fmul_rn(word_to_uniform(wd), qd) < pd) ? 1 : 0);
-      }
-    }
-    const unsigned long long hit = __ballot(ev != 0);
-    if (hit) {
-      const int first = __ffsll(hit) - 1;
-      if (__shfl(ev, first, kWave) == 2) bad = 1;
-      else A = first;
-    }
-  }
-  if (lane != 0) return;
-  if (bad) {
-    set_status(a.status, kStatusNonFinite);
-    a.n_accepted[b] = -1;
-    a.next_token[b] = -1;
-    sc.seq[b].A = -1;
-  } else if (T == 0.f) {
-    a.n_accepted[b] = A;
-    a.next_token[b] = amax[A];
-    sc.seq[b].A = -2;
-  } else {
-    a.n_accepted[b] = A;
-    sc.seq[b].A = A;
-  }
-}
-
 // Weight sources of a draw.
 enum { W_ACCEPT = 0, W_DRAFT = 1 };
 
 struct DrawArgs {
   int mode, B, V, gamma;
   float T;
-  // accept
+  // accept: p rows [B, gamma+1, V] (probabilities or logits), q rows [B, gamma, V], drafts
   const float* p;
   const float* q;
   int logits;
-  // draft: logits of the proposing rows, q output
+  const int32_t* d;
+  int ld_d;
+  // draft: logits of the proposing rows (the last of rps per sequence), q output
   const float* lg;
   int rps, slot;
   float* q_out;
   void* scratch;
   int rows;  // rows per sequence in the scratch statistics
+  // the words of the draws, the outputs
+  const uint32_t* rand;   // accept: [B, gamma+1] (accept words, then the resample word); draft: [B]
+  uint64_t seed, step;
+  int32_t* n_accepted;    // accept only
+  int32_t* out;           // accept: next_token[B]; draft: d_out + slot (stride ld_out)
+  int ld_out;
+  int32_t* status;
 };
 
 // R_j weights of sequence b at column j, for the residual (res) and the plain row (prob).
@@ -401,69 +345,140 @@ __device__ __forceinline__ void weights_at(const DrawArgs& a, const SeqState& st
   }
 }
 
-// partials: grid (NC, B), block 256.
-__global__ __launch_bounds__(kChunkThreads) void draw_partials_kernel(DrawArgs a) {
-  __shared__ unsigned long long sr[4], sp[4];
-  const int c = blockIdx.x, b = blockIdx.y, V = a.V;
-  Scratch sc = carve(a.scratch, a.B, a.rows, V);
-  const SeqState& st = sc.seq[b];
-  if (st.A < 0) return;
-  const int cs = chunk_size(V), j0 = c * cs, j1 = min(V, j0 + cs);
-  unsigned long long r_sum = 0, p_sum = 0;
-  float* qo = a.mode == W_DRAFT && a.q_out ? a.q_out + ((size_t)b * a.gamma + a.slot) * V : nullptr;
-  for (int j = j0 + threadIdx.x; j < j1; j += kChunkThreads) {
-    float res, prob;
-    weights_at(a, st, b, j, res, prob);
-    if (qo) qo[j] = prob;
-    r_sum += fp_weight(res);
-    p_sum += fp_weight(prob);
-  }
-  r_sum = wave_sum_u64(r_sum);
-  p_sum = wave_sum_u64(p_sum);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) { sr[w] = r_sum; sp[w] = p_sum; }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    DrawPart d{0ull, 0ull};
-    for (int k = 0; k < kChunkThreads / kWave; ++k) { d.res += sr[k]; d.prob += sp[k]; }
-    sc.draw[(size_t)b * gridDim.x + c] = d;
-  }
-}
-
-struct FinalArgs {
-  DrawArgs d;
-  const uint32_t* rand;   // accept: [B, gamma+1] (word gamma); draft: [B]
-  uint64_t seed, step;
-  int32_t* out;           // accept: next_token[B]; draft: d_out + slot
-  int ld_out;
-};
-
-// final: grid B, block 256.
-__global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) {
-  __shared__ unsigned long long wtot[4];
-  __shared__ int chunk_sel, use_res, done;
+// decide-and-draw: grid (NC, B), block 256.  Every block of sequence b first
+// takes the sequence's decision itself, from the chunk statistics of the stats
+// launch (merged in a fixed order: every block reaches the same result):
+//   accept: the row statistics, then the gamma accept tests in parallel lanes,
+//           the first event (rejection or error) in draft order wins;
+//   draft:  the proposing row's statistics.
+// Greedy decisions and errors are written by block 0 and end there.  Otherwise
+// block c sums the integer weights of its chunk of the row to draw from (the
+// residual and the plain row; the draft's q chunk is written here), publishes
+// them with agent-scope stores and counts itself; the last block of the
+// sequence finds the chunk holding t (a wave prefix sum over the chunk sums)
+// and scans that chunk for the token.  Integer sums: exact in any order.
+__global__ __launch_bounds__(kChunkThreads) void decide_draw_kernel(DrawArgs a) {
+  __shared__ SeqState st;
+  __shared__ int amax[kMaxGamma + 1];
+  __shared__ int bad_rows;
+  __shared__ unsigned long long sr[4], sp[4], wtot[4];
+  __shared__ int last, chunk_sel, use_res, done;
   __shared__ unsigned long long t_in_chunk;
-  const DrawArgs& a = f.d;
-  const int b = blockIdx.x, V = a.V, NC = n_chunks(V), cs = chunk_size(V);
+  const int c = blockIdx.x, b = blockIdx.y, V = a.V, NC = gridDim.x, cs = chunk_size(V);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   Scratch sc = carve(a.scratch, a.B, a.rows, V);
-  const SeqState& st = sc.seq[b];
-  if (st.A < 0) return;
-  const DrawPart* parts = sc.draw + (size_t)b * NC;
-  if (threadIdx.x < kWave) {  // wave 0: lane k holds chunk k; integer sums, exact in any order
-    const int lane = threadIdx.x;
+  const bool accept = a.mode == W_ACCEPT;
+  const int g = accept ? a.gamma : 0;
+  const float T = a.T;
+  if (threadIdx.x == 0) bad_rows = 0;
+  __syncthreads();
+  // row statistics (wave w: rows w, w + 4, ...)
+  for (int r = w; r <= g; r += kChunkThreads / kWave) {
+    const StatPart p = wave_merge_stats(sc.stats + ((size_t)b * a.rows + r) * NC, NC);
+    if (lane == 0) {
+      amax[r] = p.amax_i;
+      st.ms[r] = make_float2(p.m, p.s);
+      const bool softmax = accept ? (a.logits && T > 0.f) : T > 0.f;
+      if (p.bad || (softmax && (!isfinite(p.m) || !isfinite(p.s)))) atomicOr(&bad_rows, 1);
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    int bad = bad_rows, A = g;
+    if (accept && !bad) {
+      // lane i < g: event of draft position i (1 = rejection, 2 = error)
+      const int32_t* d = a.d + (size_t)b * a.ld_d;
+      int ev = 0;
+      if (lane < g) {
+        const int di = d[lane];
+        if (T == 0.f) {
+          ev = amax[lane] != di ? 1 : 0;
+        } else if (di < 0 || di >= V) {
+          ev = 2;
+        } else {
+          const float pd = prob_of(a.p + ((size_t)b * (g + 1) + lane) * V, di, a.logits, T, st.ms[lane]);
+          const float qd = a.q[((size_t)b * g + lane) * V + di];
+          const uint32_t wd = a.rand ? a.rand[(size_t)b * (g + 1) + lane]
+                                     : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, lane);
+          ev = !isfinite(qd) ? 2 : (!(__fmul_rn(word_to_uniform(wd), qd) < pd) ? 1 : 0);
+        }
+      }
+      const unsigned long long hit = __ballot(ev != 0);
+      if (hit) {
+        const int first = __ffsll(hit) - 1;
+        if (__shfl(ev, first, kWave) == 2) bad = 1;
+        else A = first;
+      }
+    }
+    if (lane == 0) {
+      const bool greedy = T == 0.f;
+      if (c == 0) {  // (one block writes the decision)
+        if (bad) set_status(a.status, kStatusNonFinite);
+        if (accept) {
+          a.n_accepted[b] = bad ? -1 : A;
+          if (bad) a.out[b] = -1;
+          else if (greedy) a.out[b] = amax[A];
+        } else if (bad || greedy) {
+          a.out[(size_t)b * a.ld_out] = bad ? 0 : amax[0];
+        }
+      }
+      st.A = bad ? -1 : (greedy ? -2 : (accept ? A : 0));
+    }
+  }
+  __syncthreads();
+  if (st.A < 0) return;  // (block-uniform: an error, or a greedy decision already written)
+
+  // this chunk's integer weight sums
+  {
+    const int j0 = c * cs, j1 = min(V, j0 + cs);
+    unsigned long long r_sum = 0, p_sum = 0;
+    float* qo = !accept && a.q_out ? a.q_out + ((size_t)b * a.gamma + a.slot) * V : nullptr;
+    for (int j = j0 + threadIdx.x; j < j1; j += kChunkThreads) {
+      float res, prob;
+      weights_at(a, st, b, j, res, prob);
+      if (qo) qo[j] = prob;
+      r_sum += fp_weight(res);
+      p_sum += fp_weight(prob);
+    }
+    r_sum = wave_sum_u64(r_sum);
+    p_sum = wave_sum_u64(p_sum);
+    if (lane == 0) { sr[w] = r_sum; sp[w] = p_sum; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long dr = 0ull, dp = 0ull;
+      for (int k = 0; k < kChunkThreads / kWave; ++k) { dr += sr[k]; dp += sp[k]; }
+      DrawPart* dst = sc.draw + (size_t)b * NC + c;
+      __hip_atomic_store(&dst->res, dr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&dst->prob, dp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // (the stores have completed before the count: the last block reads them with agent-scope loads)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      const uint32_t old = __hip_atomic_fetch_add(sc.count + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last = old == (uint32_t)(NC - 1);
+      if (last) __hip_atomic_store(sc.count + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!last) return;
+  }
+
+  // the last block: the chunk holding t, then the token inside it
+  if (w == 0) {  // lane k holds chunk k
     DrawPart pk{0ull, 0ull};
-    if (lane < NC) pk = parts[lane];
+    if (lane < NC) {
+      const DrawPart* src = sc.draw + (size_t)b * NC + lane;
+      pk.res = __hip_atomic_load(&src->res, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      pk.prob = __hip_atomic_load(&src->prob, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const unsigned long long tr = wave_sum_u64(pk.res), tp = wave_sum_u64(pk.prob);
-    const bool res = a.mode == W_ACCEPT && st.A < a.gamma && tr != 0;
+    const bool res = accept && st.A < g && tr != 0;
     const unsigned long long S = res ? tr : tp;
     uint32_t x;
-    if (a.mode == W_ACCEPT)
-      x = f.rand ? f.rand[(size_t)b * (a.gamma + 1) + a.gamma] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_RESAMPLE, 0);
+    if (accept)
+      x = a.rand ? a.rand[(size_t)b * (g + 1) + g] : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_RESAMPLE, 0);
     else
-      x = f.rand ? f.rand[b] : draw_word(f.seed, b, f.step, SPECDEC_PURPOSE_DRAFT, a.slot);
+      x = a.rand ? a.rand[b] : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_DRAFT, a.slot);
     if (S == 0) {
       if (lane == 0) {
-        f.out[(size_t)b * f.ld_out] = -1;
+        a.out[(size_t)b * a.ld_out] = -1;
         done = 1;
       }
     } else {
@@ -477,15 +492,15 @@ __global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) 
       }
       // the chunk whose share [incl - wk, incl) of the running sum holds t
       const unsigned long long hit = __ballot(t < incl && t >= incl - wk);
-      const int c = __ffsll(hit) - 1;
-      if (lane == c) {
-        chunk_sel = c;
+      const int csel = __ffsll(hit) - 1;
+      if (lane == csel) {
+        chunk_sel = csel;
         use_res = res;
         t_in_chunk = t - (incl - wk);
         done = 0;
       }
       if (hit == 0 && lane == 0) {  // (t < S: unreachable)
-        f.out[(size_t)b * f.ld_out] = -1;
+        a.out[(size_t)b * a.ld_out] = -1;
         done = 1;
       }
     }
@@ -494,7 +509,6 @@ __global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) 
   if (done) return;
   // scan the selected chunk: thread k owns 4 consecutive columns
   const int j0 = chunk_sel * cs, j1 = min(V, j0 + cs);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   unsigned long long mine[4], tot = 0;
   for (int base = j0; base < j1; base += 4 * kChunkThreads) {
     const int jj = base + 4 * threadIdx.x;
@@ -525,39 +539,12 @@ __global__ __launch_bounds__(kChunkThreads) void draw_final_kernel(FinalArgs f) 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         cum += mine[e];
-        if (cum > t) { f.out[(size_t)b * f.ld_out] = jj + e; break; }
+        if (cum > t) { a.out[(size_t)b * a.ld_out] = jj + e; break; }
       }
     }
     if (t < round_tot) break;  // uniform: every thread sees the same totals
     tot += round_tot;
   }
-}
-
-// draft greedy: grid B, block 64: merge the chunk argmax of the proposing row.
-__global__ __launch_bounds__(64) void draft_greedy_kernel(DraftFinishArgs a) {
-  const int b = blockIdx.x, NC = n_chunks(a.V);
-  Scratch sc = carve(a.scratch, a.B, 1, a.V);
-  const StatPart p = wave_merge_stats(sc.stats + (size_t)b * NC, NC);
-  if (threadIdx.x != 0) return;
-  if (p.bad) set_status(a.status, kStatusNonFinite);
-  a.d_out[(size_t)b * a.ld_d + a.slot] = p.bad ? 0 : p.amax_i;
-}
-
-// draft sampling: merge statistics into the sequence state (grid B, block 64).
-__global__ __launch_bounds__(64) void draft_merge_kernel(DraftFinishArgs a) {
-  const int b = blockIdx.x, NC = n_chunks(a.V);
-  Scratch sc = carve(a.scratch, a.B, 1, a.V);
-  const StatPart p = wave_merge_stats(sc.stats + (size_t)b * NC, NC);
-  if (threadIdx.x != 0) return;
-  const bool bad = p.bad || !isfinite(p.m) || !isfinite(p.s);
-  if (bad) {
-    set_status(a.status, kStatusNonFinite);
-    sc.seq[b].A = -1;
-    a.d_out[(size_t)b * a.ld_d + a.slot] = 0;
-  } else {
-    sc.seq[b].A = 0;
-  }
-  sc.seq[b].ms[0] = make_float2(p.m, p.s);
 }
 
 __global__ void copy_logits_kernel(const float* lg, int rps, int V, float* out) {
@@ -621,10 +608,11 @@ hipError_t launch_rows_embed(int dtype, const RowsArgs& a, hipStream_t s) {
 
 size_t sampling_scratch_bytes(int B, int rows, int V) {
   const int NC = n_chunks(V);
-  return align256(sizeof(StatPart) * (size_t)B * rows * NC) + align256(sizeof(SeqState) * (size_t)B) +
-         align256(sizeof(DrawPart) * (size_t)B * NC);
+  return align256(sizeof(StatPart) * (size_t)B * rows * NC) + align256(sizeof(DrawPart) * (size_t)B * NC) +
+         align256(sizeof(uint32_t) * (size_t)B);
 }
 
+// Two launches: the chunk statistics, then decide-and-draw.
 hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
   const int NC = n_chunks(a.V);
   if (a.logits_out) {
@@ -633,12 +621,7 @@ hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
   }
   Scratch sc = carve(a.scratch, a.B, 1, a.V);
   hipLaunchKernelGGL(stats_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, a.logits, a.V, 1, a.rps, a.rps - 1,
-                     a.temperature, nullptr, 0, sc.stats);
-  if (a.temperature == 0.f) {
-    hipLaunchKernelGGL(draft_greedy_kernel, dim3(a.B), dim3(64), 0, s, a);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(draft_merge_kernel, dim3(a.B), dim3(64), 0, s, a);
+                     a.temperature, nullptr, 0, sc.stats, sc.count);
   DrawArgs d{};
   d.mode = W_DRAFT;
   d.B = a.B;
@@ -651,15 +634,13 @@ hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
   d.q_out = a.q_out;
   d.scratch = a.scratch;
   d.rows = 1;
-  hipLaunchKernelGGL(draw_partials_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
-  FinalArgs f{};
-  f.d = d;
-  f.rand = a.rand;
-  f.seed = a.seed;
-  f.step = a.step;
-  f.out = a.d_out + a.slot;
-  f.ld_out = a.ld_d;
-  hipLaunchKernelGGL(draw_final_kernel, dim3(a.B), dim3(kChunkThreads), 0, s, f);
+  d.rand = a.rand;
+  d.seed = a.seed;
+  d.step = a.step;
+  d.out = a.d_out + a.slot;
+  d.ld_out = a.ld_d;
+  d.status = a.status;
+  hipLaunchKernelGGL(decide_draw_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
   return hipGetLastError();
 }
 
@@ -691,6 +672,7 @@ hipError_t static_accept_scratch(void** out) {
   return hipSuccess;
 }
 
+// Two launches: the chunk statistics of every row, then decide-and-draw.
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   if (a.gamma > kMaxGamma) return hipErrorInvalidValue;
   const int NC = n_chunks(a.V);
@@ -698,9 +680,7 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   const bool logits = a.input_kind == SPECDEC_INPUT_LOGITS;
   hipLaunchKernelGGL(stats_kernel, dim3(NC, a.B * (a.gamma + 1)), dim3(kChunkThreads), 0, s, a.p, a.V, a.gamma + 1,
                      a.gamma + 1, 0, logits ? a.temperature : 0.f, a.temperature > 0.f ? a.q : nullptr, a.gamma,
-                     sc.stats);
-  hipLaunchKernelGGL(accept_decide_kernel, dim3(a.B), dim3(64 * kMfmaWavesSamp), 0, s, a);
-  if (a.temperature == 0.f) return hipGetLastError();
+                     sc.stats, sc.count);
   DrawArgs d{};
   d.mode = W_ACCEPT;
   d.B = a.B;
@@ -710,17 +690,18 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   d.p = a.p;
   d.q = a.q;
   d.logits = logits;
+  d.d = a.d;
+  d.ld_d = a.ld_d;
   d.scratch = a.scratch;
   d.rows = a.gamma + 1;
-  hipLaunchKernelGGL(draw_partials_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
-  FinalArgs f{};
-  f.d = d;
-  f.rand = a.rand;
-  f.seed = a.seed;
-  f.step = a.step;
-  f.out = a.next_token;
-  f.ld_out = 1;
-  hipLaunchKernelGGL(draw_final_kernel, dim3(a.B), dim3(kChunkThreads), 0, s, f);
+  d.rand = a.rand;
+  d.seed = a.seed;
+  d.step = a.step;
+  d.n_accepted = a.n_accepted;
+  d.out = a.next_token;
+  d.ld_out = 1;
+  d.status = a.status;
+  hipLaunchKernelGGL(decide_draw_kernel, dim3(NC, a.B), dim3(kChunkThreads), 0, s, d);
   return hipGetLastError();
 }
 
