@@ -30,6 +30,12 @@
  *    specdec_kv_read_state or specdec_device_status.
  *  - Handles are not thread-safe; calls on one KV cache must be
  *    stream-ordered.
+ *  - Graph capture: every launch of an iteration reads lengths, pending
+ *    tokens and (with step_dev) the Philox step from the device, so one
+ *    captured iteration can be replayed R times with no host work between
+ *    replays.  Its grids are sized from the host bound kv->len_upper at
+ *    capture: set that field of each cache to the bound the R-th replay will
+ *    reach (current bound + R * (gamma+1)) before capturing, within capacity.
  *  - Storage types: SPECDEC_F32 (weights and KV float32) or SPECDEC_BF16
  *    (weights and KV bfloat16).  Activations, logits and probabilities are
  *    always float32.
@@ -110,15 +116,19 @@ typedef struct {
 typedef struct specdec_model specdec_model; /* opaque host handle */
 
 /* Per-model-instance KV cache and sequence state.  A POD the caller allocates
- * (host memory); specdec_kv_init fills it.  Fields are read-only for the caller. */
+ * (host memory); specdec_kv_init fills it.  Fields are read-only for the caller
+ * except len_upper (see graph capture above). */
 typedef struct {
   void* data;          /* device: K and V of every layer (layout private to the library) */
-  int32_t* state;      /* device: int32 [4*batch + 4]: len[B], pending[2B], n_pending[B], status */
+  int32_t* state;      /* device: int32 [4*batch + 4], 8-byte aligned: len[B], pending[2B],
+                          n_pending[B], status, one unused word, then the commit counter
+                          (uint64 over the last two words, see specdec_kv_step_word) */
   int32_t batch;       /* sequences */
   int32_t capacity;    /* positions per sequence (multiple of 64) */
   int32_t n_layers;    /* layers this cache serves */
   int32_t n_kv_heads, head_dim, dtype;
-  int64_t len_upper;   /* host-side upper bound of max_b len[b] (kept by the library) */
+  int64_t len_upper;   /* host-side upper bound of max_b len[b] (kept by the library; a
+                          caller may raise it before a graph capture) */
 } specdec_kv;
 
 /* ---------------------------------------------------------------- set-up */
@@ -200,7 +210,10 @@ SPECDEC_API size_t specdec_kv_bytes(const specdec_model_desc* desc, int32_t n_la
 SPECDEC_API int32_t specdec_kv_state_count(int32_t batch);
 
 /* Fill `kv` (host POD) over caller-owned device buffers and zero the state
- * (all lengths 0, no pending tokens, status OK).  Asynchronous on stream. */
+ * (all lengths 0, no pending tokens, status OK, commit counter 0).
+ * Asynchronous on stream.  Errors: INVALID_ARG (nulls, a state array that is
+ * not 8-byte aligned, data_bytes below specdec_kv_bytes), SHAPE (capacity not
+ * a multiple of 64). */
 SPECDEC_API specdec_status specdec_kv_init(specdec_kv* kv, const specdec_model* model, int32_t batch, int32_t capacity,
                                void* data, size_t data_bytes, int32_t* state, void* stream);
 
@@ -216,7 +229,8 @@ SPECDEC_API specdec_status specdec_kv_read_context(const specdec_kv* kv, int32_t
 
 /* Set lengths and pending tokens from HOST arrays: len[B], pending[2B]
  * (right-aligned: pending[2b+1] is the newest token), n_pending[B] in {1,2}.
- * Clears the status word.  Synchronizes the stream. */
+ * Clears the status word and leaves the commit counter as it is.
+ * Synchronizes the stream. */
 SPECDEC_API specdec_status specdec_kv_set_state(specdec_kv* kv, const int32_t* len, const int32_t* pending,
                                     const int32_t* n_pending, void* stream);
 /* Read lengths, pending tokens and the status word into HOST arrays (any may
@@ -236,6 +250,10 @@ SPECDEC_API specdec_status specdec_prefill(const specdec_model* model, specdec_k
 /* ---------------------------------------------------------------- hot path */
 
 /* Draft single-token decode step at draft slot `slot` (0 <= slot < gamma):
+ * the draft model proposing one candidate token per sequence, the first half
+ * of a draft-and-verify iteration (Sec. 2.1; Alg. 3, "run draft d_i", run
+ * gamma times per iteration).
+ *
  *  slot 0 processes the cache's 1 or 2 pending tokens (2 after an iteration
  *  that accepted every draft), slot s > 0 processes d_out[b*ld_d + s-1].
  *  It appends their K/V speculatively (len is unchanged until commit), runs
@@ -246,14 +264,20 @@ SPECDEC_API specdec_status specdec_prefill(const specdec_model* model, specdec_k
  *      the fixed-point inverse-CDF sampler (see specdec_sample) using the
  *      32-bit word rand[b] if rand != NULL, else Philox(seed, b, step,
  *      SPECDEC_PURPOSE_DRAFT, slot).
+ *  step_dev (optional): a device uint64 read by the kernel in place of `step`
+ *      (e.g. specdec_kv_step_word of the target cache), so that a captured
+ *      HIP graph of an iteration draws fresh words on every replay.
  *  logits_out (optional, [batch, V]) receives the proposing row's logits.
  * Errors: INVALID_ARG, SHAPE (batch/gamma beyond the handle's max_rows),
  * KV_CAPACITY (len_upper + 2 + gamma > capacity). */
 SPECDEC_API specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, int32_t gamma, int32_t slot,
-                                  float temperature, uint64_t seed, uint64_t step, const uint32_t* rand,
-                                  float* q_out, int32_t* d_out, int32_t ld_d, float* logits_out, void* stream);
+                                  float temperature, uint64_t seed, uint64_t step, const uint64_t* step_dev,
+                                  const uint32_t* rand, float* q_out, int32_t* d_out, int32_t ld_d,
+                                  float* logits_out, void* stream);
 
-/* Target verify pass: one forward over the gamma+1 tokens
+/* Target verify pass (Sec. 2.1: the target model checks the drafted
+ * candidates; Alg. 3, "verify with target model"): one forward over the
+ * gamma+1 tokens
  * [pending token, d[b*ld_d + 0 .. gamma-1]] at positions len[b] .. len[b]+gamma,
  * causal inside the block, against the resident cache (the drafted tokens'
  * K/V are appended speculatively).  logits_out: [batch, gamma+1, V] float32,
@@ -261,13 +285,15 @@ SPECDEC_API specdec_status specdec_draft_step(const specdec_model* draft, specde
 SPECDEC_API specdec_status specdec_verify(const specdec_model* target, specdec_kv* kv, int32_t gamma, const int32_t* d,
                               int32_t ld_d, float* logits_out, void* stream);
 
-/* Accept / resample for every sequence b (one draft-and-verify decision):
+/* Accept / resample for every sequence b (one draft-and-verify decision; it
+ * yields the accepted count A of Sec. 2.1, Eq. 1):
  *  p:  [batch, gamma+1, V] float32 -- target probabilities (input_kind PROBS)
  *      or logits (input_kind LOGITS: p = softmax(logits / temperature));
  *  q:  [batch, gamma, V] float32 draft probabilities (unused when greedy);
  *  d:  drafted tokens d[b*ld_d + i];
  *  rand: [batch, gamma+1] 32-bit words ([0, gamma) accept tests, [gamma] the
- *      resample / bonus draw) or NULL => Philox(seed, b, step, purpose, index).
+ *      resample / bonus draw) or NULL => Philox(seed, b, step, purpose, index);
+ *  step_dev: as for specdec_draft_step (NULL => `step`).
  * Sampling (temperature > 0): accept d_i iff fl32(u_i * q_i(d_i)) < p_i(d_i)
  * with u_i = (word >> 8) * 2^-24; at the first rejection emit a draw from
  * max(0, fl32(p_i - q_i)) (from p_i if that is all zero); if all accepted emit
@@ -285,8 +311,9 @@ SPECDEC_API specdec_status specdec_verify(const specdec_model* target, specdec_k
  * (gamma > 31). */
 SPECDEC_API specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
                               const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
-                              uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
-                              int32_t* status, void* workspace, size_t workspace_bytes, void* stream);
+                              uint64_t seed, uint64_t step, const uint64_t* step_dev, int32_t* n_accepted,
+                              int32_t* next_token, int32_t* status, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /* Bytes of the accept workspace for `batch` sequences of gamma+1 rows over a
  * vocabulary of `vocab` (0 for arguments specdec_accept rejects). */
@@ -310,17 +337,30 @@ SPECDEC_API size_t specdec_accept_workspace_bytes(int32_t batch, int32_t gamma, 
 SPECDEC_API specdec_status specdec_accept_noalloc(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind,
                                                   float temperature, const float* p, const float* q, const int32_t* d,
                                                   int32_t ld_d, const uint32_t* rand, uint64_t seed, uint64_t step,
-                                                  int32_t* n_accepted, int32_t* next_token, int32_t* status,
-                                                  void* stream);
+                                                  const uint64_t* step_dev, int32_t* n_accepted, int32_t* next_token,
+                                                  int32_t* status, void* stream);
 
 /* KV commit / rollback after specdec_accept (device-side, graph friendly):
+ * the A accepted drafts and the emitted token become committed text, the
+ * rejected drafts are dropped (Sec. 2.1: A tokens accepted per iteration; the
+ * end of one pass of Alg. 3's inner loop).
  *  TARGET: len += A+1; pending = [next]                       (n_pending = 1)
  *  DRAFT:  len += n_pending + min(A, gamma-1);
  *          pending = [d_gamma, next] if A == gamma else [next]
  * Entries at or beyond the new length are speculative and get overwritten.
- * A < 0 (an accept error) leaves the cache untouched. */
+ * A < 0 (an accept error) leaves that sequence untouched.  Every call adds 1
+ * to the cache's commit counter (specdec_kv_step_word).  The host bound
+ * kv->len_upper grows by gamma+1. */
 SPECDEC_API specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, const int32_t* n_accepted,
                                  const int32_t* d, int32_t ld_d, const int32_t* next_token, void* stream);
+
+/* Device address of the cache's commit counter: a uint64 in the state array,
+ * 0 after specdec_kv_init, +1 per specdec_kv_commit, kept by
+ * specdec_kv_set_state.  Passed as step_dev to the draft steps and the accept
+ * of an iteration (all before its commits), it numbers the iteration's Philox
+ * draws from the device, which is what a graph replayed without host work
+ * needs.  NULL if kv or its state is NULL. */
+SPECDEC_API const uint64_t* specdec_kv_step_word(const specdec_kv* kv);
 
 /* ---------------------------------------------------------------- draft reload
  * Only K drafts stay resident; the others live in backing storage and are

@@ -95,20 +95,21 @@ _SIGS = {
                                        ctypes.c_void_p]),
     "specdec_draft_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(KV), ctypes.c_int32, ctypes.c_int32,
                                           ctypes.c_float, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
-                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
-                                          ctypes.c_void_p]),
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_verify": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(KV), ctypes.c_int32, ctypes.c_void_p,
                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
     "specdec_accept": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                       ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p,
-                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                      ctypes.c_void_p]),
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_size_t, ctypes.c_void_p]),
     "specdec_accept_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "specdec_accept_noalloc": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
-                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p]),
     "specdec_packed_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]),
     "specdec_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
@@ -119,6 +120,7 @@ _SIGS = {
     "specdec_event_query": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32)]),
     "specdec_kv_commit": (ctypes.c_int, [ctypes.POINTER(KV), ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
+    "specdec_kv_step_word": (ctypes.c_void_p, [ctypes.POINTER(KV)]),
     "specdec_sample": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32,
                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]),
@@ -361,6 +363,15 @@ class KVCache:
                                            S.ctypes.data, _stream(stream)), "specdec_kv_read_state")
         return {"len": L, "pending": P.reshape(B, 2), "n_pending": N, "status": int(S[0])}
 
+    def step_word(self) -> int:
+        """Device address of the commit counter (the step_dev argument)."""
+        return int(lib().specdec_kv_step_word(ctypes.byref(self.kv)))
+
+    def read_step(self) -> int:
+        """The commit counter's value (synchronizes the current stream)."""
+        B = self.batch
+        return int(self.state[4 * B + 2:4 * B + 4].cpu().numpy().view(np.uint64)[0])
+
 
 # ---------------------------------------------------------------- draft reload
 def packed_range(shape, first_layer: int, n_layers: int):
@@ -444,7 +455,9 @@ def specdec_prefill(model: Model, kv: KVCache, tokens, stream=None):
 
 
 def specdec_draft_step(draft: Model, kv: KVCache, gamma: int, slot: int, temperature: float, seed: int, step: int,
-                       rand, q_out, d_out, ld_d: int, logits_out=None, stream=None):
+                       rand, q_out, d_out, ld_d: int, logits_out=None, stream=None, step_dev=None):
+    """step_dev: a cache's KVCache.step_word() (device address of its commit
+    counter) read in place of `step`, or None."""
     import torch
     B, V = kv.batch, draft.shape.vocab
     if rand is not None:
@@ -455,7 +468,7 @@ def specdec_draft_step(draft: Model, kv: KVCache, gamma: int, slot: int, tempera
     _dev(d_out, "d_out", torch.int32, (B - 1) * ld_d + gamma)
     _dev(logits_out, "logits_out", torch.float32, B * V, optional=True)
     _check(lib().specdec_draft_step(draft.handle, ctypes.byref(kv.kv), gamma, slot, temperature, seed, step,
-                                    _ptr(rand), _ptr(q_out), d_out.data_ptr(), ld_d, _ptr(logits_out),
+                                    step_dev, _ptr(rand), _ptr(q_out), d_out.data_ptr(), ld_d, _ptr(logits_out),
                                     _stream(stream)), "specdec_draft_step")
 
 
@@ -482,9 +495,11 @@ def accept_workspace(batch: int, gamma: int, vocab: int, device="cuda"):
 
 
 def specdec_accept(batch: int, gamma: int, vocab: int, input_kind: int, temperature: float, p, q, d, ld_d: int,
-                   rand, seed: int, step: int, n_accepted, next_token, status=None, workspace=None, stream=None):
+                   rand, seed: int, step: int, n_accepted, next_token, status=None, workspace=None, stream=None,
+                   step_dev=None):
     """Accept / resample.  `workspace` (uint8 device tensor) is allocated per
-    call when not given; pass one from accept_workspace() in loops."""
+    call when not given; pass one from accept_workspace() in loops.  step_dev:
+    as for specdec_draft_step."""
     import torch
     _dev(p, "p", torch.float32, batch * (gamma + 1) * vocab)
     _dev(q, "q", torch.float32, batch * gamma * vocab, optional=temperature == 0 or gamma == 0)
@@ -500,12 +515,14 @@ def specdec_accept(batch: int, gamma: int, vocab: int, input_kind: int, temperat
         workspace = accept_workspace(batch, gamma, vocab, p.device)
     _dev(workspace, "workspace", torch.uint8, 1)
     _check(lib().specdec_accept(batch, gamma, vocab, input_kind, temperature, p.data_ptr(), _ptr(q), _ptr(d), ld_d,
-                                _ptr(rand), seed, step, n_accepted.data_ptr(), next_token.data_ptr(), _ptr(status),
-                                workspace.data_ptr(), workspace.numel(), _stream(stream)), "specdec_accept")
+                                _ptr(rand), seed, step, step_dev, n_accepted.data_ptr(), next_token.data_ptr(),
+                                _ptr(status), workspace.data_ptr(), workspace.numel(), _stream(stream)),
+           "specdec_accept")
 
 
 def specdec_accept_noalloc(batch: int, gamma: int, vocab: int, input_kind: int, temperature: float, p, q, d,
-                           ld_d: int, rand, seed: int, step: int, n_accepted, next_token, status=None, stream=None):
+                           ld_d: int, rand, seed: int, step: int, n_accepted, next_token, status=None, stream=None,
+                           step_dev=None):
     """specdec_accept with the library's static scratch (no workspace, no allocation)."""
     import torch
     _dev(p, "p", torch.float32, batch * (gamma + 1) * vocab)
@@ -519,8 +536,9 @@ def specdec_accept_noalloc(batch: int, gamma: int, vocab: int, input_kind: int, 
     _dev(next_token, "next_token", torch.int32, batch)
     _dev(status, "status", torch.int32, 1, optional=True)
     _check(lib().specdec_accept_noalloc(batch, gamma, vocab, input_kind, temperature, p.data_ptr(), _ptr(q), _ptr(d),
-                                        ld_d, _ptr(rand), seed, step, n_accepted.data_ptr(), next_token.data_ptr(),
-                                        _ptr(status), _stream(stream)), "specdec_accept_noalloc")
+                                        ld_d, _ptr(rand), seed, step, step_dev, n_accepted.data_ptr(),
+                                        next_token.data_ptr(), _ptr(status), _stream(stream)),
+           "specdec_accept_noalloc")
 
 
 def specdec_kv_commit(kv: KVCache, gamma: int, role: int, n_accepted, d, ld_d: int, next_token, stream=None):
@@ -602,14 +620,17 @@ class SpecDecoder:
     The call order is the inner loop of the paper's runtime (Sec. 3.4, Alg. 3):
     gamma draft steps, one verify pass, accept / resample, commit of both
     caches.  Host code only sequences the calls; tokens and counts stay on
-    the device.
+    the device.  With device_step the Philox step of every draw is the target
+    cache's commit counter, read on the device (the `step` arguments below are
+    then ignored), so a captured iteration draws fresh words on each replay.
     """
 
     def __init__(self, target: Model, draft: Model, kv_t: KVCache, kv_d: KVCache, gamma: int,
-                 temperature: float, seed: int):
+                 temperature: float, seed: int, device_step: bool = False):
         import torch
         self.target, self.draft, self.kv_t, self.kv_d = target, draft, kv_t, kv_d
         self.gamma, self.temperature, self.seed = gamma, temperature, seed
+        self.step_dev = kv_t.step_word() if device_step else None
         B, V = kv_t.batch, target.shape.vocab
         dev = kv_t.data.device
         self.B, self.V = B, V
@@ -624,12 +645,13 @@ class SpecDecoder:
     def draft_phase(self, step: int, stream=None):
         for s in range(self.gamma):
             specdec_draft_step(self.draft, self.kv_d, self.gamma, s, self.temperature, self.seed, step, None, self.q,
-                               self.d, self.gamma, None, stream)
+                               self.d, self.gamma, None, stream, step_dev=self.step_dev)
 
     def verify_phase(self, step: int, stream=None):
         specdec_verify(self.target, self.kv_t, self.gamma, self.d, self.gamma, self.logits, stream)
         specdec_accept(self.B, self.gamma, self.V, INPUT_LOGITS, self.temperature, self.logits, self.q, self.d,
-                       self.gamma, None, self.seed, step, self.n_acc, self.next, self.status, self.accept_ws, stream)
+                       self.gamma, None, self.seed, step, self.n_acc, self.next, self.status, self.accept_ws, stream,
+                       step_dev=self.step_dev)
 
     def commit_phase(self, stream=None):
         specdec_kv_commit(self.kv_t, self.gamma, ROLE_TARGET, self.n_acc, self.d, self.gamma, self.next, stream)

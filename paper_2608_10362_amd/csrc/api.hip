@@ -225,6 +225,8 @@ int32_t* kv_len(const specdec_kv* kv) { return kv->state; }
 int32_t* kv_pending(const specdec_kv* kv) { return kv->state + kv->batch; }
 int32_t* kv_npending(const specdec_kv* kv) { return kv->state + 3 * kv->batch; }
 int32_t* kv_status(const specdec_kv* kv) { return kv->state + 4 * kv->batch; }
+uint64_t* kv_counter(const specdec_kv* kv) { return reinterpret_cast<uint64_t*>(kv->state + 4 * kv->batch + 2); }
+bool misaligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) != 0; }
 
 KvLayout kv_layout(const specdec_kv* kv) {
   return KvLayout{kv->data, kv->batch, kv->capacity, kv->n_kv_heads, kv->head_dim, kv->dtype};
@@ -628,7 +630,8 @@ int32_t specdec_kv_state_count(int32_t batch) { return batch > 0 ? 4 * batch + 4
 
 specdec_status specdec_kv_init(specdec_kv* kv, const specdec_model* model, int32_t batch, int32_t capacity,
                                void* data, size_t data_bytes, int32_t* state, void* stream) {
-  if (!kv || !model || !data || !state || batch <= 0 || capacity <= 0) return SPECDEC_ERR_INVALID_ARG;
+  if (!kv || !model || !data || !state || batch <= 0 || capacity <= 0 || misaligned8(state))
+    return SPECDEC_ERR_INVALID_ARG;
   if (capacity % 64) return SPECDEC_ERR_SHAPE;
   if (data_bytes < specdec_kv_bytes(&model->desc, model->n_layers, batch, capacity)) return SPECDEC_ERR_INVALID_ARG;
   kv->data = data;
@@ -676,7 +679,8 @@ specdec_status specdec_kv_set_state(specdec_kv* kv, const int32_t* len, const in
     mx = std::max<int64_t>(mx, len[b]);
   }
   hipStream_t s = (hipStream_t)stream;
-  SD_TRY(hipMemcpyAsync(kv->state, host.data(), host.size() * 4, hipMemcpyHostToDevice, s));
+  // lengths, pending tokens and the status word; the commit counter is kept
+  SD_TRY(hipMemcpyAsync(kv->state, host.data(), (4 * (size_t)B + 1) * 4, hipMemcpyHostToDevice, s));
   SD_TRY(hipStreamSynchronize(s));
   kv->len_upper = mx;
   return SPECDEC_OK;
@@ -735,11 +739,13 @@ specdec_status specdec_prefill(const specdec_model* model, specdec_kv* kv, int32
 }
 
 specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, int32_t gamma, int32_t slot,
-                                  float temperature, uint64_t seed, uint64_t step, const uint32_t* rand,
-                                  float* q_out, int32_t* d_out, int32_t ld_d, float* logits_out, void* stream) {
+                                  float temperature, uint64_t seed, uint64_t step, const uint64_t* step_dev,
+                                  const uint32_t* rand, float* q_out, int32_t* d_out, int32_t ld_d,
+                                  float* logits_out, void* stream) {
   specdec_status st = check_kv(draft, kv);
   if (st != SPECDEC_OK) return st;
-  if (!d_out || gamma < 1 || slot < 0 || slot >= gamma || ld_d < gamma || !(temperature >= 0.f))
+  if (!d_out || gamma < 1 || slot < 0 || slot >= gamma || ld_d < gamma || !(temperature >= 0.f) ||
+      misaligned8(step_dev))
     return SPECDEC_ERR_INVALID_ARG;
   if (temperature > 0.f && !q_out) return SPECDEC_ERR_INVALID_ARG;
   const int B = kv->batch;
@@ -768,6 +774,7 @@ specdec_status specdec_draft_step(const specdec_model* draft, specdec_kv* kv, in
   f.temperature = temperature;
   f.seed = seed;
   f.step = step;
+  f.step_dev = step_dev;
   f.rand = rand;
   f.slot = slot;
   f.gamma = gamma;
@@ -883,11 +890,13 @@ extern "C" {
 
 specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind, float temperature,
                               const float* p, const float* q, const int32_t* d, int32_t ld_d, const uint32_t* rand,
-                              uint64_t seed, uint64_t step, int32_t* n_accepted, int32_t* next_token,
-                              int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+                              uint64_t seed, uint64_t step, const uint64_t* step_dev, int32_t* n_accepted,
+                              int32_t* next_token, int32_t* status, void* workspace, size_t workspace_bytes,
+                              void* stream) {
   const specdec_status st = check_accept(batch, gamma, vocab, input_kind, temperature, p, q, d, ld_d, n_accepted,
                                          next_token);
   if (st != SPECDEC_OK) return st;
+  if (misaligned8(step_dev)) return SPECDEC_ERR_INVALID_ARG;
   if (!workspace || workspace_bytes < sampling_scratch_bytes(batch, gamma + 1, vocab)) return SPECDEC_ERR_INVALID_ARG;
   AcceptArgs a{};
   a.B = batch;
@@ -902,6 +911,7 @@ specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32
   a.rand = rand;
   a.seed = seed;
   a.step = step;
+  a.step_dev = step_dev;
   a.n_accepted = n_accepted;
   a.next_token = next_token;
   a.status = status;
@@ -913,10 +923,12 @@ specdec_status specdec_accept(int32_t batch, int32_t gamma, int32_t vocab, int32
 specdec_status specdec_accept_noalloc(int32_t batch, int32_t gamma, int32_t vocab, int32_t input_kind,
                                       float temperature, const float* p, const float* q, const int32_t* d,
                                       int32_t ld_d, const uint32_t* rand, uint64_t seed, uint64_t step,
-                                      int32_t* n_accepted, int32_t* next_token, int32_t* status, void* stream) {
+                                      const uint64_t* step_dev, int32_t* n_accepted, int32_t* next_token,
+                                      int32_t* status, void* stream) {
   const specdec_status st = check_accept(batch, gamma, vocab, input_kind, temperature, p, q, d, ld_d, n_accepted,
                                          next_token);
   if (st != SPECDEC_OK) return st;
+  if (misaligned8(step_dev)) return SPECDEC_ERR_INVALID_ARG;
   if (sampling_scratch_bytes(batch, gamma + 1, vocab) > kStaticAcceptScratchBytes) return SPECDEC_ERR_SCRATCH_LIMIT;
   void* scratch = nullptr;
   if (static_accept_scratch(&scratch) != hipSuccess) return SPECDEC_ERR_HIP;
@@ -933,12 +945,17 @@ specdec_status specdec_accept_noalloc(int32_t batch, int32_t gamma, int32_t voca
   a.rand = rand;
   a.seed = seed;
   a.step = step;
+  a.step_dev = step_dev;
   a.n_accepted = n_accepted;
   a.next_token = next_token;
   a.status = status;
   a.scratch = scratch;  // (the device address of the static array, never the array's host-side name)
   Timed t(SPECDEC_KERNEL_ACCEPT, (hipStream_t)stream);
   return hip_status(launch_accept(a, (hipStream_t)stream));
+}
+
+const uint64_t* specdec_kv_step_word(const specdec_kv* kv) {
+  return kv && kv->state ? kv_counter(kv) : nullptr;
 }
 
 specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, const int32_t* n_accepted,
@@ -957,6 +974,7 @@ specdec_status specdec_kv_commit(specdec_kv* kv, int32_t gamma, int32_t role, co
   c.d = d;
   c.ld_d = ld_d;
   c.next_token = next_token;
+  c.counter = kv_counter(kv);
   specdec_status st;
   {
     Timed t(SPECDEC_KERNEL_COMMIT, (hipStream_t)stream);

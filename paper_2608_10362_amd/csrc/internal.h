@@ -185,6 +185,7 @@ struct DraftFinishArgs {
   const float* logits;   // [M, V]
   float temperature;
   uint64_t seed, step;
+  const uint64_t* step_dev;  // or null: the step read on the device in place of `step`
   const uint32_t* rand;  // [B] or null
   int slot, gamma;
   float* q_out;          // [B, gamma, V] or null
@@ -209,6 +210,7 @@ struct AcceptArgs {
   int ld_d;
   const uint32_t* rand;
   uint64_t seed, step;
+  const uint64_t* step_dev;  // or null: the step read on the device in place of `step`
   int32_t* n_accepted;
   int32_t* next_token;
   int32_t* status;
@@ -233,6 +235,7 @@ struct CommitArgs {
   const int32_t* d;
   int ld_d;
   const int32_t* next_token;
+  uint64_t* counter;  // the cache's commit counter, +1 per launch
 };
 hipError_t launch_commit(const CommitArgs& a, hipStream_t s);
 

@@ -324,6 +324,7 @@ struct DrawArgs {
   // the words of the draws, the outputs
   const uint32_t* rand;   // accept: [B, gamma+1] (accept words, then the resample word); draft: [B]
   uint64_t seed, step;
+  const uint64_t* step_dev;  // or null: read in place of step
   int32_t* n_accepted;    // accept only
   int32_t* out;           // accept: next_token[B]; draft: d_out + slot (stride ld_out)
   int ld_out;
@@ -370,6 +371,7 @@ __global__ __launch_bounds__(kChunkThreads) void decide_draw_kernel(DrawArgs a) 
   const bool accept = a.mode == W_ACCEPT;
   const int g = accept ? a.gamma : 0;
   const float T = a.T;
+  const uint64_t step = a.step_dev ? *a.step_dev : a.step;
   if (threadIdx.x == 0) bad_rows = 0;
   __syncthreads();
   // row statistics (wave w: rows w, w + 4, ...)
@@ -399,7 +401,7 @@ __global__ __launch_bounds__(kChunkThreads) void decide_draw_kernel(DrawArgs a) 
           const float pd = prob_of(a.p + ((size_t)b * (g + 1) + lane) * V, di, a.logits, T, st.ms[lane]);
           const float qd = a.q[((size_t)b * g + lane) * V + di];
           const uint32_t wd = a.rand ? a.rand[(size_t)b * (g + 1) + lane]
-                                     : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_ACCEPT, lane);
+                                     : draw_word(a.seed, b, step, SPECDEC_PURPOSE_ACCEPT, lane);
           ev = !isfinite(qd) ? 2 : (!(__fmul_rn(word_to_uniform(wd), qd) < pd) ? 1 : 0);
         }
       }
@@ -473,9 +475,9 @@ __global__ __launch_bounds__(kChunkThreads) void decide_draw_kernel(DrawArgs a) 
     const unsigned long long S = res ? tr : tp;
     uint32_t x;
     if (accept)
-      x = a.rand ? a.rand[(size_t)b * (g + 1) + g] : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_RESAMPLE, 0);
+      x = a.rand ? a.rand[(size_t)b * (g + 1) + g] : draw_word(a.seed, b, step, SPECDEC_PURPOSE_RESAMPLE, 0);
     else
-      x = a.rand ? a.rand[b] : draw_word(a.seed, b, a.step, SPECDEC_PURPOSE_DRAFT, a.slot);
+      x = a.rand ? a.rand[b] : draw_word(a.seed, b, step, SPECDEC_PURPOSE_DRAFT, a.slot);
     if (S == 0) {
       if (lane == 0) {
         a.out[(size_t)b * a.ld_out] = -1;
@@ -594,6 +596,7 @@ __global__ void commit_kernel(CommitArgs a) {
       a.pending[2 * b + 1] = nxt;
     }
   }
+  if (threadIdx.x == 0) *a.counter += 1;
 }
 
 }  // namespace
@@ -637,6 +640,7 @@ hipError_t launch_draft_finish(const DraftFinishArgs& a, hipStream_t s) {
   d.rand = a.rand;
   d.seed = a.seed;
   d.step = a.step;
+  d.step_dev = a.step_dev;
   d.out = a.d_out + a.slot;
   d.ld_out = a.ld_d;
   d.status = a.status;
@@ -697,6 +701,7 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   d.rand = a.rand;
   d.seed = a.seed;
   d.step = a.step;
+  d.step_dev = a.step_dev;
   d.n_accepted = a.n_accepted;
   d.out = a.next_token;
   d.ld_out = 1;

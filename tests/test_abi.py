@@ -101,30 +101,44 @@ def test_call_argument_errors_before_any_launch(lib):
     kv = binding.KV()
     # null handles / buffers are rejected synchronously
     assert lib.specdec_verify(None, ctypes.byref(kv), 4, None, 4, None, None) == -1
-    assert lib.specdec_draft_step(None, ctypes.byref(kv), 4, 0, 1.0, 0, 0, None, None, None, 4, None, None) == -1
+    assert lib.specdec_draft_step(None, ctypes.byref(kv), 4, 0, 1.0, 0, 0, None, None, None, None, 4, None,
+                                  None) == -1
     fake = ctypes.c_void_p(256)
     ws = lib.specdec_accept_workspace_bytes(1, 4, 100)
     assert ws > 0 and lib.specdec_accept_workspace_bytes(1, 40, 100) == 0
-    assert lib.specdec_accept(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, fake, ws,
+    assert lib.specdec_accept(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, None, fake, ws,
                               None) == -1
-    assert lib.specdec_accept(1, 4, 100, 7, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, fake, ws,
+    assert lib.specdec_accept(1, 4, 100, 7, 1.0, fake, fake, fake, 4, None, 0, 0, None, fake, fake, None, fake, ws,
                               None) == -1
-    assert lib.specdec_accept(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, fake, fake, None, fake, ws,
+    assert lib.specdec_accept(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, None, fake, fake, None, fake, ws,
                               None) == -6
     # the workspace is required and must be large enough
-    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, None, ws,
+    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, None, fake, fake, None, None, ws,
                               None) == -1
-    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, fake, fake, None, fake, ws - 1,
+    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, None, fake, fake, None, fake, ws - 1,
                               None) == -1
     # the no-allocation accept: the same argument errors, and a request beyond its
     # static scratch is refused before any HIP call
-    assert lib.specdec_accept_noalloc(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None,
+    assert lib.specdec_accept_noalloc(0, 4, 100, 0, 1.0, None, None, None, 4, None, 0, 0, None, None, None, None,
                                       None) == -1
-    assert lib.specdec_accept_noalloc(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, fake, fake, None,
+    assert lib.specdec_accept_noalloc(1, 40, 100, 0, 1.0, fake, fake, fake, 40, None, 0, 0, None, fake, fake, None,
                                       None) == -6
     assert lib.specdec_accept_workspace_bytes(200, 8, 200000) > binding.ACCEPT_NOALLOC_SCRATCH_BYTES
-    assert lib.specdec_accept_noalloc(200, 8, 200000, 0, 1.0, fake, fake, fake, 8, None, 0, 0, fake, fake, None,
+    assert lib.specdec_accept_noalloc(200, 8, 200000, 0, 1.0, fake, fake, fake, 8, None, 0, 0, None, fake, fake, None,
                                       None) == -8
+    # a step word must be 8-byte aligned
+    odd = ctypes.c_void_p(260)
+    assert lib.specdec_accept(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, odd, fake, fake, None, fake, ws,
+                              None) == -1
+    assert lib.specdec_accept_noalloc(1, 4, 100, 0, 1.0, fake, fake, fake, 4, None, 0, 0, odd, fake, fake, None,
+                                      None) == -1
+    # the commit counter sits after the status word and one unused word
+    assert lib.specdec_kv_step_word(ctypes.byref(kv)) is None
+    kv.state = 4096
+    kv.batch = 3
+    assert lib.specdec_kv_step_word(ctypes.byref(kv)) == 4096 + 4 * (4 * 3 + 2)
+    assert lib.specdec_kv_step_word(None) is None
+    kv = binding.KV()
     assert lib.specdec_stream_read(None, 1024, fake, None) == -1
     assert lib.specdec_stream_read(ctypes.c_void_p(257), 1024, fake, None) == -1  # (16-byte alignment)
     assert lib.specdec_kv_commit(ctypes.byref(kv), 4, 0, None, None, 4, None, None) == -1

@@ -162,6 +162,80 @@ def test_tiny_verify_equals_sequential_steps(tiny):
     assert diff <= 1e-6
 
 
+def test_tiny_graph_of_whole_iterations_draws_fresh_words_each_replay(tiny):
+    """One captured HIP graph of a whole sampled iteration (gamma draft steps,
+    verify, accept, both commits), replayed R times with no library call in
+    between: the Philox step comes from the target cache's commit counter, so
+    replay i must equal the eager iteration run at explicit step c0 + i, token
+    for token and bit for bit, and differ from iterations that reuse one step."""
+    torch = torch_cuda()
+    shape, W, target, draft = tiny
+    B, g, R, T, cap = 2, 4, 5, 1.0, 256
+    prompts = synth.make_prompt(48, shape.vocab, batch=B, seed=31)
+    kv_t = binding.KVCache(target, B, cap)
+    kv_d = binding.KVCache(draft, B, cap)
+    binding.specdec_prefill(target, kv_t, i32(prompts))
+    binding.specdec_prefill(draft, kv_d, i32(prompts))
+    torch.cuda.synchronize()
+    c0 = kv_t.read_step()
+    assert c0 == 0
+    # the host bound every launch below is sized from: the one R iterations reach
+    bound_t, bound_d = kv_t.kv.len_upper + R * (g + 1), kv_d.kv.len_upper + R * (g + 1)
+    saved_t, saved_d = kv_t.state.clone(), kv_d.state.clone()
+
+    def restore():
+        kv_t.state.copy_(saved_t)
+        kv_d.state.copy_(saved_d)
+        kv_t.kv.len_upper, kv_d.kv.len_upper = bound_t, bound_d
+
+    def snap(sd):
+        return [x.clone() for x in (sd.d, sd.n_acc, sd.next, sd.q)]
+
+    def eager(steps):
+        sd = binding.SpecDecoder(target, draft, kv_t, kv_d, g, T, seed=3)
+        restore()
+        out = []
+        for st in steps:
+            kv_t.kv.len_upper, kv_d.kv.len_upper = bound_t, bound_d
+            sd.step(st)
+            out.append(snap(sd))
+        torch.cuda.synchronize()
+        return out, kv_t.read_state(), kv_t.read_step()
+
+    ref, ref_state, ref_count = eager([c0 + i for i in range(R)])
+    assert ref_count == c0 + R          # every commit counts, whatever step the draws used
+    stale, _, _ = eager([c0] * R)
+    sdg = binding.SpecDecoder(target, draft, kv_t, kv_d, g, T, seed=3, device_step=True)
+    assert sdg.step_dev == kv_t.step_word()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):       # warm-up launch off the capture
+        restore()
+        sdg.step(0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    restore()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sdg.step(0)
+    restore()
+    torch.cuda.synchronize()
+    got = []
+    for r in range(R):
+        graph.replay()
+        torch.cuda.synchronize()
+        got.append(snap(sdg))
+    n_acc = [[int(a) for a in x[1].cpu().numpy()] for x in got]
+    same = [all(torch.equal(a, b) for a, b in zip(x, y)) for x, y in zip(got, ref)]
+    fresh = [not all(torch.equal(a, b) for a, b in zip(x, y)) for x, y in zip(got, stale)]
+    log(f"graph replays: accepted {n_acc}; equal to eager at steps c0+i {same}; differ from step c0 {fresh}")
+    assert all(same)
+    assert any(fresh[1:]) and not fresh[0]
+    st = kv_t.read_state()
+    assert (st["len"] == ref_state["len"]).all() and (st["pending"] == ref_state["pending"]).all()
+    assert st["status"] == 0 and kv_t.read_step() == c0 + R
+
+
 # ---------------------------------------------------------------- bf16 Llama-shaped prefixes
 def _bf16_case(shape, n_layers, lengths, g, seed=0, capacity=None, return_logits=False):
     torch = torch_cuda()

@@ -76,7 +76,7 @@ def test_noalloc_accept_refuses_requests_beyond_its_scratch():
     with pytest.raises(binding.SpecdecError) as e:
         binding.lib()  # (loaded)
         st = binding.lib().specdec_accept_noalloc(B, g, V, binding.INPUT_PROBS, 1.0, dummy.data_ptr(),
-                                                  dummy.data_ptr(), dummy.data_ptr(), g, None, 0, 0,
+                                                  dummy.data_ptr(), dummy.data_ptr(), g, None, 0, 0, None,
                                                   dummy.data_ptr(), dummy.data_ptr(), None, None)
         binding._check(st, "specdec_accept_noalloc")
     assert e.value.status == -8
