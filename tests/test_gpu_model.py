@@ -287,6 +287,51 @@ def test_bf16_7b_shape_verify(g):
     _bf16_case(synth.LLAMA_7B, 2, [2048], g=g)
 
 
+@pytest.fixture(scope="module")
+def llama7b_2layer():
+    torch_cuda()
+    shape = synth.LLAMA_7B
+    W = synth.make_weights(shape, n_layers=2)
+    dw = binding.DeviceWeights(shape, W)
+    return shape, binding.Model(dw, 2, max_rows=5, max_ctx=2240)
+
+
+@pytest.mark.parametrize("length,bitwise", [(2171, True), (2172, False)])
+def test_bf16_7b_shape_verify_block_vs_steps_across_an_attention_partition_change(llama7b_2layer, length, bitwise):
+    """The attention kernel splits a head's keys into parts from the context
+    bound (the block's bound is len + gamma + 1, a one-row step's len + i + 1),
+    and its partials are merged part by part.  At len 2171 the block and its
+    five one-row steps get the same partition (8 parts of 8 sub-chunks) and the
+    block must equal the steps bit for bit; at len 2172 the block's bound
+    (2177 keys, 69 sub-chunks) takes 11 parts of 6 while the first four steps
+    keep 8 of 8, so the merge order differs and the rows agree within float32
+    rounding of the attention sums instead."""
+    torch = torch_cuda()
+    shape, target = llama7b_2layer
+    g, cap = 4, 2240
+    ctx = synth.make_kv_context(shape, 2, [length])
+    kv = binding.KVCache(target, 1, cap)
+    install_context(kv, ctx, [length], 2, shape.dtype)
+    pend = int(synth.make_prompt(1, shape.vocab, seed=51)[0, 0])
+    drafts = [int(t) for t in synth.make_prompt(g, shape.vocab, seed=52)[0]]
+    kv.set_state([length], [[0, pend]], [1])
+    block = torch.empty((1, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    binding.specdec_verify(target, kv, g, i32(np.array([drafts])), g, block)
+    one = torch.empty((1, 1, shape.vocab), dtype=torch.float32, device="cuda")
+    rows = []
+    for i, t in enumerate([pend] + drafts):
+        kv.set_state([length + i], [[0, t]], [1])
+        binding.specdec_verify(target, kv, 0, None, 0, one)
+        rows.append(one.cpu().numpy()[0, 0].copy())
+    b = block.cpu().numpy()[0]
+    diffs = [float(np.abs(b[i] - rows[i]).max()) for i in range(g + 1)]
+    log(f"len {length}: block vs one-row steps max diff per row {diffs}")
+    if bitwise:
+        assert max(diffs) == 0.0
+    else:
+        assert max(diffs) <= 1e-4
+
+
 def test_bf16_7b_shape_multi_request_ragged():
     # 16 sequences, ragged contexts, gamma 6: 112 rows (one launch of the wide GEMMs)
     lengths = synth.make_ragged_lengths(16, 40, 400)
