@@ -159,6 +159,8 @@ def measured_traffic(kernel: str):
             k, v = line.split(":", 1)
             fields[k.strip()] = v.strip()
     src = os.path.join(ROOT, "paper_2608_10362_amd", "csrc", "gemm.hip")
+    if not os.path.exists(src):
+        return None
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
     if fields.get("kernel_source_sha256") != sha or f"traffic_{kernel}" not in fields:
         return None

@@ -535,7 +535,38 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     s_last = last;
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!s_last) {
+    // The memory system is idle while the combining blocks finish: read this
+    // block's share of the next launch's weights into the last-level cache
+    // (block i of n: the first kNextWeightsPerBlock bytes of slice i of n).
+    // The loaded words are only kept live to the end (no store), so the loads
+    // are issued and waited for and nothing else.
+    if (a.next_w) {
+      const uint32_t nblk = gridDim.x * gridDim.y * gridDim.z;
+      const uint32_t lb = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+      const uint32_t slice = (a.next_w_bytes / nblk + 1023u) & ~1023u;
+      const __amdgpu_buffer_rsrc_t nr = __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(a.next_w),
+                                                                          (short)0, a.next_w_bytes, 0x00020000);
+      // Wave w reads KB-chunks w, w + NW, ... (at most kNextLoads of them), all
+      // issued before the one wait; a dword per lane at a 16-byte stride touches
+      // every line of the chunk.  (Offsets past the share or next_w_bytes read
+      // nothing: the out-of-range bit and the descriptor's range.)
+      constexpr int kNextLoads = 6;
+      const uint32_t lim = min(kNextWeightsPerBlock, slice);
+      uint32_t v[kNextLoads];
+#pragma unroll
+      for (int i = 0; i < kNextLoads; ++i) {
+        const uint32_t c = ((uint32_t)wave + (uint32_t)i * NW) * 1024u;
+        v[i] = __builtin_amdgcn_raw_buffer_load_b32(nr, (lb * slice + c + lane * 16u) | ((uint32_t)(c >= lim) << 31),
+                                                    0, 0);
+      }
+      uint32_t keep = 0;
+#pragma unroll
+      for (int i = 0; i < kNextLoads; ++i) keep ^= v[i];
+      asm volatile("" ::"v"(keep));
+    }
+    return;
+  }
   for (int row = wave; row < RS; row += NW) {  // (wave-uniform) one wave per query row of the tile
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;

@@ -170,7 +170,15 @@ struct AttnArgs {
   // the last block of a (sequence, tile, head) to finish combines the parts
   // (null: a separate combine kernel does).
   uint32_t* counters;
+  // Or null: the weights the next launch streams (the O projection's image,
+  // next_w_bytes long).  With the in-kernel combine, every block that does not
+  // combine reads up to kNextWeightsPerBlock bytes of its share of them after
+  // its partials are out, while the combining blocks finish: the next launch
+  // then starts on data already in the last-level cache.
+  const unsigned char* next_w;
+  uint32_t next_w_bytes;
 };
+constexpr uint32_t kNextWeightsPerBlock = 48u << 10;
 // Counters a model workspace holds for the attention's in-kernel combine.
 size_t attention_counter_count(int n_heads, int n_kv_heads, int max_rows);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s);
