@@ -1579,7 +1579,7 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
 // batch's loads in flight while the current one is multiplied): chosen so W
 // and x fragments stay within the 128 VGPRs a wave of a 16-wave block may use.
 template <int T, int MT> struct Batch;
-template <> struct Batch<1, 1> { static constexpr int UB = 3; static constexpr bool PIPE = true; };
+template <> struct Batch<1, 1> { static constexpr int UB = 4; static constexpr bool PIPE = true; };
 template <> struct Batch<1, 2> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
 template <> struct Batch<1, 4> { static constexpr int UB = 2; static constexpr bool PIPE = false; };
 template <> struct Batch<2, 1> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
