@@ -1579,7 +1579,7 @@ __global__ __launch_bounds__(256) void gemm_f32_vector(GemmArgs a) {
 // batch's loads in flight while the current one is multiplied): chosen so W
 // and x fragments stay within the 128 VGPRs a wave of a 16-wave block may use.
 template <int T, int MT> struct Batch;
-template <> struct Batch<1, 1> { static constexpr int UB = 4; static constexpr bool PIPE = true; };
+template <> struct Batch<1, 1> { static constexpr int UB = 3; static constexpr bool PIPE = true; };
 template <> struct Batch<1, 2> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
 template <> struct Batch<1, 4> { static constexpr int UB = 2; static constexpr bool PIPE = false; };
 template <> struct Batch<2, 1> { static constexpr int UB = 2; static constexpr bool PIPE = true; };
@@ -1616,12 +1616,20 @@ template <int T, int MT, int KIND, bool Q4> struct BatchQ {
   static constexpr bool PIPE = BatchK<T, MT, KIND>::PIPE && PIPE_Q;
 };
 
+// (Single-tile units reading one stacked x fragment per k-step, from memory or
+// LDS, have the registers for four k-steps per buffer: measured 9.9 -> 9.2 us
+// for the 7B O projection.  Two fragments per k-step or float32 x would spill.)
+template <int T, int MT, int KIND, bool Q4, int XS> struct BatchX {
+  static constexpr int UB = (!Q4 && T == 1 && MT == 1 && (XS == 1 || XS == 3)) ? 4 : BatchQ<T, MT, KIND, Q4>::UB;
+  static constexpr bool PIPE = BatchQ<T, MT, KIND, Q4>::PIPE;
+};
+
 template <int T, int MT, int KIND, bool Q4 = false, int XS = 0>
 void launch_mfma_mt(const GemmArgs& a, int tiles, hipStream_t s) {
   const int grid = tiles < compute_units() ? tiles : compute_units();
   hipLaunchKernelGGL(
-      (gemm_bf16_mfma<T, MT, BatchQ<T, MT, KIND, Q4>::UB, BatchQ<T, MT, KIND, Q4>::PIPE, KIND, Q4, XS>), dim3(grid),
-      dim3(kMfmaThreads), 0, s, a, tiles);
+      (gemm_bf16_mfma<T, MT, BatchX<T, MT, KIND, Q4, XS>::UB, BatchX<T, MT, KIND, Q4, XS>::PIPE, KIND, Q4, XS>),
+      dim3(grid), dim3(kMfmaThreads), 0, s, a, tiles);
 }
 
 template <int T, int KIND, bool Q4 = false>
