@@ -372,9 +372,10 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
     rec(SPECDEC_KERNEL_QKV, l, q);
 
     at.layer = l;
-    // (bf16 layer weights: the O projection's image follows the attention)
-    at.next_w = dt == SPECDEC_BF16 && m->wfmt != SPECDEC_WEIGHTS_INT4 ? (const unsigned char*)m->wo[l] : nullptr;
-    at.next_w_bytes = (uint32_t)(packed_elems(d.d_model, H * hd) * 2);
+    // (the O projection's image follows the attention: bf16 fragments, or the INT4 code blocks)
+    at.next_w = dt == SPECDEC_BF16 ? (const unsigned char*)m->wo[l] : nullptr;
+    at.next_w_bytes = (uint32_t)(m->wfmt == SPECDEC_WEIGHTS_INT4 ? packed_int4_frag_bytes(d.d_model, H * hd)
+                                                                   : packed_elems(d.d_model, H * hd) * 2);
     if (dt != SPECDEC_BF16) {
       Timed t(SPECDEC_KERNEL_ROPE_APPEND, s);
       SD_TRY(launch_rope_append(at, s));
