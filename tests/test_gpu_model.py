@@ -347,6 +347,14 @@ def test_bf16_1b_shape_stacked_operand_row_counts(B, g):
     _bf16_case(synth.LLAMA_1B, 2, list(lengths), g=g, seed=6)
 
 
+@pytest.mark.parametrize("B,g", [(7, 4), (8, 7)])
+def test_bf16_1b_shape_skinny_row_tiles(B, g):
+    # 35 and 64 rows: the skinny kernels' four-row-tile variants (float32 x, no
+    # stacked operand), up to the largest pass before the wide kernels (65 rows)
+    lengths = synth.make_ragged_lengths(B, 1, 300, seed=9)
+    _bf16_case(synth.LLAMA_1B, 2, list(lengths), g=g, seed=4)
+
+
 def test_bf16_7b_shape_many_short_sequences():
     # 10 sequences of at most ~250 keys, gamma 6 (70 rows): more (kv head,
     # sequence) units than CUs and fewer than 12 sub-chunks of 32 keys per
