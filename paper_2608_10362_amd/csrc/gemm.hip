@@ -263,6 +263,10 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
   // descriptors) in scalar registers.
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kg = lane >> 4, mrow = lane & 15;
+  // Stacked x: the lanes of a fragment's padding rows (rows >= M of its hi and
+  // lo halves) read nothing, which keeps them zero; only rows < M reach an
+  // output (5 rows: 10 of the 16 fragment rows fetched, 1 row: 2).
+  const uint32_t xrbad = XS ? (uint32_t)(((XS == 2 ? mrow : (mrow & 7)) >= a.M)) << 31 : 0u;
   const int K = a.K;
   const int KS = (K + 31) / 32;
 #ifdef SPECDEC_KSTEP_CONTIGUOUS
@@ -362,7 +366,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
       } else if constexpr (XS) {
 #pragma unroll
         for (int f = 0; f < XS; ++f) {
-          const uint32_t xoff = (((uint32_t)ks * XS + f) * 1024u + lane * 16u) | wbad;
+          const uint32_t xoff = (((uint32_t)ks * XS + f) * 1024u + lane * 16u) | wbad | xrbad;
           xv[u][f][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, xoff, 0, 0));
         }
       } else {
@@ -570,7 +574,7 @@ __global__ __launch_bounds__(kMfmaThreads) void gemm_bf16_mfma(GemmArgs a, int n
     for (int j = 0; j < 8; ++j) {
       const int ks = ks0 + j * kstride;
       xl[j] = __builtin_amdgcn_raw_buffer_load_b128(
-          xr, ((uint32_t)ks * 1024u + lane * 16u) | ((uint32_t)(j >= my_ks || ks >= KS) << 31), 0, 0);
+          xr, ((uint32_t)ks * 1024u + lane * 16u) | ((uint32_t)(j >= my_ks || ks >= KS) << 31) | xrbad, 0, 0);
     }
   }
   if (total > 0) {
