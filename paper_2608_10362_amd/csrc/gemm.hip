@@ -710,6 +710,7 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
   const int M = a.M, K = a.K, G = (K + 127) / 128;
   const int my_g = max(0, min(G - wave * gw, gw));  // groups of this wave
   const int n_chunks = kQ4Waves * GPW * M * 16;      // x chunks per window
+  const int chr = (n_chunks + kQ4Threads - 1) / kQ4Threads;  // of them per thread (<= kQ4Chunks)
 
   // Window wi: chunk c = (slot*M + m)*16 + 4j + kq, slot = wave'*GPW + lgw,
   // holds x[m][128*grp + 32j + 8kq .. +7] of group grp = wave'*gw + wi*GPW + lgw.
@@ -718,6 +719,9 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
     const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, (uint32_t)M * a.ldx * 4u);
 #pragma unroll
     for (int i = 0; i < kQ4Chunks; ++i) {
+      // (block-uniform: pieces past the window's rows are not requested at all;
+      // an out-of-range load still takes its issue slot in the texture unit)
+      if (i >= chr) break;
       const int c = tid + i * kQ4Threads, jq = c & 15, r = c >> 4;
       const int m = r % M, slot = r / M, lg = wi * GPW + slot % GPW;
       const int grp = (slot / GPW) * gw + lg;
