@@ -1781,7 +1781,7 @@ bool gemm_wide(int dtype, int M) { return dtype == SPECDEC_BF16 && M > kMaxGemmR
 int gemm_launch_rows(int dtype, int M) {
   return !gemm_wide(dtype, M) ? kMaxGemmRows : (M > kWideRows ? kTileLaunchRows : kWideRows);
 }
-constexpr int kWideSplitMax = 4;
+constexpr int kWideSplitMax = 8;
 size_t wide_ypart_floats(int n_rows) {
   return (size_t)std::max(kWideSplitMax * kWideRows, kTilePartialRows) * n_rows;
 }
@@ -1877,13 +1877,16 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
     case EPI_SWIGLU: launch_wide_t<2, EPI_SWIGLU>(a, (a.n_rows + 63) / 64, KS, 1, s); break;
     case EPI_RESID: {
       if (!a.ypart) return hipErrorInvalidValue;
-      // split K until the grid covers the CUs (each split at least one k-step)
-      const int blocks = (a.n_rows + 63) / 64;
+      // Two tiles per wave (each x slab serves 128 columns) and K split until the
+      // grid covers the CUs (each split at least one k-step): the 7B O and down
+      // projections over 112 rows run 32 column blocks x 8 splits.  (One tile per
+      // wave and 4 splits: config 5 verify 17.10 -> 16.50 ms on one box.)
+      const int blocks = (a.n_rows + 127) / 128;
       int n_split = std::min(kWideSplitMax, std::max(1, (cus + blocks - 1) / blocks));
       n_split = std::min(n_split, KS);
       const int ks_per_split = (KS + n_split - 1) / n_split;
       n_split = (KS + ks_per_split - 1) / ks_per_split;
-      launch_wide_t<1, EPI_RESID>(a, blocks, ks_per_split, n_split, s);
+      launch_wide_t<2, EPI_RESID>(a, blocks, ks_per_split, n_split, s);
       hipLaunchKernelGGL(resid_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8),
                          dim3(256), 0, s, a, n_split);
       break;
