@@ -809,10 +809,11 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
   // The wave's code blocks and scales, group-major.  All scales come first
   // (a group's products wait for its scales, and loads complete in issue
   // order); the codes of D groups are requested here and each later group's
-  // D groups ahead of its products, so the vector-memory issue of a large
-  // share (about 64 KB per CU per group issued) does not hold up the x
-  // conversion, and about 64 KB per CU stays in flight.
-  constexpr int D = F >= 6 ? 2 : (F >= 3 ? 3 : (F == 2 ? 4 : 8));
+  // D groups ahead of its products.  A shallow depth keeps the prologue's
+  // vector-memory issue short, so it does not hold up the x conversion:
+  // deeper requests (up to 8 groups, about 64 KB per CU in flight) measured
+  // 2% slower over a 7B verify, and one group is too few below six.
+  constexpr int D = F >= 6 ? 1 : 2;
   u32x4 cw[F][GW];
   uint32_t sw[F][GW];
   __amdgpu_buffer_rsrc_t crs[F], srs[F];
