@@ -65,7 +65,8 @@ typedef enum {
   SPECDEC_ERR_HIP = -5,         /* a HIP runtime call failed */
   SPECDEC_ERR_UNSUPPORTED = -6, /* valid request outside what is implemented */
   SPECDEC_ERR_BAD_TOKEN = -7,   /* token id outside [0, vocab) (device status) */
-  SPECDEC_ERR_SCRATCH_LIMIT = -8 /* needs more than the static scratch of specdec_accept_noalloc */
+  SPECDEC_ERR_SCRATCH_LIMIT = -8, /* needs more than the static scratch of specdec_accept_noalloc */
+  SPECDEC_ERR_WAIT_EXPIRED = -9   /* a kernel's bounded wait for other blocks ran out (device status) */
 } specdec_status;
 
 enum { SPECDEC_F32 = 0, SPECDEC_BF16 = 1 };

@@ -26,7 +26,8 @@ PURPOSE_DRAFT, PURPOSE_ACCEPT, PURPOSE_RESAMPLE = 0, 1, 2
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape", -3: "KV capacity exceeded",
           -4: "non-finite probability or logit", -5: "HIP runtime error", -6: "unsupported request",
           -7: "token id out of range",
-          -8: "request needs more scratch than the static no-allocation buffer holds"}
+          -8: "request needs more scratch than the static no-allocation buffer holds",
+          -9: "a kernel's bounded wait for other blocks ran out"}
 
 
 # Size of the static scratch of specdec_accept_noalloc (SPECDEC_ACCEPT_NOALLOC_SCRATCH_BYTES).

@@ -39,8 +39,11 @@ struct specdec_model {
   uint16_t* xs_d = nullptr;  // bf16: the stacked x operand of the d_model-column GEMMs (passes of <= 16 rows)
   uint16_t* xs_f = nullptr;  // bf16: the stacked attention output (the O projection's x), then SwiGLU output
   float* ypart = nullptr;  // split-K partials of the wide residual GEMMs (passes of more than 64 rows)
-  uint32_t* attn_ctr = nullptr;           // bf16: the attention's combine counters (zero between launches)
-  mutable bool attn_ctr_ready = false;    // set once they have been zeroed on a stream
+  uint32_t* attn_ctr = nullptr;           // bf16: the attention combine's epochs
+  uint32_t* attn_cnt = nullptr;           // bf16: the one-round attention combine's arrival counters
+  uint64_t* attn_ll = nullptr;            // bf16: the attention combine's tagged partial words
+  size_t attn_ll_words = 0;
+  mutable bool attn_ctr_ready = false;    // set once all three have been zeroed on a stream
   int chunk, n_split_max;
   // per-layer launches of the last forward pass, for specdec_time_kernel
   // (entry l: layer l; the head and the embedding have one)
@@ -99,7 +102,7 @@ int elem_bytes(int dtype) { return dtype == SPECDEC_BF16 ? 2 : 4; }
 
 // Workspace layout (in order); shared by specdec_workspace_bytes and create.
 struct WsLayout {
-  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, xs_d, xs_f, ypart, ctr, total;
+  size_t rows, rope, h, xg, ss, qkv, qr, o_part, ml_part, o, u, logits, samp, xs_d, xs_f, ypart, ctr, cnt, ll, total;
   int ss_parts, chunk, n_split;
 };
 
@@ -133,6 +136,8 @@ WsLayout ws_layout(const specdec_model_desc* d, int max_rows, int max_ctx) {
   w.xs_f = take(d->dtype == SPECDEC_BF16 ? (size_t)(std::max(d->ffn_dim, H * hd) + 31) / 32 * 2048 : 0);
   w.ypart = take(wide ? wide_ypart_floats(d->d_model) * 4 : 0);
   w.ctr = take(d->dtype == SPECDEC_BF16 ? attention_counter_count(H, G, max_rows) * 4 : 0);
+  w.cnt = take(d->dtype == SPECDEC_BF16 ? attention_counter_count(H, G, max_rows) * 4 : 0);
+  w.ll = take(d->dtype == SPECDEC_BF16 ? attention_ll_words(H, hd, max_rows, w.n_split) * 8 : 0);
   w.total = off;
   return w;
 }
@@ -341,11 +346,15 @@ specdec_status forward(const specdec_model* m, specdec_kv* kv, RowsArgs ra, int 
   at.o = m->o;
   at.status = kv_status(kv);
   at.seq_bound = M / ra.rps > 1;
-  if (m->attn_ctr && !m->attn_ctr_ready) {  // (a fill kernel: a capturing caller may record it)
+  if (m->attn_ctr && !m->attn_ctr_ready) {  // (fill kernels: a capturing caller may record them)
     SD_TRY(launch_fill_u32(m->attn_ctr, attention_counter_count(H, G, m->max_rows), 0u, s));
+    SD_TRY(launch_fill_u32(m->attn_cnt, attention_counter_count(H, G, m->max_rows), 0u, s));
+    SD_TRY(launch_fill_u32((uint32_t*)m->attn_ll, 2 * m->attn_ll_words, 0u, s));
     m->attn_ctr_ready = true;
   }
-  at.counters = m->attn_ctr;
+  at.epochs = m->attn_ctr;
+  at.counters = m->attn_cnt;
+  at.ll = m->attn_ll;
   at.xs = stk ? m->xs_f : nullptr;
   at.stt = stt;
 
@@ -616,6 +625,9 @@ specdec_status specdec_model_create_fmt(const specdec_model_desc* desc, const sp
   m->xs_f = desc->dtype == SPECDEC_BF16 ? (uint16_t*)(base + L.xs_f) : nullptr;
   m->ypart = gemm_wide(desc->dtype, max_rows) ? (float*)(base + L.ypart) : nullptr;
   m->attn_ctr = desc->dtype == SPECDEC_BF16 ? (uint32_t*)(base + L.ctr) : nullptr;
+  m->attn_cnt = desc->dtype == SPECDEC_BF16 ? (uint32_t*)(base + L.cnt) : nullptr;
+  m->attn_ll = desc->dtype == SPECDEC_BF16 ? (uint64_t*)(base + L.ll) : nullptr;
+  m->attn_ll_words = desc->dtype == SPECDEC_BF16 ? attention_ll_words(desc->n_heads, desc->head_dim, max_rows, L.n_split) : 0;
   m->chunk = L.chunk;
   m->n_split_max = L.n_split;
   *out = m;
@@ -1098,6 +1110,7 @@ const char* specdec_status_string(specdec_status s) {
     case SPECDEC_ERR_UNSUPPORTED: return "unsupported request";
     case SPECDEC_ERR_BAD_TOKEN: return "token id out of range";
     case SPECDEC_ERR_SCRATCH_LIMIT: return "request needs more scratch than the static no-allocation buffer holds";
+    case SPECDEC_ERR_WAIT_EXPIRED: return "a kernel's bounded wait for other blocks ran out";
   }
   return "unknown status";
 }

@@ -202,12 +202,30 @@ __device__ __forceinline__ float group16_sum(float v) {
 // Dynamic LDS: per wave a P tile [16][36] (the transposed read of P V), then,
 // reused once every wave is past P V, the merge buffers [NW][RS][HD + 4] of
 // O (rows padded against bank conflicts) and [NW][RS][2] of (max, sum), RS =
-// query rows of the tile.
-__host__ __device__ inline size_t attn_block_lds(int NW, int RS, int HD) {
+// query rows of the tile.  With the in-kernel combine (own), the combining
+// block's own part [RS][HD + 2] (O, max, sum) follows them.
+__host__ __device__ inline size_t attn_block_shared(int NW, int RS, int HD) {
   const size_t p = (size_t)NW * 16 * (kSubKeys + 4);
   const size_t m = (size_t)NW * RS * (HD + 6);
-  return (p > m ? p : m) * sizeof(float);
+  return p > m ? p : m;
 }
+__host__ __device__ inline size_t attn_block_lds(int NW, int RS, int HD, bool own = false) {
+  return (attn_block_shared(NW, RS, HD) + (own ? (size_t)RS * (HD + 2) : 0)) * sizeof(float);
+}
+
+// Flagged partial words of the in-kernel combine: the float in the low half,
+// the launch's tag in the high half, written and read as single 64-bit
+// agent-scope accesses (a reader sees a whole word, old or new).
+__device__ __forceinline__ void ll_put(uint64_t* p, float v, uint32_t tag) {
+  __hip_atomic_store(p, ((uint64_t)tag << 32) | (uint64_t)__float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+// Cache-policy bits of a load served by the coherent level (sc1), not by a
+// possibly stale line of this XCD's L2.
+constexpr int kCoherentLoad = 16;
+// Polls of the combining block before it gives up (each takes a memory round
+// trip, about a microsecond: a quarter of a second or so in all).
+constexpr int kLlMaxPolls = 1 << 18;
 
 constexpr int kMaxPartWaves = 12;  // 3 waves per SIMD: up to 170 VGPRs per lane
 constexpr int kLoopWaves = 4;      // waves per block when waves loop over several sub-chunks
@@ -273,6 +291,17 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     rd_pos = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, pos), 0, 0);
     rd_valid = (int)__builtin_amdgcn_raw_buffer_load_b32(rr, roff + offsetof(RowDesc, valid), 0, 0);
   }
+  // In-kernel combine of looping launches: the epoch of the sequence, tile
+  // and kv head (this launch tags its words with epoch + 1), read through the
+  // coherent level (sc1) and used only once the partials are out.
+  const bool ll_mode = LOOP && a.ll != nullptr;
+  const uint32_t ep_idx = (uint32_t)(((size_t)b * (gridDim.x / n_part) + mt) * G + g);
+  uint32_t ep_raw = 0;
+  if constexpr (LOOP)  // (unconditional load, range 0 without the combine: a branch here made the key loads wait for it)
+    ep_raw = __builtin_amdgcn_raw_buffer_load_b32(
+        __builtin_amdgcn_make_buffer_rsrc(a.epochs, (short)0, ll_mode ? (ep_idx + 1u) * 4u : 0u, 0x00020000),
+        ep_idx * 4u, 0, kCoherentLoad);
+  float* const sown = smem + attn_block_shared(NW, RS, HD);  // (combiner: its own part per row)
   if (wave < sub_here) {  // (wave-uniform) a wave past the part's sub-chunks only joins the merge
     // K fragments of a sub-chunk: 2 x KST contiguous 1 KB fragments (k0 + 32 <= capacity);
     // V fragments: DT contiguous 1 KB fragments (32 positions x 16 dims each).
@@ -410,6 +439,33 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
   }
 
   constexpr int DPL = HD >= 64 ? HD / 64 : 1;
+  // The combining block.  Looping launches (several rounds of blocks per
+  // CU): the block of the last part holding a key some valid row of the tile
+  // sees (the parts after it hold none); every part it waits for has a lower
+  // block index, so it was dispatched before it, and no other block waits for
+  // anything; its own part stays in LDS.  The other blocks end without
+  // waiting for their stores, which frees their CU for the next round sooner.
+  // One-round launches: the last block to count itself, after its partial
+  // stores are acknowledged (faster there than a fixed combining block that
+  // polls: all blocks run at once, and polling started before the other
+  // parts' words had landed).  (Lane reads of the descriptors, long arrived.)
+  // (The descriptor values pass through an empty asm here so that the
+  // compiler does not share this test with the one before the key loads and
+  // wait for the descriptors before issuing them.)
+  int last_part = n_part - 1;
+  uint32_t tag = 0;
+  if (ll_mode) {
+    int rp = rd_pos, rv = rd_valid;
+    asm volatile("" : "+v"(rp), "+v"(rv));
+    const int vpos = (lane < 16 && ql < nq && rv) ? rp : -1;
+    int mpos = -1;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mpos = max(mpos, __builtin_amdgcn_readlane(vpos, i));
+    if (mpos >= 0) last_part = min(mpos / a.chunk, n_part - 1);
+    tag = ep_raw + 1u == 0u ? 1u : ep_raw + 1u;
+  }
+  const bool combiner = LOOP && ll_mode && part == last_part;
+  uint32_t* const epoch = a.epochs + ep_idx;  // (combiner: the next launch's epoch goes here)
   if (NW == 1) {  // (block-uniform) the wave's own (max, sum, O) rows are the part's partials
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -417,7 +473,23 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
       if (row >= RS || qpos[r] < 0 || mx[r] == -INFINITY) continue;
       const int qc = mt * 16 + row;
       const size_t slot = ((size_t)(r0 + qc / group) * H + g * group + qc % group) * n_part + part;
-      if (a.counters) {
+      if (combiner) {
+        float* own = sown + (size_t)row * (HD + 2);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) own[dt * 16 + c16] = of[dt][r];
+        if (c16 == 0) {
+          own[HD] = mx[r];
+          own[HD + 1] = sm[r];
+        }
+      } else if (ll_mode) {
+        uint64_t* w = a.ll + slot * (HD + 2);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) ll_put(w + dt * 16 + c16, of[dt][r], tag);
+        if (c16 == 0) {
+          ll_put(w + HD, mx[r], tag);
+          ll_put(w + HD + 1, sm[r], tag);
+        }
+      } else if (a.counters) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           __hip_atomic_store(&a.o_part[slot * HD + dt * 16 + c16], of[dt][r], __ATOMIC_RELAXED,
@@ -497,7 +569,25 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     const int qc = mt * 16 + row;
     const int qrow = r0 + qc / group, head = g * group + qc % group;
     const size_t slot = ((size_t)qrow * H + head) * n_part + part;
-    if (a.counters) {  // (agent-scope stores: visible to the combining block on any XCD once completed)
+    if (combiner) {  // (kept in LDS for its own combine)
+      float* own = sown + (size_t)row * (HD + 2);
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) own[lane + 64 * j] = O[j];
+      if (lane == 0) {
+        own[HD] = M;
+        own[HD + 1] = L;
+      }
+    } else if (ll_mode) {  // (tagged words: the combining block polls them)
+      uint64_t* w = a.ll + slot * (HD + 2);
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) ll_put(w + lane + 64 * j, O[j], tag);
+      if (lane == 0) {
+        ll_put(w + HD, M, tag);
+        ll_put(w + HD + 1, L, tag);
+      }
+    } else if (a.counters) {  // (agent-scope stores: visible to the combining block on any XCD once completed)
 #pragma unroll
       for (int j = 0; j < DPL; ++j)
         if (lane + 64 * j < HD)
@@ -517,28 +607,11 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
     }
   }
   }
-  if (!a.counters) return;
-
-  // The last block of this (sequence, tile, kv head) to finish combines the
-  // parts: every wave's partial stores have completed before the block's
-  // single counter increment, and the combining block reads the partials
-  // with agent-scope loads.  The counter goes back to zero for the next launch.
-  __shared__ int s_last;
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int n_mt = gridDim.x / n_part;
-    uint32_t* ctr = a.counters + ((size_t)b * n_mt + mt) * G + g;
-    const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = old == (uint32_t)(n_part - 1);
-    if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = last;
-  }
-  __syncthreads();
-  if (!s_last) {
-    // The memory system is idle while the combining blocks finish: read this
-    // block's share of the next launch's weights into the last-level cache
-    // (block i of n: the first kNextWeightsPerBlock bytes of slice i of n).
+  // The memory system is idle while the combining blocks finish: blocks that
+  // do not combine read their share of the next launch's weights into the
+  // last-level cache before they end.
+  auto read_ahead = [&]() {
+    // (Block i of n: the first kNextWeightsPerBlock bytes of slice i of n.)
     // The loaded words are only kept live to the end (no store), so the loads
     // are issued and waited for and nothing else.
     if (a.next_w) {
@@ -565,62 +638,205 @@ __global__ __launch_bounds__(LOOP ? 64 * kLoopWaves : 64 * kMaxPartWaves, LOOP ?
       for (int i = 0; i < kNextLoads; ++i) keep ^= v[i];
       asm volatile("" ::"v"(keep));
     }
-    return;
-  }
-  for (int row = wave; row < RS; row += NW) {  // (wave-uniform) one wave per query row of the tile
-    const int qc = mt * 16 + row;
-    const int qrow = r0 + qc / group, head = g * group + qc % group;
-    RowDesc rd;
-    rd.pos = __shfl(rd_pos, row, kWave);  // (lane `row` loaded this query's row descriptor)
-    rd.valid = __shfl(rd_valid, row, kWave);
-    float* o = a.o + ((size_t)qrow * H + head) * HD;
-    if (!rd.valid) {
-#pragma unroll
-      for (int j = 0; j < DPL; ++j)
-        if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, 0.f);
-      continue;
+  };
+  if constexpr (LOOP) {
+    if (!ll_mode) return;
+    if (!combiner) {
+      read_ahead();
+      return;
     }
-    // parts holding keys <= pos (the last part also holds the remainder)
-    const int nch = min(rd.pos / a.chunk + 1, n_part);
-    if (rd.pos + 1 > a.max_ctx && lane == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
-    const size_t base = ((size_t)qrow * H + head) * n_part;
-    // lane p < nch: part p's (max, sum); the first parts' outputs in the same round trip
-    constexpr int PB = 8;
-    const int pl = min(lane, nch - 1);
-    const float mp = __hip_atomic_load(&a.ml_part[2 * (base + pl)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const float lp = __hip_atomic_load(&a.ml_part[2 * (base + pl) + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    float acc[DPL];
-#pragma unroll
-    for (int j = 0; j < DPL; ++j) acc[j] = 0.f;
-    float mx = 0.f, wgt = 0.f;
-    for (int p0 = 0; p0 < nch; p0 += PB) {  // (wave-uniform)
-      float ov[PB][DPL];
-#pragma unroll
-      for (int pp = 0; pp < PB; ++pp) {
-        const int p = min(p0 + pp, nch - 1);  // (parts past nch get weight 0 below)
+    // The combining block: one wave per query row of the tile.  Its own part
+    // comes from LDS; the other parts' words are polled until every one read
+    // carries this launch's tag (each write and read is a whole 64-bit word),
+    // in batches of PB parts; the parts are added in part order.
+    __syncthreads();  // (the block's own part in LDS)
+    for (int row = wave; row < RS; row += NW) {  // (wave-uniform)
+      const int qc = mt * 16 + row;
+      const int qrow = r0 + qc / group, head = g * group + qc % group;
+      RowDesc rd;
+      rd.pos = __shfl(rd_pos, row, kWave);  // (lane `row` loaded this query's row descriptor)
+      rd.valid = __shfl(rd_valid, row, kWave);
+      float* o = a.o + ((size_t)qrow * H + head) * HD;
+      if (!rd.valid) {
 #pragma unroll
         for (int j = 0; j < DPL; ++j)
-          ov[pp][j] = lane + 64 * j < HD ? __hip_atomic_load(&a.o_part[(base + p) * HD + lane + 64 * j],
-                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                                         : 0.f;
+          if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, 0.f);
+        continue;
       }
-      if (p0 == 0) {
-        mx = wave_max(lane < nch ? mp : -INFINITY);
-        wgt = lane < nch ? expf(mp - mx) : 0.f;
+      // parts holding keys <= pos (the last part also holds the remainder); the
+      // last one, when among them, is this block's own (nch <= last_part + 1)
+      const int nch = min(rd.pos / a.chunk + 1, n_part);
+      if (rd.pos + 1 > a.max_ctx && lane == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
+      const bool own_row = nch == last_part + 1;
+      const int npoll = own_row ? last_part : nch;  // parts read from memory
+      const float* own = sown + (size_t)row * (HD + 2);
+      const uint64_t* w = a.ll + ((size_t)qrow * H + head) * n_part * (HD + 2);
+      constexpr int PB = 8;
+      // lane p < nch: part p's (max, sum)
+      float mp = -INFINITY, lp = 0.f;
+      if (lane == last_part && own_row) {
+        mp = own[HD];
+        lp = own[HD + 1];
       }
+      float acc[DPL];
 #pragma unroll
-      for (int pp = 0; pp < PB; ++pp) {
-        const float w = __shfl(wgt, (p0 + pp) & 63, kWave);
-        const float wv = p0 + pp < nch ? w : 0.f;
+      for (int j = 0; j < DPL; ++j) acc[j] = 0.f;
+      float mx = 0.f, wgt = 0.f;
+      bool expired = false;
+      const int pl = min(lane, max(npoll - 1, 0));  // (clamped: every load below reads a polled slot)
+      for (int p0 = 0; p0 < nch; p0 += PB) {  // (wave-uniform)
+        float ov[PB][DPL];
+        for (int poll = 0;; ++poll) {  // (wave-uniform)
+          // Every load first (branch-free, addresses clamped to polled slots),
+          // then the tag tests and the selection of own and absent parts.
+          uint64_t wm = 0, wl = 0, wo[PB][DPL];
+          if (npoll > 0) {  // (wave-uniform)
+            if (p0 == 0) {
+              wm = __hip_atomic_load(const_cast<uint64_t*>(w) + (size_t)pl * (HD + 2) + HD, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+              wl = __hip_atomic_load(const_cast<uint64_t*>(w) + (size_t)pl * (HD + 2) + HD + 1, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+            }
 #pragma unroll
-        for (int j = 0; j < DPL; ++j) acc[j] += wv * ov[pp][j];
+            for (int pp = 0; pp < PB; ++pp) {
+              const int pc = min(p0 + pp, npoll - 1);
+#pragma unroll
+              for (int j = 0; j < DPL; ++j)
+                wo[pp][j] = __hip_atomic_load(const_cast<uint64_t*>(w) + (size_t)pc * (HD + 2) + min(lane + 64 * j, HD - 1),
+                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+          }
+          bool ok = true;
+          if (p0 == 0 && lane < npoll) {
+            ok = (uint32_t)(wm >> 32) == tag && (uint32_t)(wl >> 32) == tag;
+            mp = __uint_as_float((uint32_t)wm);
+            lp = __uint_as_float((uint32_t)wl);
+          }
+#pragma unroll
+          for (int pp = 0; pp < PB; ++pp) {
+            const int p = p0 + pp;
+#pragma unroll
+            for (int j = 0; j < DPL; ++j) {
+              const int dd = lane + 64 * j;
+              const bool polled = p < npoll && dd < HD;
+              ok = ok && (!polled || (uint32_t)(wo[pp][j] >> 32) == tag);
+              ov[pp][j] = polled ? __uint_as_float((uint32_t)wo[pp][j])
+                                 : (p < nch && dd < HD ? own[min(dd, HD - 1)] : 0.f);
+            }
+          }
+          if (__all(ok)) break;
+          if (poll >= kLlMaxPolls) {
+            expired = true;
+            break;
+          }
+        }
+        if (expired) break;
+        if (p0 == 0) {
+          mx = wave_max(lane < nch ? mp : -INFINITY);
+          wgt = lane < nch ? expf(mp - mx) : 0.f;
+        }
+#pragma unroll
+        for (int pp = 0; pp < PB; ++pp) {
+          const float wp = __shfl(wgt, (p0 + pp) & 63, kWave);
+          const float wv = p0 + pp < nch ? wp : 0.f;
+#pragma unroll
+          for (int j = 0; j < DPL; ++j) acc[j] += wv * ov[pp][j];
+        }
       }
+      if (expired) {  // (a part never arrived: report it, write zeros)
+        if (lane == 0) set_status(a.status, kStatusWaitExpired);
+#pragma unroll
+        for (int j = 0; j < DPL; ++j)
+          if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, 0.f);
+        continue;
+      }
+      const float L = wave_sum(wgt * lp);
+      const float inv = 1.0f / L;
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, acc[j] * inv);
     }
-    const float L = wave_sum(wgt * lp);
-    const float inv = 1.0f / L;
+    // Every part of this launch has been read (so every block of it has read
+    // the epoch): the next launch's tag.
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_store(epoch, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    if (!a.counters) return;
+
+    // The last block of this (sequence, tile, kv head) to finish combines the
+    // parts: every wave's partial stores have completed before the block's
+    // single counter increment, and the combining block reads the partials
+    // with agent-scope loads.  The counter goes back to zero for the next launch.
+    __shared__ int s_last;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t* ctr = a.counters + ep_idx;
+      const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int last = old == (uint32_t)(n_part - 1);
+      if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = last;
+    }
+    __syncthreads();
+    if (!s_last) {
+      read_ahead();
+      return;
+    }
+    for (int row = wave; row < RS; row += NW) {  // (wave-uniform) one wave per query row of the tile
+      const int qc = mt * 16 + row;
+      const int qrow = r0 + qc / group, head = g * group + qc % group;
+      RowDesc rd;
+      rd.pos = __shfl(rd_pos, row, kWave);  // (lane `row` loaded this query's row descriptor)
+      rd.valid = __shfl(rd_valid, row, kWave);
+      float* o = a.o + ((size_t)qrow * H + head) * HD;
+      if (!rd.valid) {
 #pragma unroll
-    for (int j = 0; j < DPL; ++j)
-      if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, acc[j] * inv);
+        for (int j = 0; j < DPL; ++j)
+          if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, 0.f);
+        continue;
+      }
+      // parts holding keys <= pos (the last part also holds the remainder)
+      const int nch = min(rd.pos / a.chunk + 1, n_part);
+      if (rd.pos + 1 > a.max_ctx && lane == 0) set_status(a.status, kStatusKvCapacity);  // the host's bound was wrong
+      const size_t base = ((size_t)qrow * H + head) * n_part;
+      // lane p < nch: part p's (max, sum); the first parts' outputs in the same round trip
+      constexpr int PB = 8;
+      const int pl = min(lane, nch - 1);
+      const float mp = __hip_atomic_load(&a.ml_part[2 * (base + pl)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float lp = __hip_atomic_load(&a.ml_part[2 * (base + pl) + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      float acc[DPL];
+#pragma unroll
+      for (int j = 0; j < DPL; ++j) acc[j] = 0.f;
+      float mx = 0.f, wgt = 0.f;
+      for (int p0 = 0; p0 < nch; p0 += PB) {  // (wave-uniform)
+        float ov[PB][DPL];
+#pragma unroll
+        for (int pp = 0; pp < PB; ++pp) {
+          const int p = min(p0 + pp, nch - 1);  // (parts past nch get weight 0 below)
+#pragma unroll
+          for (int j = 0; j < DPL; ++j)
+            ov[pp][j] = lane + 64 * j < HD ? __hip_atomic_load(&a.o_part[(base + p) * HD + lane + 64 * j],
+                                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                           : 0.f;
+        }
+        if (p0 == 0) {
+          mx = wave_max(lane < nch ? mp : -INFINITY);
+          wgt = lane < nch ? expf(mp - mx) : 0.f;
+        }
+#pragma unroll
+        for (int pp = 0; pp < PB; ++pp) {
+          const float w = __shfl(wgt, (p0 + pp) & 63, kWave);
+          const float wv = p0 + pp < nch ? w : 0.f;
+#pragma unroll
+          for (int j = 0; j < DPL; ++j) acc[j] += wv * ov[pp][j];
+        }
+      }
+      const float L = wave_sum(wgt * lp);
+      const float inv = 1.0f / L;
+#pragma unroll
+      for (int j = 0; j < DPL; ++j)
+        if (lane + 64 * j < HD) put_o(a, o, qrow, head, lane + 64 * j, acc[j] * inv);
+    }
   }
 }
 
@@ -823,6 +1039,13 @@ size_t attention_counter_count(int n_heads, int n_kv_heads, int max_rows) {
   return (size_t)n_kv_heads * ((size_t)max_rows * group / 16 + (size_t)max_rows + 1);
 }
 
+size_t attention_ll_words(int n_heads, int head_dim, int max_rows, int n_split_max) {
+  // slots (row, head, part) for up to min(kLlMaxParts, n_split_max) parts: a
+  // launch's parts never outnumber its sub-chunks, ceil(max_ctx / 32)
+  const size_t parts = (size_t)std::min(kLlMaxParts, n_split_max);
+  return (size_t)max_rows * n_heads * parts * (head_dim + 2);
+}
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int B = a.M / a.rps;
   AttnArgs ab = a;  // the bf16 path chooses its own parts
@@ -861,13 +1084,26 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
     if (NW > kMaxPartWaves || attn_block_lds(NW, RS, a.head_dim) > 65536) return hipErrorInvalidValue;
     ab.n_split = n_part;
     ab.chunk = S * kSubKeys;
-    // In-kernel combine: one part per lane, and at most two query rows per wave
-    // of the combining block (its rows go one after another); otherwise the
-    // separate combine kernel (one wave per row and head).
-    if (n_part > kWave || (RS + NW - 1) / NW > 2) ab.counters = nullptr;
-    dim3 grid(n_part * n_mt, a.n_kv_heads, B);
-    const size_t lds = attn_block_lds(NW, RS, a.head_dim);
+    // In-kernel combine: one part per lane, at most two query rows per wave of
+    // the combining block (its rows go one after another), and its own part's
+    // rows fit in LDS next to the merge buffers; otherwise the separate
+    // combine kernel (one wave per row and head).
+    // (Looping launches combine through the tagged words and keep the
+    // combining block's own part in LDS; one-round launches count arrivals.)
     const bool loop = S > NW;
+    if (loop) ab.counters = nullptr;
+    else {
+      ab.ll = nullptr;
+      ab.epochs = nullptr;
+    }
+    if (n_part > kLlMaxParts || (RS + NW - 1) / NW > 2 || attn_block_lds(NW, RS, a.head_dim, loop) > 65536 ||
+        (loop ? !ab.ll || !ab.epochs : !ab.counters)) {
+      ab.epochs = nullptr;
+      ab.counters = nullptr;
+      ab.ll = nullptr;
+    }
+    dim3 grid(n_part * n_mt, a.n_kv_heads, B);
+    const size_t lds = attn_block_lds(NW, RS, a.head_dim, ab.ll != nullptr);
     if (loop && NW > kLoopWaves) return hipErrorInvalidValue;  // (the looping kernel's block bound)
 #define SD_ATTN(HDV)                                                                                       \
   if (loop) hipLaunchKernelGGL((attn_block_kernel<HDV, true>), grid, dim3(64 * NW), lds, s, ab, S, n_sub, NW); \
@@ -886,7 +1122,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (ab.kv.dtype == SPECDEC_BF16 && ab.counters) return hipSuccess;  // combined by the blocks
+  if (ab.kv.dtype == SPECDEC_BF16 && (ab.ll || ab.counters)) return hipSuccess;  // combined by the blocks
   if (ab.kv.dtype == SPECDEC_BF16 && ab.n_split <= kCombineMaxSplits) {
     switch (ab.head_dim) {
       case 32: hipLaunchKernelGGL((attn_combine_wave_kernel<32>), dim3(ab.n_heads, ab.M), dim3(64), 0, s, ab); break;

@@ -159,6 +159,7 @@ struct RowDesc {
 constexpr int32_t kStatusKvCapacity = -3;
 constexpr int32_t kStatusNonFinite = -4;
 constexpr int32_t kStatusBadToken = -7;
+constexpr int32_t kStatusWaitExpired = -9;
 
 __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {
   if (status) atomicCAS(status, 0, code);

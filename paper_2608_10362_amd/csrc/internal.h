@@ -166,9 +166,17 @@ struct AttnArgs {
   int stt;
   int32_t* status;
   int seq_bound;         // 1: bound each sequence's keys by its own last row (batches of several sequences)
-  // bf16: one counter per (sequence, query tile, kv head), zero between launches;
-  // the last block of a (sequence, tile, head) to finish combines the parts
-  // (null: a separate combine kernel does).
+  // bf16 in-kernel combine (all null: a separate combine kernel adds the
+  // parts).  epochs: one word per (sequence, query tile, kv head), zero at
+  // first use; a launch reads e and tags every partial word it writes with
+  // e + 1 (never 0), and the combining block stores e + 1 once it has read
+  // every part.  ll: [M, h, parts <= kLlMaxParts, hd + 2] tagged words, zero
+  // at first use: low half the float (hd O values, then max and sum), high
+  // half the tag.  counters (one-round launches): one word per (sequence,
+  // query tile, kv head), zero between launches; the last block to count
+  // combines.
+  uint32_t* epochs;
+  uint64_t* ll;
   uint32_t* counters;
   // Or null: the weights the next launch streams (the O projection's image,
   // next_w_bytes long).  With the in-kernel combine, every block that does not
@@ -179,8 +187,11 @@ struct AttnArgs {
   uint32_t next_w_bytes;
 };
 constexpr uint32_t kNextWeightsPerBlock = 48u << 10;
-// Counters a model workspace holds for the attention's in-kernel combine.
+constexpr int kLlMaxParts = 64;  // parts of one head the in-kernel combine takes (one per lane)
+// Epoch words a model workspace holds for the attention's in-kernel combine.
 size_t attention_counter_count(int n_heads, int n_kv_heads, int max_rows);
+// Flagged partial words (uint64) of the in-kernel combine for max_rows rows.
+size_t attention_ll_words(int n_heads, int head_dim, int max_rows, int n_split_max);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s);
 int attention_chunk(int dtype, int head_dim);  // keys per split of the attention kernel
 int device_compute_units();                    // CUs of the current device (cached)
