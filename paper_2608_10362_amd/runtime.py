@@ -328,7 +328,7 @@ class SwitchingRunner:
         sd = self.sd
         active = None
         if self.mode == "memspec":
-            # Alg. 3, lines 2-5: rank with the first prediction, load the initial draft, prepare the cache
+            # Alg. 3, set-up: rank with the first prediction, load the initial draft, prepare the cache
             first = CachePolicy.ranking(scores[0])[0]
             self.policy.state[first] = "loading"
             self.slots[0].load_async(first, self.layers[first], self.copy)
