@@ -370,6 +370,56 @@ def test_bf16_7b_shape_long_context_looping_attention():
     _bf16_case(synth.LLAMA_7B, 1, [4500, 6100], g=4, seed=4)
 
 
+def test_bf16_7b_shape_attention_combine_modes_alternate_on_one_handle():
+    # One model handle, two caches: 2 sequences of 4500 and 6100 keys (looping
+    # attention: the fixed combining block polls tagged partial words, and the
+    # launch advances the per-(sequence, tile, kv head) epochs) and one of 2048
+    # keys (one-round attention: the last block to count combines).  Verifies
+    # alternate between the two several times; every repeat of a verify from the
+    # same state must give the same logits bit for bit, and the first of each
+    # must match the oracle.
+    torch = torch_cuda()
+    shape, n_layers, g = synth.LLAMA_7B, 1, 4
+    W = synth.make_weights(shape, n_layers=n_layers)
+    dw = binding.DeviceWeights(shape, W)
+    cases = [[4500, 6100], [2048]]
+    cap = int(np.ceil((max(max(c) for c in cases) + g + 1) / 64) * 64)
+    target = binding.Model(dw, n_layers, max_rows=2 * (g + 1), max_ctx=cap)
+    m = om.Model(shape, W, n_layers=n_layers)
+    setups = []
+    for ci, lengths in enumerate(cases):
+        B = len(lengths)
+        ctx = synth.make_kv_context(shape, n_layers, lengths, seed=40 + ci)
+        kv = binding.KVCache(target, B, cap)
+        install_context(kv, ctx, lengths, n_layers, shape.dtype)
+        pend = synth.make_prompt(1, shape.vocab, batch=B, seed=50 + ci)[:, 0]
+        drafts = synth.make_prompt(g, shape.vocab, batch=B, seed=60 + ci)
+        setups.append((lengths, ctx, kv, pend, drafts))
+
+    def verify(ci):
+        lengths, _, kv, pend, drafts = setups[ci]
+        B = len(lengths)
+        kv.set_state(np.asarray(lengths, np.int32), np.stack([np.zeros(B, np.int32), pend], 1), np.ones(B, np.int32))
+        logits = torch.empty((B, g + 1, shape.vocab), dtype=torch.float32, device="cuda")
+        binding.specdec_verify(target, kv, g, i32(drafts), g, logits)
+        out = logits.cpu().numpy()
+        assert kv.read_state()["status"] == 0
+        return out
+
+    first = [verify(0), verify(1)]
+    for ci, (lengths, ctx, _, pend, drafts) in enumerate(setups):
+        caches = oracle_caches(shape, n_layers, ctx, lengths, cap)
+        for b in range(len(lengths)):
+            ref = m.forward_block([int(pend[b])] + list(drafts[b]), int(lengths[b]), caches[b])
+            err = float(np.abs(first[ci][b] - ref).max())
+            log(f"case {ci} seq {b} ctx {lengths[b]}: max-abs logit error {err:.3g}")
+            assert err < TOL_BF16
+    for rep in range(3):
+        for ci in (0, 1, 0):
+            got = verify(ci)
+            assert np.array_equal(got, first[ci]), (rep, ci)
+
+
 def test_bf16_7b_shape_long_context_workload_launch_and_accept():
     # The exact launch of the 16-sequence long-context workload: contexts drawn
     # from U[1024, 8192] with the lengths seed (up to 8022 keys), gamma 6 (112
