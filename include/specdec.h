@@ -2,7 +2,7 @@
  * specdec.h -- C ABI of the MI355X (gfx950) speculative-decoding hot path.
  *
  * One draft-and-verify iteration (the inner loop of the MemSpec runtime,
- * Sec. 3.4, Alg. 3: "run draft d_i; verify with target model"):
+ * Sec. 3.4, Alg. 3: the active draft proposes, then the target verifies):
  *
  *   for s in 0..gamma-1: specdec_draft_step(draft, draft_kv, ..., slot = s)
  *   specdec_verify(target, target_kv, ...)      -- one target pass over gamma+1 tokens
@@ -252,8 +252,8 @@ SPECDEC_API specdec_status specdec_prefill(const specdec_model* model, specdec_k
 
 /* Draft single-token decode step at draft slot `slot` (0 <= slot < gamma):
  * the draft model proposing one candidate token per sequence, the first half
- * of a draft-and-verify iteration (Sec. 2.1; Alg. 3, "run draft d_i", run
- * gamma times per iteration).
+ * of a draft-and-verify iteration (Sec. 2.1; Alg. 3, the active draft's
+ * proposal step, run gamma times per iteration).
  *
  *  slot 0 processes the cache's 1 or 2 pending tokens (2 after an iteration
  *  that accepted every draft), slot s > 0 processes d_out[b*ld_d + s-1].
@@ -277,7 +277,7 @@ SPECDEC_API specdec_status specdec_draft_step(const specdec_model* draft, specde
                                   float* logits_out, void* stream);
 
 /* Target verify pass (Sec. 2.1: the target model checks the drafted
- * candidates; Alg. 3, "verify with target model"): one forward over the
+ * candidates; Alg. 3, the verification step): one forward over the
  * gamma+1 tokens
  * [pending token, d[b*ld_d + 0 .. gamma-1]] at positions len[b] .. len[b]+gamma,
  * causal inside the block, against the resident cache (the drafted tokens'
@@ -366,8 +366,8 @@ SPECDEC_API const uint64_t* specdec_kv_step_word(const specdec_kv* kv);
 /* ---------------------------------------------------------------- draft reload
  * Only K drafts stay resident; the others live in backing storage and are
  * loaded asynchronously, overlapped with decoding, and the runtime never
- * waits for a draft that is still loading (Sec. 3.3, Alg. 2 "asynchronously
- * prefetch d"; Sec. 3.4, Alg. 3).  On one GPU: the backing storage is pinned
+ * waits for a draft that is still loading (Sec. 3.3, Alg. 2, its background
+ * prefetch of a predicted draft; Sec. 3.4, Alg. 3).  On one GPU: the backing storage is pinned
  * host memory holding a packed image, a resident slot is a device buffer in
  * the packed-image format, and a load is an H2D copy on a side stream whose
  * completion an event records.  A draft model created over the slot may run
