@@ -202,22 +202,23 @@ def read_ceiling(sizes_mib=(64, 256, 1024, 4096), buf_gib=8, reps=5):
 
 # ---------------------------------------------------------------- CPU oracle baseline
 def cpu_baseline(shape, ctx, gamma):
-    """The oracle's verify pass on the host: time 1 and 2 layers (+ final norm and
-    LM head) of the 7B shape at the same context, extrapolate the per-layer time to
-    all layers."""
+    """The oracle's verify pass on the host: time 2 and 6 layers (+ final norm and
+    LM head) of the 7B shape at the same context, five runs each (about 10 s of
+    oracle time), and extrapolate the per-layer time to all layers."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import model as om
     from paper_2608_10362_amd import synth
 
-    W = synth.make_weights(shape, n_layers=2, threads=min(16, os.cpu_count() or 1))
-    ctxkv = synth.make_kv_context(shape, 2, [ctx], threads=min(16, os.cpu_count() or 1))
+    L0, L1, runs = 2, 6, 5
+    W = synth.make_weights(shape, n_layers=L1, threads=min(16, os.cpu_count() or 1))
+    ctxkv = synth.make_kv_context(shape, L1, [ctx], threads=min(16, os.cpu_count() or 1))
     toks = [int(t) for t in synth.make_prompt(gamma + 1, shape.vocab)[0]]
     times = {}
-    for L in (1, 2):
+    for L in (L0, L1):
         best = []
-        for _ in range(2):
+        for _ in range(runs):
             c = om.KVCache(shape, L, ctx + gamma + 1)
             for l in range(L):
                 c.load(l, ctxkv[l][0]["k"], ctxkv[l][0]["v"])
@@ -227,15 +228,15 @@ def cpu_baseline(shape, ctx, gamma):
             m.forward_block(toks, ctx, c)
             best.append(time.perf_counter() - t0)
         times[L] = float(np.median(best))
-    t_layer = max(times[2] - times[1], 1e-9)
-    t_rest = max(times[1] - t_layer, 0.0)
+    t_layer = max((times[L1] - times[L0]) / (L1 - L0), 1e-9)
+    t_rest = max(times[L0] - L0 * t_layer, 0.0)
     t_full = t_rest + shape.n_layers * t_layer
     threads = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
     return {"value": (gamma + 1) / t_full, "unit": "tokens/s", "cores": int(max(threads) if threads else 1),
             "kind": "oracle",
-            "sample": (f"float64 numpy oracle verify pass (gamma={gamma}, ctx {ctx}) over 1 and 2 layers of the "
-                       f"7B shape + LM head, median of 2 runs each ({times[1]:.2f} s, {times[2]:.2f} s); per-layer "
-                       f"time x {shape.n_layers} layers -> {t_full:.1f} s per verify step")}
+            "sample": (f"float64 numpy oracle verify pass (gamma={gamma}, ctx {ctx}) over {L0} and {L1} layers of the "
+                       f"7B shape + LM head, median of {runs} runs each ({times[L0]:.2f} s, {times[L1]:.2f} s); "
+                       f"per-layer time x {shape.n_layers} layers -> {t_full:.1f} s per verify step")}
 
 
 # ---------------------------------------------------------------- draft reload
