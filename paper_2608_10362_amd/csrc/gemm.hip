@@ -1347,6 +1347,40 @@ __global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_spl
   if ((tid & 31) == 0 && m < M) a.ss_out[(size_t)blockIdx.x * a.ss_ld + m] = t;
 }
 
+// Sum of the split-K partial sums of a wide pass's Q|K|V projections in split
+// order, times the row's RMSNorm scale (its partial sums of squares added in
+// order), stored with the Q and K columns back in natural order for
+// rope_append_kernel.  Block = 128 columns x 8 rows; thread = 4 columns of one row.
+__global__ __launch_bounds__(256) void qkv_reduce_kernel(GemmArgs a, int n_split) {
+  __shared__ float s_scale[8];
+  const int tid = threadIdx.x, m = (int)blockIdx.y * 8 + (tid >> 5);
+  const int n = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
+  const int M = a.M;
+  if (tid < 8) {
+    const int mr = (int)blockIdx.y * 8 + tid;
+    float ss = 0.f;
+    if (a.ss_in && mr < M)
+      for (int p = 0; p < a.n_ss; ++p) ss += a.ss_in[(size_t)p * a.ss_ld + mr];
+    s_scale[tid] = a.ss_in ? 1.0f / sqrtf(ss / (float)a.K + a.eps) : 1.0f;
+  }
+  __syncthreads();
+  if (m >= M || n >= a.n_rows) return;
+  f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < n_split; ++s) y += *(const f32x4*)(a.ypart + ((size_t)s * M + m) * a.n_rows + n);
+  const float sc = s_scale[tid >> 5];
+  const int hd = a.head_dim, nqk = a.n_seg[0] + a.n_seg[1];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int nn = n + e;
+    int col = nn;
+    if (nn < nqk) {  // (Q and K columns come in the packed RoPE order, as the tile kernel's store)
+      const int base = nn >= a.n_seg[0] ? a.n_seg[0] : 0, r = nn - base, w = r % hd, tq = w >> 4, ec = w & 15;
+      col = base + (r / hd) * hd + (ec < 8 ? 8 * tq + ec : hd / 2 + 8 * tq + ec - 8);
+    }
+    a.out[(size_t)m * a.ldo + col] = y[e] * sc;
+  }
+}
+
 // ---------------------------------------------------------------- tile MFMA kernel (bf16 weights, 129+ rows)
 // Launches of more than 128 rows (prefill chunks, up to 4 row tiles of 256 per
 // launch, row tiles adjacent in the grid so the blocks sharing a weight
@@ -1870,11 +1904,33 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       else launch_wide_t<1, EPI_STORE>(a, blocks, KS, 1, s);
       break;
     }
-    case EPI_QKV:
+    case EPI_QKV: {
       if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
         return hipErrorInvalidValue;
-      launch_wide_t<1, EPI_QKV>(a, (a.n_rows + 63) / 64, KS, 1, s);
-      break;
+      // Two tiles per wave over a K split that keeps the grid within the CUs:
+      // raw partial sums, then qkv_reduce_kernel (row scale, natural column
+      // order) and rope_append_kernel.
+      const int blocks = (a.n_rows + 127) / 128;
+      int n_split = std::min({kWideSplitMax, KS, std::max(1, cus / blocks)});
+      const int ks_per_split = (KS + n_split - 1) / n_split;
+      n_split = (KS + ks_per_split - 1) / ks_per_split;
+      if (!a.ypart || !a.out || a.ldo < a.n_rows || a.n_rows % 4 ||
+          (size_t)n_split * a.M * a.n_rows > wide_ypart_floats(a.K)) {
+        launch_wide_t<1, EPI_QKV>(a, (a.n_rows + 63) / 64, KS, 1, s);
+        break;
+      }
+      GemmArgs p = a;
+      p.kind = EPI_RESID;
+      launch_wide_t<2, EPI_RESID>(p, blocks, ks_per_split, n_split, s);
+      hipLaunchKernelGGL(qkv_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8), dim3(256), 0,
+                         s, a, n_split);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      AttnArgs r{};
+      r.rows = a.rows; r.M = a.M; r.rps = a.M; r.n_heads = a.n_heads; r.n_kv_heads = a.n_kv_heads;
+      r.head_dim = a.head_dim; r.qkv = a.out; r.rope_cs = a.rope_cs; r.qr = a.qr; r.kv = a.kv; r.layer = a.layer;
+      return launch_rope_append(r, s);
+    }
     case EPI_SWIGLU: launch_wide_t<2, EPI_SWIGLU>(a, (a.n_rows + 63) / 64, KS, 1, s); break;
     case EPI_RESID: {
       if (!a.ypart) return hipErrorInvalidValue;
