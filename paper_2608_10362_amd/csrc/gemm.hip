@@ -1026,7 +1026,11 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
 // in register rings.  The groups' sums are added in group order in LDS; the
 // epilogues (store, SwiGLU, QKV with RoPE) then read the accumulators in
 // place.  Residual GEMMs (O, down: few row tiles) split K over the grid and
-// write partial sums, which resid_reduce_kernel adds in a fixed order.
+// write partial sums, which resid_reduce_kernel adds in a fixed order; Q|K|V
+// and gate|up do the same with three tiles per wave, their partial sums added
+// by qkv_reduce_kernel (then RoPE and the KV append in rope_append_kernel) and
+// swiglu_reduce_kernel.  (With three tiles per wave the x ring holds two slabs,
+// and the groups' sums go through the slab buffers one tile at a time.)
 constexpr int kWideGroups = 2;
 constexpr int kWideThreads = 256 * kWideGroups;
 constexpr int kWideRows = 128;  // rows per launch of the wide kernel
@@ -1038,7 +1042,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
   constexpr int G = kWideGroups;
   constexpr int MP = 16 * MT, NC = 64 * T;
   constexpr int D = T == 1 ? 8 : 4;                  // weight k-steps in flight per wave
-  constexpr int XR = 4;                              // x slabs in flight per group
+  constexpr int XR = T >= 3 ? 2 : 4;                 // x slabs in flight per group (registers: T >= 3)
   constexpr int PJ = (MP * 4 + 255) / 256;           // 32-byte x pieces per thread per slab
   constexpr int MTP = PJ * 256 / 64;                 // m tiles the pieces cover (>= MT; extra rows read zeros)
   constexpr bool QKV = KIND == EPI_QKV, SCALE = KIND != EPI_RESID;
@@ -1048,7 +1052,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
   static_assert(!QKV || T == 1, "the QKV epilogue tables cover one tile per wave");
   static_assert(D % XR == 0, "the unrolled step loop indexes both rings statically");
   static_assert(MP % (4 * G) == 0, "row-scale rows split evenly over the waves");
-  static_assert((G - 1) * 4 * T * MT <= G * 2 * MTP * 2, "group sums fit in the slab buffers");
+  static_assert(4 * MT <= G * 2 * MTP * 2, "one tile's group sums fit in the slab buffers");
   __shared__ u32x4 s_a[G][2][MTP][2][kWave];  // [group][buffer][m tile][hi, lo][lane]
   __shared__ float scale[MP];
   __shared__ f32x4 s_cs[QKV ? 4 : 1][QKV ? MP : 1][4];  // per tile wave, per row: cos of its 8 dims, then sin
@@ -1232,7 +1236,25 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
 
   // Group sums: groups 1.. park theirs in the (now free) slab buffers, group 0
   // adds them in group order and runs the epilogue.
-  if constexpr (G > 1) {
+  if constexpr (G > 1 && (G - 1) * 4 * T * MT > G * 2 * MTP * 2) {
+    // (too many for the slab buffers at once: one tile at a time)
+    static_assert(G == 2, "tile-at-a-time group sums: two groups");
+    floatx4* park = reinterpret_cast<floatx4*>(&s_a[0][0][0][0][0]);
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      if (grp > 0) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) park[(wl * MT + mt) * kWave + lane] = acc[t][mt];
+      }
+      __syncthreads();
+      if (grp == 0) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] += park[(wl * MT + mt) * kWave + lane];
+      }
+      __syncthreads();
+    }
+    if (grp > 0) return;
+  } else if constexpr (G > 1) {
     floatx4* park = reinterpret_cast<floatx4*>(&s_a[0][0][0][0][0]);
     if (grp > 0) {
 #pragma unroll
@@ -1345,6 +1367,36 @@ __global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_spl
 #pragma unroll
   for (int o = 16; o > 0; o >>= 1) t += __shfl_xor(t, o, kWave);
   if ((tid & 31) == 0 && m < M) a.ss_out[(size_t)blockIdx.x * a.ss_ld + m] = t;
+}
+
+// Sum of the split-K partial sums of a wide pass's gate and up projections
+// (rows [0, F) and [F, 2F) of the partials) in split order, times the row's
+// RMSNorm scale, then SwiGLU.  Block = 128 columns x 8 rows; thread = 4 columns of one row.
+__global__ __launch_bounds__(256) void swiglu_reduce_kernel(GemmArgs a, int n_split) {
+  __shared__ float s_scale[8];
+  const int tid = threadIdx.x, m = (int)blockIdx.y * 8 + (tid >> 5);
+  const int f = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
+  const int M = a.M, F = a.n_rows, W = 2 * F;
+  if (tid < 8) {
+    const int mr = (int)blockIdx.y * 8 + tid;
+    float ss = 0.f;
+    if (a.ss_in && mr < M)
+      for (int p = 0; p < a.n_ss; ++p) ss += a.ss_in[(size_t)p * a.ss_ld + mr];
+    s_scale[tid] = a.ss_in ? 1.0f / sqrtf(ss / (float)a.K + a.eps) : 1.0f;
+  }
+  __syncthreads();
+  if (m >= M || f >= F) return;
+  f32x4 gs = f32x4{0.f, 0.f, 0.f, 0.f}, us = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < n_split; ++s) {
+    const float* yp = a.ypart + ((size_t)s * M + m) * W;
+    gs += *(const f32x4*)(yp + f);
+    us += *(const f32x4*)(yp + F + f);
+  }
+  const float sc = s_scale[tid >> 5];
+  f32x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = silu_f(gs[e] * sc) * (us[e] * sc);
+  *(f32x4*)(a.out + (size_t)m * a.ldo + f) = o;
 }
 
 // Sum of the split-K partial sums of a wide pass's Q|K|V projections in split
@@ -1907,10 +1959,14 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
     case EPI_QKV: {
       if (a.kv.dtype != SPECDEC_BF16 || a.head_dim % 16 || a.n_seg[0] % a.head_dim || a.n_seg[1] % a.head_dim)
         return hipErrorInvalidValue;
-      // Two tiles per wave over a K split that keeps the grid within the CUs:
-      // raw partial sums, then qkv_reduce_kernel (row scale, natural column
-      // order) and rope_append_kernel.
-      const int blocks = (a.n_rows + 127) / 128;
+      // Three tiles per wave over a K split that keeps the grid within the
+      // CUs (the 7B shape: 64 column blocks x 4 splits): raw partial sums,
+      // then qkv_reduce_kernel (row scale, natural column order) and
+      // rope_append_kernel.  The wide kernel's time follows its k-steps per
+      // block more than its products per k-step, so fewer k-steps per block
+      // pay for the extra launches (config 5: 16.53 -> 15.16 ms on one box
+      // together with the SwiGLU split, one tile per wave and no split before).
+      const int blocks = (a.n_rows + 191) / 192;
       int n_split = std::min({kWideSplitMax, KS, std::max(1, cus / blocks)});
       const int ks_per_split = (KS + n_split - 1) / n_split;
       n_split = (KS + ks_per_split - 1) / ks_per_split;
@@ -1921,7 +1977,7 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       }
       GemmArgs p = a;
       p.kind = EPI_RESID;
-      launch_wide_t<2, EPI_RESID>(p, blocks, ks_per_split, n_split, s);
+      launch_wide_t<3, EPI_RESID>(p, blocks, ks_per_split, n_split, s);
       hipLaunchKernelGGL(qkv_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8), dim3(256), 0,
                          s, a, n_split);
       hipError_t e = hipGetLastError();
@@ -1931,7 +1987,28 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       r.head_dim = a.head_dim; r.qkv = a.out; r.rope_cs = a.rope_cs; r.qr = a.qr; r.kv = a.kv; r.layer = a.layer;
       return launch_rope_append(r, s);
     }
-    case EPI_SWIGLU: launch_wide_t<2, EPI_SWIGLU>(a, (a.n_rows + 63) / 64, KS, 1, s); break;
+    case EPI_SWIGLU: {
+      // The gate and up rows as one 2F-row matrix, three tiles per wave, K
+      // split within the CUs: raw partial sums, then swiglu_reduce_kernel.
+      const int W = 2 * a.n_rows, blocks = (W + 191) / 192;
+      int n_split = std::min({kWideSplitMax, KS, std::max(1, cus / blocks)});
+      const int ks_per_split = (KS + n_split - 1) / n_split;
+      n_split = (KS + ks_per_split - 1) / ks_per_split;
+      if (n_split < 2 || !a.ypart || a.n_rows % 16 || a.ldo % 4 || (size_t)n_split * a.M * W > wide_ypart_floats(a.K)) {
+        launch_wide_t<2, EPI_SWIGLU>(a, (a.n_rows + 63) / 64, KS, 1, s);
+        break;
+      }
+      GemmArgs p = a;
+      p.kind = EPI_RESID;
+      p.n_rows = W;
+      p.n_seg[0] = a.n_rows;
+      p.n_seg[1] = a.n_rows;
+      p.n_seg[2] = 0;
+      launch_wide_t<3, EPI_RESID>(p, blocks, ks_per_split, n_split, s);
+      hipLaunchKernelGGL(swiglu_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8), dim3(256),
+                         0, s, a, n_split);
+      break;
+    }
     case EPI_RESID: {
       if (!a.ypart) return hipErrorInvalidValue;
       // Two tiles per wave (each x slab serves 128 columns) and K split until the
