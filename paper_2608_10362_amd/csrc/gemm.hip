@@ -1868,7 +1868,7 @@ bool gemm_wide(int dtype, int M) { return dtype == SPECDEC_BF16 && M > kMaxGemmR
 int gemm_launch_rows(int dtype, int M) {
   return !gemm_wide(dtype, M) ? kMaxGemmRows : (M > kWideRows ? kTileLaunchRows : kWideRows);
 }
-constexpr int kWideSplitMax = 8;
+constexpr int kWideSplitMax = 12;
 size_t wide_ypart_floats(int n_rows) {
   return (size_t)std::max(kWideSplitMax * kWideRows, kTilePartialRows) * n_rows;
 }
@@ -2011,16 +2011,18 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
     }
     case EPI_RESID: {
       if (!a.ypart) return hipErrorInvalidValue;
-      // Two tiles per wave (each x slab serves 128 columns) and K split until the
-      // grid covers the CUs (each split at least one k-step): the 7B O and down
-      // projections over 112 rows run 32 column blocks x 8 splits.  (One tile per
-      // wave and 4 splits: config 5 verify 17.10 -> 16.50 ms on one box.)
-      const int blocks = (a.n_rows + 127) / 128;
-      int n_split = std::min(kWideSplitMax, std::max(1, (cus + blocks - 1) / blocks));
+      // Three tiles per wave (each x slab serves 192 columns) and K split as far
+      // as the grid stays within the CUs (each split at least one k-step): the
+      // 7B O and down projections over 112 rows run 22 column blocks x 11
+      // splits.  (One tile per wave and 4 splits, then two tiles and 8 splits:
+      // config 5 verify 17.10 -> 16.50 ms, then 15.46-15.71 -> 15.11-15.25 ms,
+      // each on one box.)
+      const int blocks = (a.n_rows + 191) / 192;
+      int n_split = std::min(kWideSplitMax, std::max(1, cus / blocks));
       n_split = std::min(n_split, KS);
       const int ks_per_split = (KS + n_split - 1) / n_split;
       n_split = (KS + ks_per_split - 1) / ks_per_split;
-      launch_wide_t<2, EPI_RESID>(a, blocks, ks_per_split, n_split, s);
+      launch_wide_t<3, EPI_RESID>(a, blocks, ks_per_split, n_split, s);
       hipLaunchKernelGGL(resid_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8),
                          dim3(256), 0, s, a, n_split);
       break;
