@@ -1036,6 +1036,7 @@ constexpr int kWideThreads = 256 * kWideGroups;
 constexpr int kWideRows = 128;  // rows per launch of the wide kernel
 constexpr int kWideCols = 128;  // columns per block of the split-K reduction (and per ss partial)
 constexpr int kWideMaxSs = 64;  // ss partials a wide launch sums (one per lane)
+constexpr int kWideSplitMax = 12;  // K splits of a wide launch's partial sums
 
 template <int MT, int T, int KIND>
 __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int ks_per_split, int n_split) {
@@ -1344,6 +1345,52 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
   }
 }
 
+// Split-K partial sums of 4 columns of one row, added in split order; every
+// split's load is issued before the first add (the split index is clamped, so
+// loads past n_split re-read the last split and are not added).
+template <int NS>
+__device__ __forceinline__ f32x4 sum_splits_n(const float* yp, size_t split_stride, int n_split) {
+  f32x4 v[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) v[s] = *(const f32x4*)(yp + (size_t)min(s, n_split - 1) * split_stride);
+  f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < n_split) y += v[s];
+  return y;
+}
+__device__ __forceinline__ f32x4 sum_splits(const float* yp, size_t split_stride, int n_split) {
+  if (n_split <= 4) return sum_splits_n<4>(yp, split_stride, n_split);  // (block-uniform)
+  if (n_split <= 8) return sum_splits_n<8>(yp, split_stride, n_split);
+  return sum_splits_n<kWideSplitMax>(yp, split_stride, n_split);
+}
+
+// RMSNorm scales of rows m0 .. m0+7 into s_scale: the block loads every
+// partial sum of squares at once (two per thread), then thread r < 8 adds its
+// row's in partial order.
+__device__ __forceinline__ void row_scales8(const GemmArgs& a, int m0, float* s_scale, float (*s_ss)[kWideMaxSs]) {
+  const int tid = threadIdx.x;
+  float v[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + 256 * k, r = i / kWideMaxSs, p = i % kWideMaxSs, m = m0 + r;
+    v[k] = a.ss_in && p < a.n_ss && m < a.M ? a.ss_in[(size_t)p * a.ss_ld + m] : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + 256 * k;
+    s_ss[i / kWideMaxSs][i % kWideMaxSs] = v[k];
+  }
+  __syncthreads();
+  if (tid < 8) {
+    float ss = 0.f;
+    for (int p = 0; p < a.n_ss; ++p) ss += s_ss[tid][p];
+    s_scale[tid] = a.ss_in ? 1.0f / sqrtf(ss / (float)a.K + a.eps) : 1.0f;
+  }
+  __syncthreads();
+}
+static_assert(8 * kWideMaxSs == 512, "row_scales8: two partials per thread of a 256-thread block");
+
 // Sum of the split-K partials of a residual GEMM in split order, residual
 // add, next RMSNorm input and its sums of squares.  Block = 128 columns x 8
 // rows; thread = 4 columns of one row; ss partial p = column block p.
@@ -1353,8 +1400,7 @@ __global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_spl
   const int M = a.M;
   float t = 0.f;
   if (m < M && n < a.n_rows) {
-    f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < n_split; ++s) y += *(const f32x4*)(a.ypart + ((size_t)s * M + m) * a.n_rows + n);
+    const f32x4 y = sum_splits(a.ypart + (size_t)m * a.n_rows + n, (size_t)M * a.n_rows, n_split);
     float* hp = a.out + (size_t)m * a.ldo + n;
     const f32x4 h = *(const f32x4*)hp + y;
     *(f32x4*)hp = h;
@@ -1374,24 +1420,14 @@ __global__ __launch_bounds__(256) void resid_reduce_kernel(GemmArgs a, int n_spl
 // RMSNorm scale, then SwiGLU.  Block = 128 columns x 8 rows; thread = 4 columns of one row.
 __global__ __launch_bounds__(256) void swiglu_reduce_kernel(GemmArgs a, int n_split) {
   __shared__ float s_scale[8];
+  __shared__ float s_ss[8][kWideMaxSs];
   const int tid = threadIdx.x, m = (int)blockIdx.y * 8 + (tid >> 5);
   const int f = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
   const int M = a.M, F = a.n_rows, W = 2 * F;
-  if (tid < 8) {
-    const int mr = (int)blockIdx.y * 8 + tid;
-    float ss = 0.f;
-    if (a.ss_in && mr < M)
-      for (int p = 0; p < a.n_ss; ++p) ss += a.ss_in[(size_t)p * a.ss_ld + mr];
-    s_scale[tid] = a.ss_in ? 1.0f / sqrtf(ss / (float)a.K + a.eps) : 1.0f;
-  }
-  __syncthreads();
+  row_scales8(a, (int)blockIdx.y * 8, s_scale, s_ss);
   if (m >= M || f >= F) return;
-  f32x4 gs = f32x4{0.f, 0.f, 0.f, 0.f}, us = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < n_split; ++s) {
-    const float* yp = a.ypart + ((size_t)s * M + m) * W;
-    gs += *(const f32x4*)(yp + f);
-    us += *(const f32x4*)(yp + F + f);
-  }
+  const float* yp = a.ypart + (size_t)m * W;
+  const f32x4 gs = sum_splits(yp + f, (size_t)M * W, n_split), us = sum_splits(yp + F + f, (size_t)M * W, n_split);
   const float sc = s_scale[tid >> 5];
   f32x4 o;
 #pragma unroll
@@ -1405,20 +1441,13 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(GemmArgs a, int n_sp
 // rope_append_kernel.  Block = 128 columns x 8 rows; thread = 4 columns of one row.
 __global__ __launch_bounds__(256) void qkv_reduce_kernel(GemmArgs a, int n_split) {
   __shared__ float s_scale[8];
+  __shared__ float s_ss[8][kWideMaxSs];
   const int tid = threadIdx.x, m = (int)blockIdx.y * 8 + (tid >> 5);
   const int n = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
   const int M = a.M;
-  if (tid < 8) {
-    const int mr = (int)blockIdx.y * 8 + tid;
-    float ss = 0.f;
-    if (a.ss_in && mr < M)
-      for (int p = 0; p < a.n_ss; ++p) ss += a.ss_in[(size_t)p * a.ss_ld + mr];
-    s_scale[tid] = a.ss_in ? 1.0f / sqrtf(ss / (float)a.K + a.eps) : 1.0f;
-  }
-  __syncthreads();
+  row_scales8(a, (int)blockIdx.y * 8, s_scale, s_ss);
   if (m >= M || n >= a.n_rows) return;
-  f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < n_split; ++s) y += *(const f32x4*)(a.ypart + ((size_t)s * M + m) * a.n_rows + n);
+  const f32x4 y = sum_splits(a.ypart + (size_t)m * a.n_rows + n, (size_t)M * a.n_rows, n_split);
   const float sc = s_scale[tid >> 5];
   const int hd = a.head_dim, nqk = a.n_seg[0] + a.n_seg[1];
 #pragma unroll
@@ -1868,7 +1897,6 @@ bool gemm_wide(int dtype, int M) { return dtype == SPECDEC_BF16 && M > kMaxGemmR
 int gemm_launch_rows(int dtype, int M) {
   return !gemm_wide(dtype, M) ? kMaxGemmRows : (M > kWideRows ? kTileLaunchRows : kWideRows);
 }
-constexpr int kWideSplitMax = 12;
 size_t wide_ypart_floats(int n_rows) {
   return (size_t)std::max(kWideSplitMax * kWideRows, kTilePartialRows) * n_rows;
 }
