@@ -1028,7 +1028,7 @@ __global__ __launch_bounds__(kQ4Threads) void gemm_q4_lds(GemmArgs a, int n_unit
 // place.  Residual GEMMs (O, down: few row tiles) split K over the grid and
 // write partial sums, which resid_reduce_kernel adds in a fixed order; Q|K|V
 // and gate|up do the same with three tiles per wave, their partial sums added
-// by qkv_reduce_kernel (then RoPE and the KV append in rope_append_kernel) and
+// by qkv_reduce_kernel (with RoPE, the query store and the KV append) and
 // swiglu_reduce_kernel.  (With three tiles per wave the x ring holds two slabs,
 // and the groups' sums go through the slab buffers one tile at a time.)
 constexpr int kWideGroups = 2;
@@ -1436,9 +1436,13 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(GemmArgs a, int n_sp
 }
 
 // Sum of the split-K partial sums of a wide pass's Q|K|V projections in split
-// order, times the row's RMSNorm scale (its partial sums of squares added in
-// order), stored with the Q and K columns back in natural order for
-// rope_append_kernel.  Block = 128 columns x 8 rows; thread = 4 columns of one row.
+// order, times the row's RMSNorm scale, then RoPE on the Q and K columns and
+// the stores: rotated queries to qr, rotated keys and the values appended to
+// the KV cache (valid rows).  Q and K columns come in the packed RoPE order:
+// column c of a head's 16-column tile tq is dim 8tq + c for c < 8, hd/2 + 8tq
+// + c - 8 otherwise, so each column's rotation partner (c ^ 8) is 8 columns
+// away, in the lane ^ 2 of the row's 32 threads.  Block = 128 columns x 8
+// rows; thread = 4 columns of one row.
 __global__ __launch_bounds__(256) void qkv_reduce_kernel(GemmArgs a, int n_split) {
   __shared__ float s_scale[8];
   __shared__ float s_ss[8][kWideMaxSs];
@@ -1446,19 +1450,39 @@ __global__ __launch_bounds__(256) void qkv_reduce_kernel(GemmArgs a, int n_split
   const int n = (int)blockIdx.x * kWideCols + 4 * (tid & 31);
   const int M = a.M;
   row_scales8(a, (int)blockIdx.y * 8, s_scale, s_ss);
-  if (m >= M || n >= a.n_rows) return;
-  const f32x4 y = sum_splits(a.ypart + (size_t)m * a.n_rows + n, (size_t)M * a.n_rows, n_split);
+  const bool live = m < M && n < a.n_rows;
+  f32x4 y = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (live) y = sum_splits(a.ypart + (size_t)m * a.n_rows + n, (size_t)M * a.n_rows, n_split);
   const float sc = s_scale[tid >> 5];
-  const int hd = a.head_dim, nqk = a.n_seg[0] + a.n_seg[1];
+  f32x4 z;  // (every lane takes part in the shuffles)
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const int nn = n + e;
-    int col = nn;
-    if (nn < nqk) {  // (Q and K columns come in the packed RoPE order, as the tile kernel's store)
-      const int base = nn >= a.n_seg[0] ? a.n_seg[0] : 0, r = nn - base, w = r % hd, tq = w >> 4, ec = w & 15;
-      col = base + (r / hd) * hd + (ec < 8 ? 8 * tq + ec : hd / 2 + 8 * tq + ec - 8);
-    }
-    a.out[(size_t)m * a.ldo + col] = y[e] * sc;
+    y[e] *= sc;
+    z[e] = __shfl_xor(y[e], 2, kWave);
+  }
+  if (!live) return;
+  const int H = a.n_heads, hd = a.head_dim, half = hd >> 1, cap = a.kv.capacity;
+  const int nq = a.n_seg[0], nqk = nq + a.n_seg[1];
+  const RowDesc rd = a.rows[m];
+  if (n >= nqk) {  // values: natural order
+    if (!rd.valid) return;
+    const int r = n - nqk, head = r / hd, w = r % hd;
+    uint16_t* kvb = k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::v(rd.pos, w + e, hd, cap), y[e]);
+    return;
+  }
+  const bool is_q = n < nq;
+  const int r = n - (is_q ? 0 : nq), head = r / hd, w = r % hd, tq = w >> 4;
+  const float* cs = a.rope_cs + (size_t)m * hd;
+  uint16_t* kvb = is_q || !rd.valid ? nullptr : k_block<uint16_t>(a.kv, a.layer, rd.b, head);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int ec = (w & 15) + e, j = 8 * tq + (ec & 7), d = ec < 8 ? j : half + j;
+    const float c = cs[j], sn = cs[half + j];
+    const float out = ec < 8 ? y[e] * c - z[e] * sn : y[e] * c + z[e] * sn;
+    if (is_q) a.qr[((size_t)m * H + head) * hd + d] = out;
+    else if (kvb) Storage<uint16_t>::store(kvb + KvIndex<uint16_t>::k(rd.pos, d, hd, cap), out);
   }
 }
 
@@ -1989,8 +2013,8 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
         return hipErrorInvalidValue;
       // Three tiles per wave over a K split that keeps the grid within the
       // CUs (the 7B shape: 64 column blocks x 4 splits): raw partial sums,
-      // then qkv_reduce_kernel (row scale, natural column order) and
-      // rope_append_kernel.  The wide kernel's time follows its k-steps per
+      // then qkv_reduce_kernel (row scale, RoPE, the query store and the KV
+      // append).  The wide kernel's time follows its k-steps per
       // block more than its products per k-step, so fewer k-steps per block
       // pay for the extra launches (config 5: 16.53 -> 15.16 ms on one box
       // together with the SwiGLU split, one tile per wave and no split before).
@@ -1998,8 +2022,7 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       int n_split = std::min({kWideSplitMax, KS, std::max(1, cus / blocks)});
       const int ks_per_split = (KS + n_split - 1) / n_split;
       n_split = (KS + ks_per_split - 1) / ks_per_split;
-      if (!a.ypart || !a.out || a.ldo < a.n_rows || a.n_rows % 4 ||
-          (size_t)n_split * a.M * a.n_rows > wide_ypart_floats(a.K)) {
+      if (!a.ypart || a.n_rows % 16 || (size_t)n_split * a.M * a.n_rows > wide_ypart_floats(a.K)) {
         launch_wide_t<1, EPI_QKV>(a, (a.n_rows + 63) / 64, KS, 1, s);
         break;
       }
@@ -2008,12 +2031,7 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       launch_wide_t<3, EPI_RESID>(p, blocks, ks_per_split, n_split, s);
       hipLaunchKernelGGL(qkv_reduce_kernel, dim3((a.n_rows + kWideCols - 1) / kWideCols, (a.M + 7) / 8), dim3(256), 0,
                          s, a, n_split);
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      AttnArgs r{};
-      r.rows = a.rows; r.M = a.M; r.rps = a.M; r.n_heads = a.n_heads; r.n_kv_heads = a.n_kv_heads;
-      r.head_dim = a.head_dim; r.qkv = a.out; r.rope_cs = a.rope_cs; r.qr = a.qr; r.kv = a.kv; r.layer = a.layer;
-      return launch_rope_append(r, s);
+      break;
     }
     case EPI_SWIGLU: {
       // The gate and up rows as one 2F-row matrix, three tiles per wave, K
