@@ -1276,17 +1276,29 @@ __global__ __launch_bounds__(kWideThreads) void gemm_bf16_wide(GemmArgs a, int k
   // Epilogue (group 0).  acc[t][mt][r] is row mt*16 + 4*(lane/16) + r, column lane%16 of tile t.
   const int M = a.M, cl = lane & 15, rg = lane >> 4;
   if constexpr (KIND == EPI_RESID) {
+    // Each 16 x 16 accumulator tile goes through a wave-private LDS square
+    // (inside the wave's own part of the group-sum area, which it has read):
+    // lane l then holds 4 consecutive columns of row l/4 and stores them as
+    // one 16-byte write, a quarter of the store instructions of writing each
+    // lane's 4 rows of one column.  (LDS operations of a wave complete in
+    // order; the wave barriers keep the compiler from reordering them.)
     float* yp = a.ypart + (size_t)split * M * a.n_rows;
+    constexpr int PSTRIDE = ((G - 1) * 4 * T * MT > G * 2 * MTP * 2 ? MT : T * MT) * 256;  // floats per wave
+    float* sq = reinterpret_cast<float*>(&s_a[0][0][0][0][0]) + (size_t)wl * PSTRIDE;  // [16][17]
+    const int rr = lane >> 2, c4 = 4 * (lane & 3);
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-      const int n = blk * NC + (wl * T + t) * 16 + cl;
+      const int n0 = blk * NC + (wl * T + t) * 16;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = mt * 16 + 4 * rg + r;
-          if (m < M && n < a.n_rows) yp[(size_t)m * a.n_rows + n] = acc[t][mt][r];
-        }
+        for (int r = 0; r < 4; ++r) sq[(4 * rg + r) * 17 + cl] = acc[t][mt][r];
+        __builtin_amdgcn_wave_barrier();
+        const f32x4 v = f32x4{sq[rr * 17 + c4], sq[rr * 17 + c4 + 1], sq[rr * 17 + c4 + 2], sq[rr * 17 + c4 + 3]};
+        __builtin_amdgcn_wave_barrier();
+        const int m = mt * 16 + rr;
+        if (m < M && n0 + c4 < a.n_rows) *(f32x4*)(yp + (size_t)m * a.n_rows + n0 + c4) = v;
+      }
     }
   } else if constexpr (KIND == EPI_STORE) {
 #pragma unroll
@@ -2056,7 +2068,7 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       break;
     }
     case EPI_RESID: {
-      if (!a.ypart) return hipErrorInvalidValue;
+      if (!a.ypart || a.n_rows % 16) return hipErrorInvalidValue;
       // Three tiles per wave (each x slab serves 192 columns) and K split as far
       // as the grid stays within the CUs (each split at least one k-step): the
       // 7B O and down projections over 112 rows run 22 column blocks x 11
