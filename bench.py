@@ -408,12 +408,12 @@ def verify_bytes_ragged(shape, lengths, gamma):
 
 
 CONFIGS = {
-    1: dict(desc="tiny float32 (L=2, d=128, 4x32 MHA, F=512, V=512), 1-layer draft, 64-token prompt",
+    1: dict(metric_name="tiny float32 model", desc="tiny float32 (L=2, d=128, 4x32 MHA, F=512, V=512), 1-layer draft, 64-token prompt",
             shape="TINY", batch=1, gamma=4, prompt=64, temperature=1.0, draft_layers=1, generate=32),
-    2: dict(desc="1.1B-shaped bf16 (L=22, d=2048, 32q/4kv x 64, F=5632, V=32000), 4-layer draft, "
+    2: dict(metric_name="1.1B-shaped, batch 1", desc="1.1B-shaped bf16 (L=22, d=2048, 32q/4kv x 64, F=5632, V=32000), 4-layer draft, "
                  "512-token prompt", shape="LLAMA_1B", batch=1, gamma=4, prompt=512, temperature=1.0,
             draft_layers=4, generate=256),
-    5: dict(desc="7B-shaped bf16, 16 sequences with resident contexts U[1024, 8192] (seed 4), 4-layer draft",
+    5: dict(metric_name="7B-shaped, 16 long-context sequences", desc="7B-shaped bf16, 16 sequences with resident contexts U[1024, 8192] (seed 4), 4-layer draft",
             shape="LLAMA_7B", batch=16, gamma=6, lengths=(1024, 8192), temperature=0.8, draft_layers=4),
 }
 
@@ -480,7 +480,7 @@ def run_config(args):
     vbytes = verify_bytes_ragged(shape, lengths, g)
     gbps = vbytes / (tm["verify_ms"] * 1e-3) / 1e9
     result = {
-        "metric": f"verify-step tokens/s (config {args.config})", "value": round(B * (g + 1) / (tm["verify_ms"] * 1e-3), 2),
+        "metric": f"verify-step tokens/s ({cfg['metric_name']})", "value": round(B * (g + 1) / (tm["verify_ms"] * 1e-3), 2),
         "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(tm["step_ms"], 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if shape.dtype == "bf16" else "f32", "data": "synthetic",
@@ -496,7 +496,7 @@ def run_config(args):
     print(json.dumps(result), flush=True)
 
 
-# ---------------------------------------------------------------- config 4: draft switching
+# ---------------------------------------------------------------- draft switching
 def run_switching(args):
     """Draft switching on the 7B-shaped target (Sec. 3.3-3.4 on one GPU): drafts
     of 2, 4 and 8 layers, context 1024, gamma 4, greedy, scheduling every N = 4
@@ -555,7 +555,7 @@ def run_switching(args):
         del r, target, kv_t
         torch.cuda.empty_cache()
     result = {
-        "metric": "generated tokens/s under draft switching (config 4)", "value": out["memspec"]["tokens_per_s"],
+        "metric": "generated tokens/s under draft switching (7B target, 2/4/8-layer drafts)", "value": out["memspec"]["tokens_per_s"],
         "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
         "config": {"workload": "7B-shaped bf16 target, drafts of 2/4/8 layers, context 1024, gamma 4, greedy, "
                                "interval N=4, K=2, Markov schedule stay 0.8 (seed 3), 128 generated tokens",

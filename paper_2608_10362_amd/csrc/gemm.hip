@@ -2028,8 +2028,9 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       // then qkv_reduce_kernel (row scale, RoPE, the query store and the KV
       // append).  The wide kernel's time follows its k-steps per
       // block more than its products per k-step, so fewer k-steps per block
-      // pay for the extra launches (config 5: 16.53 -> 15.16 ms on one box
-      // together with the SwiGLU split, one tile per wave and no split before).
+      // pay for the extra launches (16 long-context 7B sequences, 112 rows per
+      // verify: 16.53 -> 15.16 ms on one box together with the SwiGLU split,
+      // one tile per wave and no split before).
       const int blocks = (a.n_rows + 191) / 192;
       int n_split = std::min({kWideSplitMax, KS, std::max(1, cus / blocks)});
       const int ks_per_split = (KS + n_split - 1) / n_split;
@@ -2073,8 +2074,8 @@ hipError_t launch_wide(const GemmArgs& a, hipStream_t s) {
       // as the grid stays within the CUs (each split at least one k-step): the
       // 7B O and down projections over 112 rows run 22 column blocks x 11
       // splits.  (One tile per wave and 4 splits, then two tiles and 8 splits:
-      // config 5 verify 17.10 -> 16.50 ms, then 15.46-15.71 -> 15.11-15.25 ms,
-      // each on one box.)
+      // the 16-sequence long-context verify 17.10 -> 16.50 ms, then
+      // 15.46-15.71 -> 15.11-15.25 ms, each on one box.)
       const int blocks = (a.n_rows + 191) / 192;
       int n_split = std::min(kWideSplitMax, std::max(1, cus / blocks));
       n_split = std::min(n_split, KS);
